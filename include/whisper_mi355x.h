@@ -1,0 +1,280 @@
+/*
+ * whisper_mi355x.h -- C ABI of the MI355X (gfx950) batched Whisper engine.
+ *
+ * The engine transcribes a batch of independent speech segments, each with
+ * its own prompt, in one multiplexed pass: the method of "Scalable Offline
+ * ASR for Command-Style Dictation in Courtrooms" (Section 2.3 and Listing 1:
+ * features per segment, padded to a 30 s window, stacked, encoded once,
+ * then generated from prompt + no-timestamps tokens), fed by a central
+ * priority queue with continuous batching over all users' segments
+ * (Section 2.2). Segments are self-contained units, so every segment's
+ * result equals the one it would get alone.
+ *
+ * Conventions for every call:
+ *  - Return value: WHISPER_OK (0) or a negative whisper_status. On error,
+ *    whisper_last_error(ctx) holds a message, and no slot state changed
+ *    (checks run before any device work), except WHISPER_E_DEVICE, after
+ *    which the context must be destroyed.
+ *  - Ownership: the caller owns every pointer it passes; inputs are only read
+ *    during the call, outputs only written during it. The context owns its
+ *    device memory (weights, caches, workspaces) and frees it on destroy.
+ *  - Host/device: pointers are host memory unless stated otherwise.
+ *  - Synchronisation: every call has finished its device work when it
+ *    returns. Work runs on the context's stream (see whisper_ctx_set_stream).
+ *  - Threads: a context is not thread-safe; use one context per thread.
+ *    Contexts are independent of each other.
+ */
+#ifndef WHISPER_MI355X_H
+#define WHISPER_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t whisper_status;
+enum {
+    WHISPER_OK = 0,
+    WHISPER_E_INVAL = -1,    /* bad argument (NULL, out of range, inconsistent) */
+    WHISPER_E_NOMEM = -2,    /* device or host allocation failed */
+    WHISPER_E_DEVICE = -3,   /* HIP runtime or kernel launch error */
+    WHISPER_E_CAPACITY = -4, /* slot index or batch beyond the context's capacity */
+    WHISPER_E_STATE = -5,    /* slot busy (encode) or idle (decode step) */
+    WHISPER_E_BUFFER = -6,   /* caller's output buffer too small */
+    WHISPER_E_FORMAT = -7    /* weight blob malformed or not matching params */
+};
+
+enum { WHISPER_DTYPE_F32 = 0, WHISPER_DTYPE_BF16 = 1 };
+
+/*
+ * Model shape and runtime options. The model fields must equal the weight
+ * blob's header (whisper_params_from_blob fills them from it).
+ *   n_mels            80 or 128 log-mel bins
+ *   n_audio_ctx       encoder positions, must be 1500 (30 s window)
+ *   n_audio_state/head/layer, n_text_state/head/layer: widths, head counts
+ *                     (head size must be 64) and layer counts; the two
+ *                     widths and head counts must be equal
+ *   n_vocab           vocabulary (output head rows)
+ *   n_text_ctx        decoder positions, must be 448
+ *   dtype             WHISPER_DTYPE_F32: fp32 storage and arithmetic;
+ *                     WHISPER_DTYPE_BF16: bf16 weights and activations, bf16
+ *                     MFMA with fp32 accumulation; layer norm, softmax, the
+ *                     residual stream and logits in fp32
+ *   max_slots         decode slots, 1..128; each holds one segment's
+ *                     self- and cross-attention caches
+ *   max_encode_batch  segments per encoder pass (workspace size), 1..max_slots;
+ *                     0 selects min(max_slots, 32); larger encode requests are
+ *                     split into passes of this size
+ *   pad_mode          0: zero-pad audio to 30 s before the transform;
+ *                     1: transform the segment alone (n/160 frames) and pad
+ *                     the normalised features with zeros to 3000 frames
+ *   refill_min        continuous batching: refill free slots from the queue
+ *                     when at least this many slots are free or fewer than
+ *                     this many are active (0 selects 16); results never
+ *                     depend on it
+ */
+typedef struct {
+    int32_t n_mels, n_audio_ctx, n_audio_state, n_audio_head, n_audio_layer;
+    int32_t n_vocab, n_text_ctx, n_text_state, n_text_head, n_text_layer;
+    int32_t dtype;
+    int32_t max_slots;
+    int32_t max_encode_batch;
+    int32_t pad_mode;
+    int32_t refill_min;
+    int32_t reserved[5];
+} whisper_params;
+
+/*
+ * One speech segment (a VAD-cut unit of 3-30 s, Section 2.1).
+ *   audio           16 kHz mono fp32 samples; host memory, or device memory
+ *                   of the context's GPU when audio_on_device is 1
+ *   n_samples       1..480000
+ *   user_id,
+ *   segment_id      echoed verbatim in the results
+ *   prompt          host array of n_prompt token ids in [0, n_vocab)
+ *   n_prompt        >= 1; n_prompt + max_new_tokens <= n_text_ctx
+ *   max_new_tokens  >= 1: exactly this many tokens are generated
+ *   arrival_us      queue priority key (whisper_batch_transcribe only)
+ */
+typedef struct {
+    const float* audio;
+    int32_t n_samples;
+    int32_t audio_on_device;
+    int64_t segment_id;
+    const int32_t* prompt;
+    int32_t n_prompt;
+    int32_t max_new_tokens;
+    int32_t user_id;
+    int32_t reserved;
+    int64_t arrival_us;
+} whisper_segment;
+
+/* Result of one input segment (results[i] belongs to segs[i]). */
+typedef struct {
+    int64_t segment_id;
+    int64_t token_offset;  /* first token in token_buf */
+    int32_t user_id;
+    int32_t status;        /* WHISPER_OK, or the error that stopped the batch */
+    int32_t n_tokens;      /* = max_new_tokens when status is WHISPER_OK */
+    int32_t reserved;
+} whisper_result;
+
+typedef struct whisper_ctx whisper_ctx;
+
+/*
+ * Weight blob (host memory): a 256-byte header, then every tensor in the
+ * canonical order below, each starting at a multiple of 256 bytes,
+ * row-major, fp32 or bf16 (header dtype), no other padding.
+ * Header (little-endian): char magic[8] = "WHSPMI01"; int32 version = 1,
+ * dtype, n_mels, n_audio_ctx, n_audio_state, n_audio_head, n_audio_layer,
+ * n_vocab, n_text_ctx, n_text_state, n_text_head, n_text_layer, n_tensors,
+ * reserved; zeros to byte 256.
+ * Canonical order (d = state, matrices are [out, in], conv [out, in, 3]):
+ *   enc.conv1.w [d, n_mels, 3], enc.conv1.b, enc.conv2.w [d, d, 3], enc.conv2.b,
+ *   per encoder layer: attn_ln.{g,b}, attn.{q.w, q.b, k.w, v.w, v.b, o.w, o.b},
+ *     mlp_ln.{g,b}, mlp.{fc1.w [4d, d], fc1.b, fc2.w [d, 4d], fc2.b},
+ *   enc.ln_post.{g,b}, dec.tok_emb [n_vocab, d], dec.pos_emb [n_text_ctx, d],
+ *   per decoder layer: attn_ln, attn (as above), cross_ln, cross (as above),
+ *     mlp_ln, mlp (as above),
+ *   dec.ln.{g,b}.
+ */
+
+/* Fills the model fields of *out from a blob header and sets the runtime
+ * options to their defaults (max_slots 32, max_encode_batch 0, pad_mode 0,
+ * refill_min 0). Returns WHISPER_E_FORMAT for a bad header. */
+whisper_status whisper_params_from_blob(const void* blob, size_t blob_bytes,
+                                        whisper_params* out);
+
+/* Creates a context on HIP device `device`: copies and repacks the weights
+ * (host blob, blob_bytes must match the layout exactly), allocates caches and
+ * workspaces. *out is set only on success. Errors: E_INVAL, E_FORMAT,
+ * E_NOMEM, E_DEVICE; whisper_last_error(NULL) then holds the message. */
+whisper_status whisper_ctx_create(const whisper_params* params, const void* weights,
+                                  size_t weights_bytes, int device, whisper_ctx** out);
+
+/* Frees everything the context owns. NULL is allowed. */
+void whisper_ctx_destroy(whisper_ctx* ctx);
+
+/* Last error message of ctx (or of the calling thread's last failed create
+ * when ctx is NULL); valid until the next call on the same context. */
+const char* whisper_last_error(const whisper_ctx* ctx);
+
+/* Runs the context's work on `hip_stream` (a hipStream_t of the context's
+ * device, e.g. torch.cuda.current_stream().cuda_stream) from now on; NULL
+ * selects the context's own stream. The stream must outlive its use. */
+whisper_status whisper_ctx_set_stream(whisper_ctx* ctx, void* hip_stream);
+
+/*
+ * Encodes n segments into the given free decode slots (slots[i] receives
+ * segs[i]; host array of n distinct indices in [0, max_slots)): log-mel
+ * front end, conv stem, encoder, and the cross-attention keys and values of
+ * every decoder layer, written into each slot's cache. The slot's
+ * self-attention cache is reset and its prompt seated; the slot is then
+ * active. n = 0 is a no-op. Errors: E_INVAL (bad segment or slot), E_STATE
+ * (a slot is active), E_CAPACITY (slot >= max_slots). Section 2.3, Listing 1
+ * (features, pad to 30 s, stack, encode).
+ */
+whisper_status whisper_batch_encode(whisper_ctx* ctx, const whisper_segment* segs, int32_t n,
+                                    const int32_t* slots);
+
+/*
+ * One greedy decoder step for each of the n active slots listed (host array,
+ * distinct): every slot feeds the token at its current position (prompt
+ * token, or the previous step's token) and advances by one position.
+ *   forced      NULL: the next input of a generating slot is this step's
+ *               argmax; else forced[i] (host) replaces it (teacher forcing)
+ *   out_tokens  NULL or n int32 (host): the argmax of this step (lowest id on
+ *               ties), or -1 while the slot is still inside its prompt
+ *   out_logits  NULL or n * n_vocab fp32 (host): this step's logits
+ * A slot whose generated count reaches max_new_tokens becomes idle; its
+ * tokens stay readable with whisper_slot_tokens until it is encoded again.
+ * n = 0 is a no-op. Errors: E_INVAL, E_STATE (slot idle). Listing 1
+ * (generate with prompt + no-timestamps tokens), greedy search.
+ */
+whisper_status whisper_batch_decode_step(whisper_ctx* ctx, const int32_t* slots, int32_t n,
+                                         const int32_t* forced, int32_t* out_tokens,
+                                         float* out_logits);
+
+/* Copies the tokens generated so far in `slot` (at most cap) to dst (host)
+ * and their count to *n_out. */
+whisper_status whisper_slot_tokens(whisper_ctx* ctx, int32_t slot, int32_t* dst, int32_t cap,
+                                   int32_t* n_out);
+
+/*
+ * Transcribes n segments with continuous batching: segments are queued by
+ * (arrival_us, user_id, segment_id, input index); free slots are refilled
+ * from the queue (encode passes of up to max_encode_batch), every active
+ * slot advances one decode step per iteration, and a slot retires when it
+ * has generated max_new_tokens tokens. Section 2.2 (central priority queue,
+ * continuous batching) and Section 2.3.
+ *   token_buf      host, token_buf_cap int32; segment i's tokens start at
+ *                  results[i].token_offset = sum of max_new_tokens of
+ *                  segments 0..i-1 (input order, independent of schedule)
+ *   results        host, n entries, results[i] describes segs[i]
+ * Errors: E_INVAL (any bad segment: nothing runs), E_BUFFER (token_buf_cap
+ * below the total; nothing runs, message states the size needed).
+ * Requires every slot to be idle on entry; leaves every slot idle.
+ */
+whisper_status whisper_batch_transcribe(whisper_ctx* ctx, const whisper_segment* segs,
+                                        int32_t n, int32_t* token_buf, int64_t token_buf_cap,
+                                        whisper_result* results);
+
+/* Tensors readable with whisper_debug_copy (test use: per-stage parity). */
+enum {
+    WHISPER_T_MEL = 0,     /* fp32 [n_mels][3000] normalised log-mel of entry `index`
+                              of the last encode pass */
+    WHISPER_T_ENC_OUT = 1, /* fp32 [1500][d] encoder output of that entry */
+    WHISPER_T_CROSS_K = 2, /* fp32 [n_text_layer][n_head][1500][64] of slot `index` */
+    WHISPER_T_CROSS_V = 3  /* same shape, values */
+};
+
+/* Copies a stage's tensor to dst (host, `bytes` must equal its size). */
+whisper_status whisper_debug_copy(whisper_ctx* ctx, int32_t tensor, int32_t index, void* dst,
+                                  size_t bytes);
+
+/* Kernels that can be timed live with HIP events (on the stream they are
+ * launched on): every launch between enable and read is bracketed. */
+enum {
+    WHISPER_K_CROSS_ATTN = 0,  /* decode-step cross-attention over the cache */
+    WHISPER_K_ENC_GEMM = 1,    /* encoder fc1 GEMM (bf16 MFMA) */
+    WHISPER_K_SELF_ATTN = 2,   /* decode-step self-attention */
+    WHISPER_K_ENC_ATTN = 3,    /* encoder attention */
+    WHISPER_K_ENC_PASS = 4,    /* a whole encode pass (front end to cross-KV) */
+    WHISPER_K_DEC_STEP = 5,    /* a whole decode step (embedding to argmax) */
+    WHISPER_K_COUNT = 6
+};
+
+/* Starts (enable = 1) or stops (0) timing of `kernel`, clearing its totals. */
+whisper_status whisper_profile_enable(whisper_ctx* ctx, int32_t kernel, int32_t enable);
+
+/* Total milliseconds and launch count of `kernel` since it was enabled
+ * (synchronises the stream). */
+whisper_status whisper_profile_read(whisper_ctx* ctx, int32_t kernel, double* total_ms,
+                                    int64_t* launches);
+
+/*
+ * Host-only check of the continuous batcher (no device work): runs the
+ * scheduler of whisper_batch_transcribe over n fake segments given by
+ * arrival_us, user_id, segment_id and max_new_tokens (n_prompt = 1) with
+ * `slots` decode slots, encode passes of up to `encode_batch` and refill
+ * threshold `refill_min`, against an engine whose token at generated index
+ * j of a segment is (segment_id * 7919 + j * 104729) mod 50000.
+ * Writes tokens (token_buf) and results as whisper_batch_transcribe would,
+ * and, if events is not NULL, the schedule: one int32 triple per engine call
+ * (kind 0 = encode, slot, input index) or (kind 1 = decode step, number of
+ * active slots, 0), at most events_cap triples, count in *n_events.
+ */
+whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const int32_t* user_id,
+                                    const int64_t* segment_id, const int32_t* max_new_tokens,
+                                    int32_t slots, int32_t encode_batch, int32_t refill_min,
+                                    int32_t* token_buf, int64_t token_buf_cap,
+                                    whisper_result* results, int32_t* events,
+                                    int32_t events_cap, int32_t* n_events);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WHISPER_MI355X_H */

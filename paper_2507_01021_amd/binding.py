@@ -1,0 +1,246 @@
+"""ctypes binding of libwhisper_mi355x.so (include/whisper_mi355x.h).
+
+Argument marshalling only: every step of the path runs inside the HIP
+library. The functions keep the C names; `Context` wraps a context for
+numpy callers. Loading fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwhisper_mi355x.so")
+
+OK, E_INVAL, E_NOMEM, E_DEVICE, E_CAPACITY, E_STATE, E_BUFFER, E_FORMAT = 0, -1, -2, -3, -4, -5, -6, -7
+DTYPE_F32, DTYPE_BF16 = 0, 1
+T_MEL, T_ENC_OUT, T_CROSS_K, T_CROSS_V = 0, 1, 2, 3
+K_CROSS_ATTN, K_ENC_GEMM, K_SELF_ATTN, K_ENC_ATTN, K_ENC_PASS, K_DEC_STEP = 0, 1, 2, 3, 4, 5
+
+EXPORTS = (
+    "whisper_params_from_blob", "whisper_ctx_create", "whisper_ctx_destroy", "whisper_last_error",
+    "whisper_ctx_set_stream", "whisper_batch_encode", "whisper_batch_decode_step",
+    "whisper_slot_tokens", "whisper_batch_transcribe", "whisper_debug_copy",
+    "whisper_profile_enable", "whisper_profile_read", "whisper_test_batcher",
+)
+
+
+class whisper_params(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in (
+        "n_mels", "n_audio_ctx", "n_audio_state", "n_audio_head", "n_audio_layer",
+        "n_vocab", "n_text_ctx", "n_text_state", "n_text_head", "n_text_layer",
+        "dtype", "max_slots", "max_encode_batch", "pad_mode", "refill_min")] + [
+        ("reserved", C.c_int32 * 5)]
+
+
+class whisper_segment(C.Structure):
+    _fields_ = [
+        ("audio", C.c_void_p), ("n_samples", C.c_int32), ("audio_on_device", C.c_int32),
+        ("segment_id", C.c_int64), ("prompt", C.POINTER(C.c_int32)), ("n_prompt", C.c_int32),
+        ("max_new_tokens", C.c_int32), ("user_id", C.c_int32), ("reserved", C.c_int32),
+        ("arrival_us", C.c_int64)]
+
+
+class whisper_result(C.Structure):
+    _fields_ = [("segment_id", C.c_int64), ("token_offset", C.c_int64), ("user_id", C.c_int32),
+                ("status", C.c_int32), ("n_tokens", C.c_int32), ("reserved", C.c_int32)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> C.CDLL:
+    """Loads the library (once). Raises if it is missing: there is no
+    fallback path."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2507_01021_amd.build`")
+    lib = C.CDLL(path)
+    i32, i64, vp, pi32 = C.c_int32, C.c_int64, C.c_void_p, C.POINTER(C.c_int32)
+    sig = {
+        "whisper_params_from_blob": (i32, [vp, C.c_size_t, C.POINTER(whisper_params)]),
+        "whisper_ctx_create": (i32, [C.POINTER(whisper_params), vp, C.c_size_t, C.c_int, C.POINTER(vp)]),
+        "whisper_ctx_destroy": (None, [vp]),
+        "whisper_last_error": (C.c_char_p, [vp]),
+        "whisper_ctx_set_stream": (i32, [vp, vp]),
+        "whisper_batch_encode": (i32, [vp, C.POINTER(whisper_segment), i32, pi32]),
+        "whisper_batch_decode_step": (i32, [vp, pi32, i32, pi32, pi32, C.POINTER(C.c_float)]),
+        "whisper_slot_tokens": (i32, [vp, i32, pi32, i32, pi32]),
+        "whisper_batch_transcribe": (i32, [vp, C.POINTER(whisper_segment), i32, pi32, i64,
+                                          C.POINTER(whisper_result)]),
+        "whisper_debug_copy": (i32, [vp, i32, i32, vp, C.c_size_t]),
+        "whisper_profile_enable": (i32, [vp, i32, i32]),
+        "whisper_profile_read": (i32, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64)]),
+        "whisper_test_batcher": (i32, [i32, C.POINTER(i64), pi32, C.POINTER(i64), pi32, i32, i32, i32,
+                                      pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+class WhisperError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(C.POINTER(ctype))
+
+
+def _check(st: int, ctx_handle=None):
+    if st != OK:
+        msg = load().whisper_last_error(ctx_handle)
+        raise WhisperError(st, msg.decode() if msg else "")
+
+
+def params_from_blob(blob: np.ndarray) -> whisper_params:
+    p = whisper_params()
+    _check(load().whisper_params_from_blob(blob.ctypes.data, blob.nbytes, C.byref(p)))
+    return p
+
+
+class _SegArray:
+    """Keeps the ctypes segment array and every buffer it points to alive."""
+
+    def __init__(self, segs, device_audio=None):
+        self.keep = []
+        self.arr = (whisper_segment * max(1, len(segs)))()
+        for i, s in enumerate(segs):
+            pr = np.ascontiguousarray(s.prompt, dtype=np.int32)
+            self.keep.append(pr)
+            e = self.arr[i]
+            if device_audio is not None:
+                e.audio = C.c_void_p(int(device_audio[i]))
+                e.audio_on_device = 1
+            else:
+                a = np.ascontiguousarray(s.audio, dtype=np.float32)
+                self.keep.append(a)
+                e.audio = C.c_void_p(a.ctypes.data)
+                e.audio_on_device = 0
+            e.n_samples = int(s.audio.size if hasattr(s.audio, "size") else len(s.audio))
+            e.segment_id = int(s.segment_id)
+            e.prompt = _ptr(pr, C.c_int32)
+            e.n_prompt = int(pr.size)
+            e.max_new_tokens = int(s.max_new_tokens)
+            e.user_id = int(s.user_id)
+            e.arrival_us = int(s.arrival_us)
+
+
+class Context:
+    """One engine context on a HIP device."""
+
+    def __init__(self, blob: np.ndarray, max_slots: int = 32, max_encode_batch: int = 0,
+                 pad_mode: int = 0, refill_min: int = 0, device: int = 0):
+        lib = load()
+        p = params_from_blob(blob)
+        p.max_slots, p.max_encode_batch, p.pad_mode, p.refill_min = (
+            max_slots, max_encode_batch, pad_mode, refill_min)
+        self.params = p
+        h = C.c_void_p()
+        _check(lib.whisper_ctx_create(C.byref(p), blob.ctypes.data, blob.nbytes, device, C.byref(h)))
+        self.h = h
+        self.n_vocab = p.n_vocab
+
+    def close(self):
+        if getattr(self, "h", None):
+            load().whisper_ctx_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def _check(self, st):
+        _check(st, self.h)
+
+    def set_stream(self, stream_handle: int | None):
+        self._check(load().whisper_ctx_set_stream(self.h, C.c_void_p(stream_handle or 0)))
+
+    def encode(self, segs, slots, device_audio=None):
+        sa = _SegArray(segs, device_audio)
+        sl = np.ascontiguousarray(slots, dtype=np.int32)
+        self._check(load().whisper_batch_encode(self.h, sa.arr, len(segs), _ptr(sl, C.c_int32)))
+
+    def decode_step(self, slots, forced=None, logits=False):
+        sl = np.ascontiguousarray(slots, dtype=np.int32)
+        n = sl.size
+        toks = np.empty(n, dtype=np.int32)
+        fo = None if forced is None else np.ascontiguousarray(forced, dtype=np.int32)
+        lg = np.empty((n, self.n_vocab), dtype=np.float32) if logits else None
+        self._check(load().whisper_batch_decode_step(
+            self.h, _ptr(sl, C.c_int32), n, None if fo is None else _ptr(fo, C.c_int32),
+            _ptr(toks, C.c_int32), None if lg is None else _ptr(lg, C.c_float)))
+        return (toks, lg) if logits else toks
+
+    def slot_tokens(self, slot: int, cap: int = 448):
+        buf = np.empty(cap, dtype=np.int32)
+        n = C.c_int32()
+        self._check(load().whisper_slot_tokens(self.h, slot, _ptr(buf, C.c_int32), cap, C.byref(n)))
+        return buf[: min(n.value, cap)].copy()
+
+    def transcribe(self, segs, device_audio=None):
+        sa = _SegArray(segs, device_audio)
+        total = sum(int(s.max_new_tokens) for s in segs)
+        buf = np.zeros(max(1, total), dtype=np.int32)
+        res = (whisper_result * max(1, len(segs)))()
+        self._check(load().whisper_batch_transcribe(self.h, sa.arr, len(segs), _ptr(buf, C.c_int32),
+                                                    buf.size, res))
+        out = []
+        for i in range(len(segs)):
+            r = res[i]
+            out.append({"user_id": r.user_id, "segment_id": r.segment_id, "status": r.status,
+                        "tokens": buf[r.token_offset: r.token_offset + r.n_tokens].copy()})
+        return out
+
+    def debug_copy(self, tensor: int, index: int, shape):
+        out = np.empty(shape, dtype=np.float32)
+        self._check(load().whisper_debug_copy(self.h, tensor, index, out.ctypes.data, out.nbytes))
+        return out
+
+    def profile_enable(self, kernel: int, on: bool = True):
+        self._check(load().whisper_profile_enable(self.h, kernel, 1 if on else 0))
+
+    def profile_read(self, kernel: int):
+        ms, n = C.c_double(), C.c_int64()
+        self._check(load().whisper_profile_read(self.h, kernel, C.byref(ms), C.byref(n)))
+        return ms.value, n.value
+
+
+def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_batch, refill_min,
+                 events_cap=100000):
+    """Runs the library's scheduler on the host with its fake engine."""
+    lib = load()
+    n = len(arrival_us)
+    a = np.ascontiguousarray(arrival_us, dtype=np.int64)
+    u = np.ascontiguousarray(user_id, dtype=np.int32)
+    s = np.ascontiguousarray(segment_id, dtype=np.int64)
+    m = np.ascontiguousarray(max_new_tokens, dtype=np.int32)
+    total = int(m.sum())
+    buf = np.zeros(max(1, total), dtype=np.int32)
+    res = (whisper_result * max(1, n))()
+    ev = np.zeros(3 * events_cap, dtype=np.int32)
+    ne = C.c_int32()
+    st = lib.whisper_test_batcher(n, _ptr(a, C.c_int64), _ptr(u, C.c_int32), _ptr(s, C.c_int64),
+                                  _ptr(m, C.c_int32), slots, encode_batch, refill_min,
+                                  _ptr(buf, C.c_int32), buf.size, res, _ptr(ev, C.c_int32),
+                                  events_cap, C.byref(ne))
+    _check(st)
+    results = [(res[i].segment_id, res[i].token_offset, res[i].user_id, res[i].status, res[i].n_tokens)
+               for i in range(n)]
+    return buf[:total], results, ev[: 3 * min(ne.value, events_cap)].reshape(-1, 3)

@@ -1,0 +1,65 @@
+#include "batcher.h"
+
+#include <algorithm>
+#include <deque>
+#include <set>
+#include <stdexcept>
+#include <tuple>
+
+namespace wmi {
+
+void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots, int encode_batch, int refill_min,
+                             const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be) {
+    if (n_slots < 1 || encode_batch < 1 || refill_min < 1) throw std::invalid_argument("batcher: bad parameters");
+    const int n = (int)segs.size();
+    std::vector<int> order(n);
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::sort(order.begin(), order.end(), [&](int a, int b) {
+        return std::make_tuple(segs[a].arrival_us, segs[a].user_id, segs[a].segment_id, a) <
+               std::make_tuple(segs[b].arrival_us, segs[b].user_id, segs[b].segment_id, b);
+    });
+    std::deque<int> queue(order.begin(), order.end());
+    std::set<int> free_slots;
+    for (int s = 0; s < n_slots; ++s) free_slots.insert(s);
+    std::vector<int> seg_of(n_slots, -1), steps_left(n_slots, 0);
+    int active = 0;
+    std::vector<int> idx, slots, list;
+    for (;;) {
+        const int nfree = n_slots - active;
+        if (!queue.empty() && nfree > 0 && (nfree >= refill_min || active < refill_min)) {
+            while (!queue.empty() && !free_slots.empty()) {
+                idx.clear();
+                slots.clear();
+                while (!queue.empty() && !free_slots.empty() && (int)idx.size() < encode_batch) {
+                    const int i = queue.front();
+                    queue.pop_front();
+                    const int s = *free_slots.begin();
+                    free_slots.erase(free_slots.begin());
+                    idx.push_back(i);
+                    slots.push_back(s);
+                    seg_of[s] = i;
+                    steps_left[s] = segs[i].n_prompt + segs[i].max_new_tokens - 1;
+                }
+                be.encode(idx.data(), (int)idx.size(), slots.data());
+                active += (int)idx.size();
+            }
+        }
+        if (active == 0) break;  // nothing active means nothing queued either
+        list.clear();
+        for (int s = 0; s < n_slots; ++s)
+            if (seg_of[s] >= 0) list.push_back(s);
+        be.step(list.data(), (int)list.size());
+        for (int s : list) {
+            if (--steps_left[s] == 0) {
+                const int i = seg_of[s];
+                be.retire(s, i, segs[i].max_new_tokens, token_buf + offsets[i]);
+                seg_of[s] = -1;
+                free_slots.insert(s);
+                --active;
+            }
+        }
+    }
+    be.finish();
+}
+
+}  // namespace wmi

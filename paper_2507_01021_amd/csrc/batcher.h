@@ -1,0 +1,47 @@
+// Continuous batcher: the central priority queue over every user's segments
+// feeding a fixed set of decode slots (Section 2.2: a central queue batches
+// segments from all active users into one shared inference pipeline, with
+// continuous batching to keep the batch full).
+//
+// Policy: segments are served in (arrival_us, user_id, segment_id, input
+// index) order. Whenever at least `refill_min` slots are free, or fewer than
+// `refill_min` are active, every free slot (lowest index first) is filled
+// from the queue, in encode passes of at most `encode_batch` segments. Every
+// active slot then advances one decode step; a slot retires after exactly
+// n_prompt + max_new_tokens - 1 steps and its tokens are copied to the
+// caller's buffer at the segment's input-order offset. Results do not depend
+// on the policy's parameters, because each segment is an independent unit.
+#pragma once
+
+#include <stdint.h>
+
+#include <vector>
+
+namespace wmi {
+
+struct QueuedSegment {
+    int64_t arrival_us;
+    int32_t user_id;
+    int64_t segment_id;
+    int32_t n_prompt;
+    int32_t max_new_tokens;
+};
+
+class BatchBackend {
+   public:
+    virtual ~BatchBackend() {}
+    // Encode segments idx[0..n) into slots[0..n).
+    virtual void encode(const int* idx, int n, const int* slots) = 0;
+    // One decode step over the listed slots (ascending).
+    virtual void step(const int* slots, int n) = 0;
+    // Slot finished segment idx: deliver its `count` tokens to dst (may be
+    // deferred until finish()).
+    virtual void retire(int slot, int idx, int count, int32_t* dst) = 0;
+    virtual void finish() = 0;
+};
+
+// Runs the whole queue; offsets[i] is segment i's first token in token_buf.
+void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots, int encode_batch, int refill_min,
+                             const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be);
+
+}  // namespace wmi

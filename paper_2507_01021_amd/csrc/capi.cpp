@@ -1,0 +1,375 @@
+// C ABI (include/whisper_mi355x.h): argument validation, slot bookkeeping,
+// error codes and messages, and the continuous-batching driver that ties the
+// batcher to the engine. Every check runs before any device work.
+#include <string.h>
+
+#include <memory>
+#include <new>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "batcher.h"
+#include "common.h"
+#include "engine.h"
+
+namespace {
+
+thread_local std::string g_create_error;
+
+struct SlotState {
+    bool active = false;
+    int n_prompt = 0, max_new = 0, steps = 0, generated = 0;
+};
+
+}  // namespace
+
+struct whisper_ctx {
+    whisper_params p;
+    std::unique_ptr<wmi::Engine> eng;
+    std::string err;
+    std::vector<SlotState> slots;
+    bool broken = false;
+};
+
+namespace {
+
+whisper_status fail(whisper_ctx* c, whisper_status code, const std::string& msg) {
+    if (c) {
+        c->err = msg;
+        if (code == WHISPER_E_DEVICE) c->broken = true;
+    } else {
+        g_create_error = msg;
+    }
+    return code;
+}
+
+template <class F>
+whisper_status guarded(whisper_ctx* c, F&& f) {
+    try {
+        return f();
+    } catch (const wmi::ArgError& e) {
+        return fail(c, e.code, e.what());
+    } catch (const wmi::DeviceError& e) {
+        return fail(c, WHISPER_E_DEVICE, e.what());
+    } catch (const std::bad_alloc&) {
+        return fail(c, WHISPER_E_NOMEM, "host allocation failed");
+    } catch (const std::exception& e) {
+        return fail(c, WHISPER_E_DEVICE, e.what());
+    }
+}
+
+std::string check_segment(const whisper_params& p, const whisper_segment& s, int i) {
+    const std::string at = "segment " + std::to_string(i) + ": ";
+    if (!s.audio) return at + "audio is NULL";
+    if (s.n_samples < 1 || s.n_samples > 480000) return at + "n_samples must be in 1..480000";
+    if (s.audio_on_device != 0 && s.audio_on_device != 1) return at + "audio_on_device must be 0 or 1";
+    if (s.n_prompt < 1 || !s.prompt) return at + "needs a prompt of at least one token";
+    if (s.max_new_tokens < 1) return at + "max_new_tokens must be >= 1";
+    if ((int64_t)s.n_prompt + s.max_new_tokens > p.n_text_ctx)
+        return at + "n_prompt + max_new_tokens exceeds the text context (" + std::to_string(p.n_text_ctx) + ")";
+    for (int k = 0; k < s.n_prompt; ++k)
+        if (s.prompt[k] < 0 || s.prompt[k] >= p.n_vocab) return at + "prompt token out of range";
+    return "";
+}
+
+std::string check_params(const whisper_params& p, const whisper_params& blob) {
+    if (p.n_mels != blob.n_mels || p.n_audio_ctx != blob.n_audio_ctx || p.n_audio_state != blob.n_audio_state ||
+        p.n_audio_head != blob.n_audio_head || p.n_audio_layer != blob.n_audio_layer || p.n_vocab != blob.n_vocab ||
+        p.n_text_ctx != blob.n_text_ctx || p.n_text_state != blob.n_text_state ||
+        p.n_text_head != blob.n_text_head || p.n_text_layer != blob.n_text_layer || p.dtype != blob.dtype)
+        return "params do not match the weight blob header";
+    if (p.dtype != WHISPER_DTYPE_F32 && p.dtype != WHISPER_DTYPE_BF16) return "dtype must be 0 (fp32) or 1 (bf16)";
+    if (p.n_audio_ctx != 1500) return "n_audio_ctx must be 1500";
+    if (p.n_text_ctx != 448) return "n_text_ctx must be 448";
+    if (p.n_audio_state != p.n_text_state || p.n_audio_head != p.n_text_head)
+        return "encoder and decoder widths and head counts must match";
+    if (p.n_audio_head < 1 || p.n_audio_state != 64 * p.n_audio_head) return "head size must be 64";
+    if (p.n_audio_state > 2048) return "width above 2048 is not supported";
+    if (p.n_mels < 4 || p.n_mels > 128 || p.n_mels % 4) return "n_mels must be a multiple of 4 in 4..128";
+    if (p.n_audio_layer < 1 || p.n_text_layer < 1 || p.n_vocab < 1) return "layer counts and vocabulary must be >= 1";
+    if (p.max_slots < 1 || p.max_slots > 128) return "max_slots must be in 1..128";
+    if (p.max_encode_batch < 0 || p.max_encode_batch > p.max_slots) return "max_encode_batch must be in 0..max_slots";
+    if (p.pad_mode != 0 && p.pad_mode != 1) return "pad_mode must be 0 or 1";
+    if (p.refill_min < 0) return "refill_min must be >= 0";
+    return "";
+}
+
+// Batch backend on a real context.
+struct EngineBackend : wmi::BatchBackend {
+    whisper_ctx* c;
+    const whisper_segment* segs;
+    std::vector<wmi::SegmentDesc> descs;
+    void encode(const int* idx, int n, const int* slots) override {
+        descs.resize(n);
+        for (int k = 0; k < n; ++k) {
+            const whisper_segment& s = segs[idx[k]];
+            descs[k] = wmi::SegmentDesc{s.audio, s.n_samples, s.audio_on_device == 1, s.prompt, s.n_prompt};
+        }
+        c->eng->encode(descs.data(), n, slots, false);
+    }
+    void step(const int* slots, int n) override { c->eng->decode_step(slots, n, nullptr, nullptr, nullptr, false); }
+    void retire(int slot, int, int count, int32_t* dst) override { c->eng->read_tokens_async(slot, count, dst); }
+    void finish() override { c->eng->finish_reads(); }
+};
+
+// Batch backend of the host-only scheduler check.
+struct FakeBackend : wmi::BatchBackend {
+    const int64_t* seg_ids;
+    std::vector<int32_t>* events;
+    void encode(const int* idx, int n, const int* slots) override {
+        for (int k = 0; k < n; ++k) events->insert(events->end(), {0, slots[k], idx[k]});
+    }
+    void step(const int*, int n) override { events->insert(events->end(), {1, n, 0}); }
+    void retire(int, int idx, int count, int32_t* dst) override {
+        for (int j = 0; j < count; ++j)
+            dst[j] = (int32_t)((uint64_t)(seg_ids[idx] * 7919 + (int64_t)j * 104729) % 50000);
+    }
+    void finish() override {}
+};
+
+std::vector<int64_t> offsets_of(const std::vector<wmi::QueuedSegment>& q, int64_t* total) {
+    std::vector<int64_t> off(q.size());
+    int64_t t = 0;
+    for (size_t i = 0; i < q.size(); ++i) { off[i] = t; t += q[i].max_new_tokens; }
+    *total = t;
+    return off;
+}
+
+}  // namespace
+
+extern "C" {
+
+whisper_status whisper_params_from_blob(const void* blob, size_t blob_bytes, whisper_params* out) {
+    if (!out) return fail(nullptr, WHISPER_E_INVAL, "out is NULL");
+    const char* why = "";
+    const int st = wmi::parse_blob_header(blob, blob_bytes, out, &why);
+    if (st != WHISPER_OK) return fail(nullptr, st, why);
+    return WHISPER_OK;
+}
+
+whisper_status whisper_ctx_create(const whisper_params* params, const void* weights, size_t weights_bytes, int device,
+                                  whisper_ctx** out) {
+    if (!params || !weights || !out) return fail(nullptr, WHISPER_E_INVAL, "params, weights and out must not be NULL");
+    whisper_params blob;
+    const char* why = "";
+    const int st = wmi::parse_blob_header(weights, weights_bytes, &blob, &why);
+    if (st != WHISPER_OK) return fail(nullptr, st, why);
+    const std::string bad = check_params(*params, blob);
+    if (!bad.empty()) return fail(nullptr, bad.find("header") != std::string::npos ? WHISPER_E_FORMAT : WHISPER_E_INVAL, bad);
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev)
+        return fail(nullptr, WHISPER_E_DEVICE, "no HIP device " + std::to_string(device));
+    whisper_params p = *params;
+    if (p.max_encode_batch == 0) p.max_encode_batch = p.max_slots < 32 ? p.max_slots : 32;
+    if (p.refill_min == 0) p.refill_min = 16;
+    std::unique_ptr<whisper_ctx> c(new (std::nothrow) whisper_ctx());
+    if (!c) return fail(nullptr, WHISPER_E_NOMEM, "host allocation failed");
+    c->p = p;
+    c->slots.resize(p.max_slots);
+    const whisper_status r = guarded(nullptr, [&]() -> whisper_status {
+        c->eng = wmi::make_engine(p, weights, weights_bytes, device);
+        return WHISPER_OK;
+    });
+    if (r != WHISPER_OK) return r;
+    *out = c.release();
+    return WHISPER_OK;
+}
+
+void whisper_ctx_destroy(whisper_ctx* ctx) { delete ctx; }
+
+const char* whisper_last_error(const whisper_ctx* ctx) {
+    return ctx ? ctx->err.c_str() : g_create_error.c_str();
+}
+
+whisper_status whisper_ctx_set_stream(whisper_ctx* ctx, void* hip_stream) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    return guarded(ctx, [&]() -> whisper_status {
+        ctx->eng->set_stream(hip_stream);
+        return WHISPER_OK;
+    });
+}
+
+whisper_status whisper_batch_encode(whisper_ctx* ctx, const whisper_segment* segs, int32_t n, const int32_t* slots) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (n < 0) return fail(ctx, WHISPER_E_INVAL, "n must be >= 0");
+    if (n == 0) return WHISPER_OK;
+    if (!segs || !slots) return fail(ctx, WHISPER_E_INVAL, "segs and slots must not be NULL");
+    std::set<int> seen;
+    for (int i = 0; i < n; ++i) {
+        const std::string bad = check_segment(ctx->p, segs[i], i);
+        if (!bad.empty()) return fail(ctx, WHISPER_E_INVAL, bad);
+        if (slots[i] < 0 || slots[i] >= ctx->p.max_slots)
+            return fail(ctx, WHISPER_E_CAPACITY, "slot " + std::to_string(slots[i]) + " outside 0..max_slots-1");
+        if (!seen.insert(slots[i]).second) return fail(ctx, WHISPER_E_INVAL, "slots must be distinct");
+        if (ctx->slots[slots[i]].active)
+            return fail(ctx, WHISPER_E_STATE, "slot " + std::to_string(slots[i]) + " is active");
+    }
+    return guarded(ctx, [&]() -> whisper_status {
+        std::vector<wmi::SegmentDesc> d(n);
+        for (int i = 0; i < n; ++i)
+            d[i] = wmi::SegmentDesc{segs[i].audio, segs[i].n_samples, segs[i].audio_on_device == 1, segs[i].prompt,
+                                    segs[i].n_prompt};
+        ctx->eng->encode(d.data(), n, slots, true);
+        for (int i = 0; i < n; ++i) {
+            SlotState& s = ctx->slots[slots[i]];
+            s.active = true;
+            s.n_prompt = segs[i].n_prompt;
+            s.max_new = segs[i].max_new_tokens;
+            s.steps = 0;
+            s.generated = 0;
+        }
+        return WHISPER_OK;
+    });
+}
+
+whisper_status whisper_batch_decode_step(whisper_ctx* ctx, const int32_t* slots, int32_t n, const int32_t* forced,
+                                         int32_t* out_tokens, float* out_logits) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (n < 0 || n > ctx->p.max_slots) return fail(ctx, WHISPER_E_INVAL, "n must be in 0..max_slots");
+    if (n == 0) return WHISPER_OK;
+    if (!slots) return fail(ctx, WHISPER_E_INVAL, "slots must not be NULL");
+    std::set<int> seen;
+    for (int i = 0; i < n; ++i) {
+        if (slots[i] < 0 || slots[i] >= ctx->p.max_slots)
+            return fail(ctx, WHISPER_E_CAPACITY, "slot " + std::to_string(slots[i]) + " outside 0..max_slots-1");
+        if (!seen.insert(slots[i]).second) return fail(ctx, WHISPER_E_INVAL, "slots must be distinct");
+        if (!ctx->slots[slots[i]].active)
+            return fail(ctx, WHISPER_E_STATE, "slot " + std::to_string(slots[i]) + " is idle");
+        if (forced && (forced[i] < 0 || forced[i] >= ctx->p.n_vocab))
+            return fail(ctx, WHISPER_E_INVAL, "forced token out of range");
+    }
+    return guarded(ctx, [&]() -> whisper_status {
+        ctx->eng->decode_step(slots, n, forced, out_tokens, out_logits, true);
+        for (int i = 0; i < n; ++i) {
+            SlotState& s = ctx->slots[slots[i]];
+            if (s.steps >= s.n_prompt - 1) s.generated++;
+            s.steps++;
+            if (s.generated == s.max_new) s.active = false;
+        }
+        return WHISPER_OK;
+    });
+}
+
+whisper_status whisper_slot_tokens(whisper_ctx* ctx, int32_t slot, int32_t* dst, int32_t cap, int32_t* n_out) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (slot < 0 || slot >= ctx->p.max_slots) return fail(ctx, WHISPER_E_CAPACITY, "slot outside 0..max_slots-1");
+    if (!n_out || (cap > 0 && !dst) || cap < 0) return fail(ctx, WHISPER_E_INVAL, "bad output buffer");
+    const int g = ctx->slots[slot].generated;
+    const int k = g < cap ? g : cap;
+    return guarded(ctx, [&]() -> whisper_status {
+        ctx->eng->read_tokens(slot, k, dst);
+        *n_out = g;
+        return WHISPER_OK;
+    });
+}
+
+whisper_status whisper_batch_transcribe(whisper_ctx* ctx, const whisper_segment* segs, int32_t n, int32_t* token_buf,
+                                        int64_t token_buf_cap, whisper_result* results) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (n < 0) return fail(ctx, WHISPER_E_INVAL, "n must be >= 0");
+    if (n == 0) return WHISPER_OK;
+    if (!segs || !results) return fail(ctx, WHISPER_E_INVAL, "segs and results must not be NULL");
+    for (auto& s : ctx->slots)
+        if (s.active) return fail(ctx, WHISPER_E_STATE, "transcribe needs every slot idle");
+    std::vector<wmi::QueuedSegment> q(n);
+    for (int i = 0; i < n; ++i) {
+        const std::string bad = check_segment(ctx->p, segs[i], i);
+        if (!bad.empty()) return fail(ctx, WHISPER_E_INVAL, bad);
+        q[i] = wmi::QueuedSegment{segs[i].arrival_us, segs[i].user_id, segs[i].segment_id, segs[i].n_prompt,
+                                  segs[i].max_new_tokens};
+    }
+    int64_t total = 0;
+    const std::vector<int64_t> off = offsets_of(q, &total);
+    if (!token_buf || token_buf_cap < total)
+        return fail(ctx, WHISPER_E_BUFFER, "token_buf needs " + std::to_string(total) + " entries");
+    for (int i = 0; i < n; ++i)
+        results[i] = whisper_result{segs[i].segment_id, off[i], segs[i].user_id, WHISPER_OK, segs[i].max_new_tokens, 0};
+    const whisper_status r = guarded(ctx, [&]() -> whisper_status {
+        EngineBackend be;
+        be.c = ctx;
+        be.segs = segs;
+        wmi::run_continuous_batching(q, ctx->p.max_slots, ctx->p.max_encode_batch, ctx->p.refill_min, off, token_buf,
+                                     be);
+        return WHISPER_OK;
+    });
+    for (auto& s : ctx->slots) s = SlotState();
+    if (r != WHISPER_OK)
+        for (int i = 0; i < n; ++i) { results[i].status = r; results[i].n_tokens = 0; }
+    return r;
+}
+
+whisper_status whisper_debug_copy(whisper_ctx* ctx, int32_t tensor, int32_t index, void* dst, size_t bytes) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (!dst) return fail(ctx, WHISPER_E_INVAL, "dst is NULL");
+    return guarded(ctx, [&]() -> whisper_status {
+        ctx->eng->debug_copy(tensor, index, dst, bytes);
+        return WHISPER_OK;
+    });
+}
+
+whisper_status whisper_profile_enable(whisper_ctx* ctx, int32_t kernel, int32_t enable) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (kernel < 0 || kernel >= WHISPER_K_COUNT) return fail(ctx, WHISPER_E_INVAL, "unknown kernel id");
+    return guarded(ctx, [&]() -> whisper_status {
+        ctx->eng->profile_enable(kernel, enable != 0);
+        return WHISPER_OK;
+    });
+}
+
+whisper_status whisper_profile_read(whisper_ctx* ctx, int32_t kernel, double* total_ms, int64_t* launches) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (kernel < 0 || kernel >= WHISPER_K_COUNT || !total_ms || !launches)
+        return fail(ctx, WHISPER_E_INVAL, "unknown kernel id or NULL output");
+    return guarded(ctx, [&]() -> whisper_status {
+        ctx->eng->profile_read(kernel, total_ms, launches);
+        return WHISPER_OK;
+    });
+}
+
+whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const int32_t* user_id,
+                                    const int64_t* segment_id, const int32_t* max_new_tokens, int32_t slots,
+                                    int32_t encode_batch, int32_t refill_min, int32_t* token_buf,
+                                    int64_t token_buf_cap, whisper_result* results, int32_t* events,
+                                    int32_t events_cap, int32_t* n_events) {
+    if (n < 0 || (n > 0 && (!arrival_us || !user_id || !segment_id || !max_new_tokens || !results)))
+        return fail(nullptr, WHISPER_E_INVAL, "bad arguments");
+    if (slots < 1 || encode_batch < 1 || refill_min < 1)
+        return fail(nullptr, WHISPER_E_INVAL, "slots, encode_batch and refill_min must be >= 1");
+    std::vector<wmi::QueuedSegment> q(n);
+    for (int i = 0; i < n; ++i) {
+        if (max_new_tokens[i] < 1) return fail(nullptr, WHISPER_E_INVAL, "max_new_tokens must be >= 1");
+        q[i] = wmi::QueuedSegment{arrival_us[i], user_id[i], segment_id[i], 1, max_new_tokens[i]};
+    }
+    int64_t total = 0;
+    const std::vector<int64_t> off = offsets_of(q, &total);
+    if ((total > 0 && !token_buf) || token_buf_cap < total)
+        return fail(nullptr, WHISPER_E_BUFFER, "token_buf needs " + std::to_string(total) + " entries");
+    std::vector<int32_t> ev;
+    FakeBackend be;
+    be.seg_ids = segment_id;
+    be.events = &ev;
+    try {
+        wmi::run_continuous_batching(q, slots, encode_batch, refill_min, off, token_buf, be);
+    } catch (const std::exception& e) {
+        return fail(nullptr, WHISPER_E_INVAL, e.what());
+    }
+    for (int i = 0; i < n; ++i)
+        results[i] = whisper_result{segment_id[i], off[i], user_id[i], WHISPER_OK, max_new_tokens[i], 0};
+    if (n_events) *n_events = (int32_t)(ev.size() / 3);
+    if (events) {
+        const size_t k = ev.size() < (size_t)events_cap * 3 ? ev.size() : (size_t)events_cap * 3;
+        memcpy(events, ev.data(), k * sizeof(int32_t));
+    }
+    return WHISPER_OK;
+}
+
+}  // extern "C"

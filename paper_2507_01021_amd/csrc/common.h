@@ -1,0 +1,116 @@
+// Shared device helpers for the gfx950 kernels: bf16 storage type,
+// conversions, vector types, wavefront reductions, error checks.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <stdexcept>
+#include <string>
+
+namespace wmi {
+
+// bf16 as raw bits; arithmetic always happens in fp32.
+struct bf16 {
+    uint16_t x;
+};
+
+__host__ __device__ inline float bf2f(bf16 v) {
+    union { uint32_t u; float f; } c;
+    c.u = (uint32_t)v.x << 16;
+    return c.f;
+}
+
+// fp32 -> bf16, round to nearest even (finite inputs; NaN stays NaN).
+__host__ __device__ inline bf16 f2bf(float f) {
+    union { uint32_t u; float f; } c;
+    c.f = f;
+    uint32_t u = c.u;
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x7fffffu)) {
+        bf16 r; r.x = (uint16_t)((u >> 16) | 0x40); return r;
+    }
+    u += 0x7fffu + ((u >> 16) & 1u);
+    bf16 r; r.x = (uint16_t)(u >> 16);
+    return r;
+}
+
+// Storage-type traits: load as fp32, store from fp32.
+template <class T> struct St;
+template <> struct St<float> {
+    __device__ static inline float ld(const float* p) { return *p; }
+    __device__ static inline void st(float* p, float v) { *p = v; }
+};
+template <> struct St<bf16> {
+    __device__ static inline float ld(const bf16* p) { return bf2f(*p); }
+    __device__ static inline void st(bf16* p, float v) { *p = f2bf(v); }
+};
+
+template <class T> __device__ inline float ldf(const T* p) { return St<T>::ld(p); }
+template <class T> __device__ inline void stf(T* p, float v) { St<T>::st(p, v); }
+
+// Native vectors (plain loads/stores; HIP's uint4 struct copies as memcpy).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+// Four consecutive elements, stored with one 8-byte (bf16) or 16-byte (fp32) access.
+__device__ inline void st4(float* p, float a, float b, float c, float d) {
+    *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+__device__ inline void st4(bf16* p, float a, float b, float c, float d) {
+    uint32_t lo = (uint32_t)f2bf(a).x | ((uint32_t)f2bf(b).x << 16);
+    uint32_t hi = (uint32_t)f2bf(c).x | ((uint32_t)f2bf(d).x << 16);
+    *reinterpret_cast<u32x2*>(p) = u32x2{lo, hi};
+}
+__device__ inline float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ inline float4 ld4(const bf16* p) {
+    const u32x2 u = *reinterpret_cast<const u32x2*>(p);
+    union { uint32_t u; float f; } a, b, c, d;
+    a.u = u.x << 16; b.u = u.x & 0xffff0000u; c.u = u.y << 16; d.u = u.y & 0xffff0000u;
+    return make_float4(a.f, b.f, c.f, d.f);
+}
+
+__device__ inline float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+__device__ inline float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// Order-preserving map of fp32 to uint32 (for atomic max of floats).
+__device__ inline uint32_t f2ord(float f) {
+    uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ inline float ord2f(uint32_t o) {
+    uint32_t u = (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o;
+    return __uint_as_float(u);
+}
+
+// MFMA operand vectors.
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4;
+
+}  // namespace wmi
+
+#define WMI_HIP(call)                                                                  \
+    do {                                                                               \
+        hipError_t e_ = (call);                                                        \
+        if (e_ != hipSuccess)                                                          \
+            throw ::wmi::DeviceError(std::string(#call) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+namespace wmi {
+struct DeviceError : std::runtime_error {
+    using std::runtime_error::runtime_error;
+};
+struct ArgError : std::runtime_error {
+    int code;
+    ArgError(int c, const std::string& m) : std::runtime_error(m), code(c) {}
+};
+}  // namespace wmi

@@ -1,0 +1,53 @@
+// Engine interface (host side, no HIP types): owns the device weights, the
+// per-slot decoder caches and state, and the encoder workspace of one
+// context, and runs encode passes and decode steps on the context's stream.
+// Argument validation happens in the C ABI layer before anything here runs.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <memory>
+
+#include "../../include/whisper_mi355x.h"
+
+namespace wmi {
+
+struct SegmentDesc {
+    const float* audio;
+    int n_samples;
+    bool on_device;
+    const int32_t* prompt;
+    int n_prompt;
+};
+
+class Engine {
+   public:
+    virtual ~Engine() {}
+    virtual void set_stream(void* hip_stream) = 0;
+    // Encodes n segments into the given slots (seating prompts). sync = false
+    // leaves the work queued on the stream.
+    virtual void encode(const SegmentDesc* segs, int n, const int* slots, bool sync) = 0;
+    // One decode step for n slots; optional teacher forcing / outputs (host).
+    // sync = false leaves the work queued (outputs must then be null).
+    virtual void decode_step(const int* slots, int n, const int* forced, int* out_tok, float* out_logits,
+                             bool sync) = 0;
+    // Copies gen[slot][0..count) to host dst (synchronous).
+    virtual void read_tokens(int slot, int count, int32_t* dst) = 0;
+    // Queues a copy of gen[slot][0..count) into host memory owned by the
+    // engine; finish_reads() waits and delivers every queued copy to dst.
+    virtual void read_tokens_async(int slot, int count, int32_t* dst) = 0;
+    virtual void finish_reads() = 0;
+    virtual void sync() = 0;
+    virtual void debug_copy(int tensor, int index, void* dst, size_t bytes) = 0;
+    virtual void profile_enable(int kernel, bool on) = 0;
+    virtual void profile_read(int kernel, double* ms, int64_t* launches) = 0;
+};
+
+// Throws ArgError (code = whisper_status) or DeviceError.
+std::unique_ptr<Engine> make_engine(const whisper_params& p, const void* blob, size_t bytes, int device);
+
+// Blob header check; fills the model fields of *out. Returns a whisper_status.
+int parse_blob_header(const void* blob, size_t bytes, whisper_params* out, const char** why);
+
+}  // namespace wmi

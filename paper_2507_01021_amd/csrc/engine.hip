@@ -1,0 +1,724 @@
+// Engine: device weights, caches and workspaces of one context, and the
+// encode pass / decode step that drive the kernels on the context's stream.
+//
+// Encode pass (Listing 1: features per segment, pad to 30 s, stack, encode):
+//   audio -> reflect-padded window -> DFT power (SIMT GEMM, window folded
+//   into the basis) -> mel projection + log10 -> per-segment max and
+//   normalisation -> conv stem (two implicit-im2col GEMMs over overlapping
+//   rows) -> encoder layers (LN, QK and V projections, attention, output
+//   projection + residual, LN, fc1 + GELU, fc2 + residual) -> final LN ->
+//   cross-attention keys and values of every decoder layer written straight
+//   into the slots' caches -> prompts seated.
+// Decode step (greedy generate, one token per active slot):
+//   embedding -> per layer: LN, fused QKV projection appending this position
+//   to the self-attention cache, self-attention over the slot's positions,
+//   output projection + residual, LN, cross query, cross-attention over the
+//   1500 cached encoder positions (chunked + combine), output projection +
+//   residual, LN, fc1 + GELU, fc2 + residual -> final LN -> logits against
+//   the token embedding -> argmax, next input, position advance.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <map>
+#include <type_traits>
+#include <string>
+#include <vector>
+
+#include "engine.h"
+#include "kernels.h"
+
+namespace wmi {
+
+// ------------------------------------------------------------------ blob
+
+struct TensorSpec {
+    std::string name;
+    std::vector<long long> shape;
+    long long numel() const {
+        long long n = 1;
+        for (auto s : shape) n *= s;
+        return n;
+    }
+};
+
+static void add_attn(std::vector<TensorSpec>& v, const std::string& p, long long d) {
+    v.push_back({p + ".q.w", {d, d}});
+    v.push_back({p + ".q.b", {d}});
+    v.push_back({p + ".k.w", {d, d}});
+    v.push_back({p + ".v.w", {d, d}});
+    v.push_back({p + ".v.b", {d}});
+    v.push_back({p + ".o.w", {d, d}});
+    v.push_back({p + ".o.b", {d}});
+}
+static void add_ln(std::vector<TensorSpec>& v, const std::string& p, long long d) {
+    v.push_back({p + ".g", {d}});
+    v.push_back({p + ".b", {d}});
+}
+static void add_mlp(std::vector<TensorSpec>& v, const std::string& p, long long d) {
+    v.push_back({p + ".fc1.w", {4 * d, d}});
+    v.push_back({p + ".fc1.b", {4 * d}});
+    v.push_back({p + ".fc2.w", {d, 4 * d}});
+    v.push_back({p + ".fc2.b", {d}});
+}
+
+static std::vector<TensorSpec> canonical_specs(const whisper_params& p) {
+    const long long d = p.n_audio_state;
+    std::vector<TensorSpec> v;
+    v.push_back({"enc.conv1.w", {d, p.n_mels, 3}});
+    v.push_back({"enc.conv1.b", {d}});
+    v.push_back({"enc.conv2.w", {d, d, 3}});
+    v.push_back({"enc.conv2.b", {d}});
+    for (int i = 0; i < p.n_audio_layer; ++i) {
+        const std::string q = "enc." + std::to_string(i);
+        add_ln(v, q + ".attn_ln", d);
+        add_attn(v, q + ".attn", d);
+        add_ln(v, q + ".mlp_ln", d);
+        add_mlp(v, q + ".mlp", d);
+    }
+    add_ln(v, "enc.ln_post", d);
+    v.push_back({"dec.tok_emb", {p.n_vocab, d}});
+    v.push_back({"dec.pos_emb", {p.n_text_ctx, d}});
+    for (int i = 0; i < p.n_text_layer; ++i) {
+        const std::string q = "dec." + std::to_string(i);
+        add_ln(v, q + ".attn_ln", d);
+        add_attn(v, q + ".attn", d);
+        add_ln(v, q + ".cross_ln", d);
+        add_attn(v, q + ".cross", d);
+        add_ln(v, q + ".mlp_ln", d);
+        add_mlp(v, q + ".mlp", d);
+    }
+    add_ln(v, "dec.ln", d);
+    return v;
+}
+
+static size_t blob_size(const whisper_params& p, std::map<std::string, std::pair<size_t, long long>>* offs) {
+    const size_t esz = p.dtype == WHISPER_DTYPE_F32 ? 4 : 2;
+    size_t off = 256;
+    for (auto& t : canonical_specs(p)) {
+        if (offs) (*offs)[t.name] = {off, t.numel()};
+        off += (size_t)t.numel() * esz;
+        off = (off + 255) / 256 * 256;
+    }
+    return off;
+}
+
+int parse_blob_header(const void* blob, size_t bytes, whisper_params* out, const char** why) {
+    if (!blob || bytes < 256) { *why = "blob shorter than its 256-byte header"; return WHISPER_E_FORMAT; }
+    const char* b = static_cast<const char*>(blob);
+    if (memcmp(b, "WHSPMI01", 8) != 0) { *why = "bad blob magic"; return WHISPER_E_FORMAT; }
+    int32_t h[14];
+    memcpy(h, b + 8, sizeof(h));
+    if (h[0] != 1) { *why = "unsupported blob version"; return WHISPER_E_FORMAT; }
+    whisper_params p;
+    memset(&p, 0, sizeof(p));
+    p.dtype = h[1];
+    p.n_mels = h[2]; p.n_audio_ctx = h[3]; p.n_audio_state = h[4]; p.n_audio_head = h[5];
+    p.n_audio_layer = h[6]; p.n_vocab = h[7]; p.n_text_ctx = h[8]; p.n_text_state = h[9];
+    p.n_text_head = h[10]; p.n_text_layer = h[11];
+    p.max_slots = 32;
+    *out = p;
+    return WHISPER_OK;
+}
+
+// ------------------------------------------------------------------ tables (host, double)
+
+constexpr double kPi = 3.14159265358979323846;
+
+static std::vector<float> dft_basis() {  // [404][400]: rows 2k, 2k+1 = w cos, w sin of bin k
+    std::vector<float> b(404 * 400, 0.f);
+    for (int k = 0; k <= 200; ++k)
+        for (int n = 0; n < 400; ++n) {
+            const double w = 0.5 - 0.5 * cos(2.0 * kPi * n / 400.0);
+            const double ang = 2.0 * kPi * (double)((k * n) % 400) / 400.0;
+            b[(2 * k) * 400 + n] = (float)(w * cos(ang));
+            b[(2 * k + 1) * 400 + n] = (float)(w * sin(ang));
+        }
+    return b;
+}
+
+static double slaney_mel(double f) {
+    return f < 1000.0 ? 3.0 * f / 200.0 : 15.0 + log(f / 1000.0) / (log(6.4) / 27.0);
+}
+static double slaney_hz(double m) {
+    return m < 15.0 ? 200.0 * m / 3.0 : 1000.0 * exp((m - 15.0) * (log(6.4) / 27.0));
+}
+
+static std::vector<float> mel_bank(int nm) {  // [nm][201]
+    std::vector<double> edges(nm + 2);
+    const double top = slaney_mel(8000.0);
+    for (int i = 0; i < nm + 2; ++i) edges[i] = slaney_hz(top * i / (nm + 1));
+    std::vector<float> fb((size_t)nm * 201);
+    for (int i = 0; i < nm; ++i)
+        for (int k = 0; k < 201; ++k) {
+            const double f = 40.0 * k;
+            const double up = (f - edges[i]) / (edges[i + 1] - edges[i]);
+            const double down = (edges[i + 2] - f) / (edges[i + 2] - edges[i + 1]);
+            const double tri = std::max(0.0, std::min(up, down));
+            fb[(size_t)i * 201 + k] = (float)(tri * 2.0 / (edges[i + 2] - edges[i]));
+        }
+    return fb;
+}
+
+static std::vector<float> sinusoids(int T, int d) {  // [T][d]
+    std::vector<float> pe((size_t)T * d);
+    const int half = d / 2;
+    const double inc = log(10000.0) / (half - 1);
+    for (int t = 0; t < T; ++t)
+        for (int j = 0; j < half; ++j) {
+            const double a = t * exp(-inc * j);
+            pe[(size_t)t * d + j] = (float)sin(a);
+            pe[(size_t)t * d + half + j] = (float)cos(a);
+        }
+    return pe;
+}
+
+// ------------------------------------------------------------------ engine
+
+template <class T> struct HostElem;
+template <> struct HostElem<float> { static float to_f(const void* p, long long i) { return static_cast<const float*>(p)[i]; } };
+template <> struct HostElem<bf16> {
+    static float to_f(const void* p, long long i) { bf16 v; v.x = static_cast<const uint16_t*>(p)[i]; return bf2f(v); }
+};
+
+template <class T>
+struct EncLayerW {
+    float *ln1g, *ln1b, *bq, *bv, *bo, *ln2g, *ln2b, *b1, *b2;
+    T *Wqk, *Wv, *Wo, *W1, *W2;
+};
+template <class T>
+struct DecLayerW {
+    float *ln1g, *ln1b, *bq, *bv, *bo, *ln2g, *ln2b, *cbq, *cbo, *ln3g, *ln3b, *b1, *b2;
+    T *Wqkv, *Wo, *Wcq, *Wco, *W1, *W2;
+};
+
+constexpr int CROSS_CHUNKS = (N_CTX + 255) / 256;
+
+template <class T>
+class EngineT final : public Engine {
+   public:
+    EngineT(const whisper_params& p, const void* blob, size_t bytes, int device)
+        : P_(p), dev_(device) {
+        d_ = p.n_audio_state; H_ = p.n_audio_head; Le_ = p.n_audio_layer; Ld_ = p.n_text_layer;
+        V_ = p.n_vocab; nm_ = p.n_mels; S_ = p.max_slots;
+        EB_ = p.max_encode_batch;
+        WMI_HIP(hipSetDevice(dev_));
+        WMI_HIP(hipStreamCreateWithFlags(&own_stream_, hipStreamNonBlocking));
+        st_ = own_stream_;
+        load_weights(blob, bytes);
+        alloc_state();
+        WMI_HIP(hipDeviceSynchronize());
+    }
+
+    ~EngineT() override {
+        (void)hipSetDevice(dev_);
+        if (st_) (void)hipStreamSynchronize(st_);
+        for (auto& pr : prof_)
+            for (auto& e : pr.used) { (void)hipEventDestroy(e.first); (void)hipEventDestroy(e.second); }
+        for (auto e : event_pool_) (void)hipEventDestroy(e);
+        for (auto& s : stage_) {
+            if (s.ev) (void)hipEventDestroy(s.ev);
+            if (s.host) (void)hipHostFree(s.host);
+        }
+        if (tokpin_) (void)hipHostFree(tokpin_);
+        for (void* q : allocs_) (void)hipFree(q);
+        if (own_stream_) (void)hipStreamDestroy(own_stream_);
+    }
+
+    void set_stream(void* s) override {
+        WMI_HIP(hipStreamSynchronize(st_));
+        st_ = s ? static_cast<hipStream_t>(s) : own_stream_;
+    }
+
+    void sync() override { WMI_HIP(hipStreamSynchronize(st_)); }
+
+    // -------------------------------------------------------------- encode
+    void encode(const SegmentDesc* segs, int n, const int* slots, bool sync_) override {
+        WMI_HIP(hipSetDevice(dev_));
+        for (int s0 = 0; s0 < n; s0 += EB_) encode_pass(segs + s0, std::min(EB_, n - s0), slots + s0);
+        WMI_HIP(hipGetLastError());
+        if (sync_) WMI_HIP(hipStreamSynchronize(st_));
+    }
+
+    // -------------------------------------------------------------- decode step
+    void decode_step(const int* slots, int n, const int* forced, int* out_tok, float* out_logits,
+                     bool sync_) override {
+        WMI_HIP(hipSetDevice(dev_));
+        if (n != (int)list_host_.size() || !std::equal(slots, slots + n, list_host_.begin())) {
+            list_host_.assign(slots, slots + n);
+            upload(0, list_, slots, n * sizeof(int));
+        }
+        if (forced) upload(1, forced_, forced, n * sizeof(int));
+        const int d = d_;
+        prof_begin(WHISPER_K_DEC_STEP);
+        hipLaunchKernelGGL(embed_kernel<T>, dim3(n), dim3(256), 0, st_, tok_emb_, pos_emb_, list_, pos_, seq_, dx_, d);
+        for (int l = 0; l < Ld_; ++l) {
+            const DecLayerW<T>& L = dec_[l];
+            const long long sl = (long long)l * S_ * H_ * 64;
+            ln(dx_, dz_, L.ln1g, L.ln1b, n);
+            proj(L.Wqkv, 3 * d, dz_, n, d,
+                 EpiDecQKV<T>{L.bq, L.bv, dq_, kts_ + sl * TS, vs_ + sl * TS, list_, pos_, d, H_});
+            DecAttnArgs sa{dq_, kts_ + sl * TS, vs_ + sl * TS, datt_, part_, list_, pos_, 0, TS, H_, d, 1};
+            prof_begin(WHISPER_K_SELF_ATTN);
+            hipLaunchKernelGGL((dec_attn_kernel<T, 8>), dim3(1, H_, n), dim3(64), 0, st_, sa);
+            prof_end(WHISPER_K_SELF_ATTN);
+            proj(L.Wo, d, datt_, n, d, EpiResid{L.bo, dx_, d});
+            ln(dx_, dz_, L.ln2g, L.ln2b, n);
+            proj(L.Wcq, d, dz_, n, d, EpiQ<T>{L.cbq, dq_, d});
+            DecAttnArgs ca{dq_, ktc_ + sl * TC, vc_ + sl * TC, datt_, part_, list_, nullptr, N_CTX, TC, H_, d,
+                           CROSS_CHUNKS};
+            prof_begin(WHISPER_K_CROSS_ATTN);
+            hipLaunchKernelGGL((dec_attn_kernel<T, 4>), dim3(CROSS_CHUNKS, H_, n), dim3(64), 0, st_, ca);
+            prof_end(WHISPER_K_CROSS_ATTN);
+            hipLaunchKernelGGL(dec_attn_combine_kernel<T>, dim3(H_, n), dim3(64), 0, st_, part_, datt_, H_, d,
+                               CROSS_CHUNKS);
+            proj(L.Wco, d, datt_, n, d, EpiResid{L.cbo, dx_, d});
+            ln(dx_, dz_, L.ln3g, L.ln3b, n);
+            proj(L.W1, 4 * d, dz_, n, d, EpiGelu<T>{L.b1, dh_, 4 * d});
+            proj(L.W2, d, dh_, n, 4 * d, EpiResid{L.b2, dx_, d});
+        }
+        ln(dx_, dz_, lnfg_, lnfb_, n);
+        proj(tok_emb_, V_, dz_, n, d, EpiLogits{logits_, V_});
+        hipLaunchKernelGGL(argmax_step_kernel, dim3(n), dim3(256), 0, st_, logits_, V_, list_, pos_, npr_, seq_, gen_,
+                           forced ? forced_ : nullptr, outtok_);
+        prof_end(WHISPER_K_DEC_STEP);
+        WMI_HIP(hipGetLastError());
+        if (out_tok) WMI_HIP(hipMemcpyAsync(out_tok, outtok_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
+        if (out_logits)
+            WMI_HIP(hipMemcpyAsync(out_logits, logits_, (size_t)n * V_ * sizeof(float), hipMemcpyDeviceToHost, st_));
+        if (sync_ || out_tok || out_logits || forced) WMI_HIP(hipStreamSynchronize(st_));
+    }
+
+    void read_tokens(int slot, int count, int32_t* dst) override {
+        WMI_HIP(hipSetDevice(dev_));
+        if (count <= 0) return;
+        WMI_HIP(hipMemcpyAsync(dst, gen_ + (size_t)slot * 448, count * sizeof(int), hipMemcpyDeviceToHost, st_));
+        WMI_HIP(hipStreamSynchronize(st_));
+    }
+
+    void read_tokens_async(int slot, int count, int32_t* dst) override {
+        if (count <= 0) return;
+        if (tokpin_used_ + count > tokpin_cap_) {
+            finish_reads();
+            if ((size_t)count > tokpin_cap_) {
+                if (tokpin_) WMI_HIP(hipHostFree(tokpin_));
+                tokpin_ = nullptr;
+                tokpin_cap_ = std::max<size_t>(count, 1 << 16);
+                WMI_HIP(hipHostMalloc(reinterpret_cast<void**>(&tokpin_), tokpin_cap_ * sizeof(int)));
+            }
+        }
+        WMI_HIP(hipMemcpyAsync(tokpin_ + tokpin_used_, gen_ + (size_t)slot * 448, count * sizeof(int),
+                               hipMemcpyDeviceToHost, st_));
+        pending_.push_back({tokpin_used_, count, dst});
+        tokpin_used_ += count;
+    }
+
+    void finish_reads() override {
+        WMI_HIP(hipStreamSynchronize(st_));
+        for (auto& r : pending_) memcpy(r.dst, tokpin_ + r.off, r.count * sizeof(int));
+        pending_.clear();
+        tokpin_used_ = 0;
+    }
+
+    // -------------------------------------------------------------- debug
+    void debug_copy(int tensor, int index, void* dst, size_t bytes) override {
+        WMI_HIP(hipSetDevice(dev_));
+        WMI_HIP(hipStreamSynchronize(st_));
+        float* out = static_cast<float*>(dst);
+        if (tensor == WHISPER_T_MEL) {
+            need(bytes, (size_t)nm_ * 3000 * 4, index < last_nb_);
+            std::vector<float> h((size_t)3000 * nm_);
+            WMI_HIP(hipMemcpy(h.data(), logmel_ + (size_t)index * 3000 * nm_, h.size() * 4, hipMemcpyDeviceToHost));
+            for (int f = 0; f < 3000; ++f)
+                for (int c = 0; c < nm_; ++c) out[(size_t)c * 3000 + f] = h[(size_t)f * nm_ + c];
+        } else if (tensor == WHISPER_T_ENC_OUT) {
+            need(bytes, (size_t)N_CTX * d_ * 4, index < last_nb_);
+            std::vector<T> h((size_t)N_CTX * d_);
+            WMI_HIP(hipMemcpy(h.data(), zb_ + (size_t)index * N_CTX * d_, h.size() * sizeof(T), hipMemcpyDeviceToHost));
+            for (size_t i = 0; i < h.size(); ++i) out[i] = HostElem<T>::to_f(h.data(), i);
+        } else if (tensor == WHISPER_T_CROSS_K || tensor == WHISPER_T_CROSS_V) {
+            need(bytes, (size_t)Ld_ * H_ * N_CTX * 64 * 4, index < S_);
+            std::vector<T> h((size_t)H_ * 64 * TC);
+            for (int l = 0; l < Ld_; ++l) {
+                const size_t base = (((size_t)l * S_ + index) * H_) * 64 * TC;
+                WMI_HIP(hipMemcpy(h.data(), (tensor == WHISPER_T_CROSS_K ? ktc_ : vc_) + base, h.size() * sizeof(T),
+                                  hipMemcpyDeviceToHost));
+                for (int hh = 0; hh < H_; ++hh)
+                    for (int t = 0; t < N_CTX; ++t)
+                        for (int j = 0; j < 64; ++j) {
+                            const size_t src = tensor == WHISPER_T_CROSS_K ? ((size_t)hh * 64 + j) * TC + t
+                                                                          : ((size_t)hh * TC + t) * 64 + j;
+                            out[(((size_t)l * H_ + hh) * N_CTX + t) * 64 + j] = HostElem<T>::to_f(h.data(), src);
+                        }
+            }
+        } else {
+            throw ArgError(WHISPER_E_INVAL, "unknown debug tensor");
+        }
+    }
+
+    // -------------------------------------------------------------- profiling
+    void profile_enable(int k, bool on) override {
+        WMI_HIP(hipStreamSynchronize(st_));
+        recycle(k);
+        prof_[k].on = on;
+        prof_[k].total_ms = 0.0;
+        prof_[k].launches = 0;
+    }
+    void profile_read(int k, double* ms, int64_t* launches) override {
+        WMI_HIP(hipStreamSynchronize(st_));
+        recycle(k);
+        *ms = prof_[k].total_ms;
+        *launches = prof_[k].launches;
+    }
+
+   private:
+    struct Prof {
+        bool on = false;
+        hipEvent_t open = nullptr;
+        std::vector<std::pair<hipEvent_t, hipEvent_t>> used;
+        double total_ms = 0.0;
+        int64_t launches = 0;
+    };
+    struct Stage {
+        void* host = nullptr;
+        size_t cap = 0;
+        hipEvent_t ev = nullptr;
+    };
+    struct PendingRead {
+        size_t off;
+        int count;
+        int32_t* dst;
+    };
+
+    whisper_params P_;
+    int dev_;
+    int d_, H_, Le_, Ld_, V_, nm_, S_, EB_;
+    hipStream_t own_stream_ = nullptr, st_ = nullptr;
+    std::vector<void*> allocs_;
+
+    // weights
+    T *W1r_, *W2r_, *tok_emb_, *pos_emb_, *WcK_, *WcV_;
+    float *cb1_, *cb2_, *lnpg_, *lnpb_, *lnfg_, *lnfb_, *bcV_;
+    std::vector<EncLayerW<T>> enc_;
+    std::vector<DecLayerW<T>> dec_;
+    float *basis_, *melfb_, *pe_;
+    // encoder workspace
+    float *stage_audio_, *xpad_, *power_, *logmel_, *x_;
+    SegSrc* segsrc_;
+    int *nvalid_, *slot_of_, *seat_np_, *seat_prompts_;
+    T *ypad_, *h1_, *zb_, *qh_, *kh_, *vt_, *ob_, *hb_;
+    int last_nb_ = 0;
+    // decoder state and workspace
+    int *seq_, *gen_, *pos_, *npr_, *list_, *forced_, *outtok_;
+    T *kts_, *vs_, *ktc_, *vc_, *dz_, *dq_, *datt_, *dh_;
+    float *dx_, *logits_, *part_;
+    std::vector<int> list_host_;
+    // host staging
+    Stage stage_[3];
+    int32_t* tokpin_ = nullptr;
+    size_t tokpin_cap_ = 0, tokpin_used_ = 0;
+    std::vector<PendingRead> pending_;
+    Prof prof_[WHISPER_K_COUNT];
+    std::vector<hipEvent_t> event_pool_;
+
+    template <class U>
+    U* dalloc(size_t count) {
+        void* q = nullptr;
+        if (hipMalloc(&q, std::max<size_t>(count, 1) * sizeof(U)) != hipSuccess)
+            throw ArgError(WHISPER_E_NOMEM, "device allocation of " + std::to_string(count * sizeof(U)) + " bytes failed");
+        allocs_.push_back(q);
+        WMI_HIP(hipMemset(q, 0, std::max<size_t>(count, 1) * sizeof(U)));
+        return static_cast<U*>(q);
+    }
+    template <class U>
+    U* upload_new(const std::vector<U>& h) {
+        U* q = dalloc<U>(h.size());
+        WMI_HIP(hipMemcpy(q, h.data(), h.size() * sizeof(U), hipMemcpyHostToDevice));
+        return q;
+    }
+
+    // Copies host bytes to device memory through pinned staging area `which`
+    // (waits for the previous copy from that area first).
+    void upload(int which, void* dst, const void* src, size_t bytes) {
+        Stage& s = stage_[which];
+        if (s.ev) WMI_HIP(hipEventSynchronize(s.ev));
+        else WMI_HIP(hipEventCreateWithFlags(&s.ev, hipEventDisableTiming));
+        if (bytes > s.cap) {
+            if (s.host) WMI_HIP(hipHostFree(s.host));
+            s.host = nullptr;
+            s.cap = std::max<size_t>(bytes, 4096);
+            WMI_HIP(hipHostMalloc(&s.host, s.cap));
+        }
+        memcpy(s.host, src, bytes);
+        WMI_HIP(hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, st_));
+        WMI_HIP(hipEventRecord(s.ev, st_));
+    }
+
+    hipEvent_t get_event() {
+        if (!event_pool_.empty()) { hipEvent_t e = event_pool_.back(); event_pool_.pop_back(); return e; }
+        hipEvent_t e;
+        WMI_HIP(hipEventCreate(&e));
+        return e;
+    }
+    void prof_begin(int k) {
+        if (!prof_[k].on) return;
+        prof_[k].open = get_event();
+        WMI_HIP(hipEventRecord(prof_[k].open, st_));
+    }
+    void prof_end(int k) {
+        if (!prof_[k].on) return;
+        hipEvent_t e = get_event();
+        WMI_HIP(hipEventRecord(e, st_));
+        prof_[k].used.push_back({prof_[k].open, e});
+        if (prof_[k].used.size() >= 4096) {  // bound the number of live events
+            WMI_HIP(hipStreamSynchronize(st_));
+            recycle(k);
+        }
+    }
+    void recycle(int k) {
+        for (auto& pr : prof_[k].used) {
+            float ms = 0.f;
+            WMI_HIP(hipEventElapsedTime(&ms, pr.first, pr.second));
+            prof_[k].total_ms += ms;
+            prof_[k].launches += 1;
+            event_pool_.push_back(pr.first);
+            event_pool_.push_back(pr.second);
+        }
+        prof_[k].used.clear();
+    }
+
+    static void need(size_t got, size_t want, bool index_ok) {
+        if (!index_ok) throw ArgError(WHISPER_E_INVAL, "debug_copy: index out of range");
+        if (got != want)
+            throw ArgError(WHISPER_E_BUFFER, "debug_copy: buffer must hold exactly " + std::to_string(want) + " bytes");
+    }
+
+    // -------------------------------------------------------------- kernels
+    void ln(const float* x, T* y, const float* g, const float* b, int rows) {
+        hipLaunchKernelGGL(layer_norm_kernel<T>, dim3((rows + 3) / 4), dim3(256), 0, st_, x, y, g, b, rows, d_);
+    }
+
+    template <class Epi>
+    void gemm(const T* A, int lda, long long sA, const T* B, int ldb, long long sB, int MA, int MB, int K, int batch,
+              const Epi& epi) {
+        if constexpr (std::is_same<T, bf16>::value) gemm_bf16(A, lda, sA, B, ldb, sB, MA, MB, K, batch, epi, st_);
+        else gemm_simt(A, lda, sA, B, ldb, sB, MA, MB, K, batch, epi, st_);
+    }
+
+    // decode projection: rows = weight rows (MA), n activation rows of width K
+    template <class Epi>
+    void proj(const T* W, int MA, const T* X, int n, int K, const Epi& epi) {
+        if constexpr (std::is_same<T, bf16>::value) skinny_bf16(W, MA, X, n, K, epi, st_);
+        else gemm_simt(W, K, 0, X, K, 0, MA, n, K, 1, epi, st_);
+    }
+
+    void encode_pass(const SegmentDesc* segs, int nb, const int* slots) {
+        const int d = d_, M = nb * N_CTX;
+        // small per-pass arrays: sources, valid frames, slots, prompts
+        std::vector<SegSrc> src(nb);
+        std::vector<int> small((size_t)nb * (3 + 448), 0);  // nvalid | slot_of | n_prompt | prompts
+        int* nv = small.data();
+        int* so = nv + nb;
+        int* npv = so + nb;
+        int* pr = npv + nb;
+        for (int i = 0; i < nb; ++i) {
+            const SegmentDesc& s = segs[i];
+            if (s.on_device) {
+                src[i] = SegSrc{s.audio, s.n_samples, 0};
+            } else {
+                float* dst = stage_audio_ + (size_t)i * 480000;
+                WMI_HIP(hipMemcpyAsync(dst, s.audio, (size_t)s.n_samples * 4, hipMemcpyHostToDevice, st_));
+                src[i] = SegSrc{dst, s.n_samples, 0};
+            }
+            nv[i] = P_.pad_mode == 0 ? 3000 : s.n_samples / 160;
+            so[i] = slots[i];
+            npv[i] = s.n_prompt;
+            memcpy(pr + (size_t)i * 448, s.prompt, s.n_prompt * sizeof(int));
+        }
+        upload(2, segsrc_, src.data(), nb * sizeof(SegSrc));
+        // the three int arrays and prompts live contiguously behind nvalid_
+        WMI_HIP(hipEventSynchronize(stage_[2].ev));
+        upload(2, nvalid_, small.data(), small.size() * sizeof(int));
+        last_nb_ = nb;
+
+        prof_begin(WHISPER_K_ENC_PASS);
+        hipLaunchKernelGGL(prep_audio_kernel, dim3((480400 + 255) / 256, nb), dim3(256), 0, st_, segsrc_, xpad_,
+                           P_.pad_mode);
+        gemm_simt(basis_, 400, 0, xpad_, 160, 480400, 404, 3000, 400, nb, EpiPower{power_}, st_);
+        gemm_simt(melfb_, 201, 0, power_, 201, 0, nm_, nb * 3000, 201, 1, EpiLogMel{logmel_, nm_}, st_);
+        hipLaunchKernelGGL(mel_norm_kernel<T>, dim3(nb), dim3(1024), 0, st_, logmel_, ypad_, nvalid_, nm_);
+        gemm(W1r_, 3 * CP, 0, ypad_, CP, 3002LL * CP, d, 3000, 3 * CP, nb, EpiConv1<T>{cb1_, h1_, d});
+        gemm(W2r_, 3 * d, 0, h1_, 2 * d, 3002LL * d, d, N_CTX, 3 * d, nb, EpiConv2{cb2_, pe_, x_, d});
+        for (int l = 0; l < Le_; ++l) {
+            const EncLayerW<T>& L = enc_[l];
+            ln(x_, zb_, L.ln1g, L.ln1b, M);
+            gemm(L.Wqk, d, 0, zb_, d, 0, 2 * d, M, d, 1, EpiQK<T>{L.bq, qh_, kh_, d, H_});
+            gemm(zb_, d, 0, L.Wv, d, 0, M, d, d, 1, EpiVt<T>{L.bv, vt_, H_});
+            prof_begin(WHISPER_K_ENC_ATTN);
+            if constexpr (std::is_same<T, bf16>::value)
+                hipLaunchKernelGGL(enc_attn_bf16_kernel, dim3((N_CTX + ea::QB - 1) / ea::QB, nb * H_), dim3(256), 0,
+                                   st_, qh_, kh_, vt_, ob_, H_, d);
+            else
+                hipLaunchKernelGGL(enc_attn_f32_kernel, dim3((N_CTX + 63) / 64, nb * H_), dim3(64), 0, st_, qh_, kh_,
+                                   vt_, ob_, H_, d);
+            prof_end(WHISPER_K_ENC_ATTN);
+            gemm(L.Wo, d, 0, ob_, d, 0, d, M, d, 1, EpiResid{L.bo, x_, d});
+            ln(x_, zb_, L.ln2g, L.ln2b, M);
+            prof_begin(WHISPER_K_ENC_GEMM);
+            gemm(L.W1, d, 0, zb_, d, 0, 4 * d, M, d, 1, EpiGelu<T>{L.b1, hb_, 4 * d});
+            prof_end(WHISPER_K_ENC_GEMM);
+            gemm(L.W2, 4 * d, 0, hb_, 4 * d, 0, d, M, 4 * d, 1, EpiResid{L.b2, x_, d});
+        }
+        ln(x_, zb_, lnpg_, lnpb_, M);
+        gemm(zb_, d, 0, WcK_, d, 0, M, Ld_ * d, d, 1, EpiCrossK<T>{ktc_, slot_of_, d, H_, S_});
+        gemm(WcV_, d, 0, zb_, d, 0, Ld_ * d, M, d, 1, EpiCrossV<T>{bcV_, vc_, slot_of_, d, H_, S_});
+        hipLaunchKernelGGL(seat_kernel, dim3(nb), dim3(256), 0, st_, slot_of_, seat_np_, seat_prompts_, seq_, pos_, npr_);
+        prof_end(WHISPER_K_ENC_PASS);
+    }
+
+    // -------------------------------------------------------------- setup
+    void load_weights(const void* blob, size_t bytes) {
+        std::map<std::string, std::pair<size_t, long long>> offs;
+        const size_t want = blob_size(P_, &offs);
+        if (bytes != want)
+            throw ArgError(WHISPER_E_FORMAT, "weight blob has " + std::to_string(bytes) + " bytes, layout needs " +
+                                                 std::to_string(want));
+        const char* base = static_cast<const char*>(blob);
+        auto raw = [&](const std::string& name) -> const T* {
+            return reinterpret_cast<const T*>(base + offs.at(name).first);
+        };
+        auto count = [&](const std::string& name) { return (size_t)offs.at(name).second; };
+        auto mat = [&](const std::string& name) -> T* {
+            T* q = dalloc<T>(count(name));
+            WMI_HIP(hipMemcpy(q, raw(name), count(name) * sizeof(T), hipMemcpyHostToDevice));
+            return q;
+        };
+        auto vecf = [&](const std::string& name) -> float* {
+            std::vector<float> h(count(name));
+            for (size_t i = 0; i < h.size(); ++i) h[i] = HostElem<T>::to_f(raw(name), i);
+            return upload_new(h);
+        };
+        auto cat = [&](const std::vector<std::string>& names) -> T* {
+            size_t tot = 0;
+            for (auto& nme : names) tot += count(nme);
+            T* q = dalloc<T>(tot);
+            size_t o = 0;
+            for (auto& nme : names) {
+                WMI_HIP(hipMemcpy(q + o, raw(nme), count(nme) * sizeof(T), hipMemcpyHostToDevice));
+                o += count(nme);
+            }
+            return q;
+        };
+        const int d = d_;
+        {  // conv kernels to [out][tap][in] (input channels of conv1 padded to CP)
+            std::vector<T> w1((size_t)d * 3 * CP);
+            memset(w1.data(), 0, w1.size() * sizeof(T));
+            const T* s1 = raw("enc.conv1.w");
+            for (int o = 0; o < d; ++o)
+                for (int c = 0; c < nm_; ++c)
+                    for (int t = 0; t < 3; ++t) w1[(size_t)o * 3 * CP + t * CP + c] = s1[((size_t)o * nm_ + c) * 3 + t];
+            W1r_ = upload_new(w1);
+            std::vector<T> w2((size_t)d * 3 * d);
+            const T* s2 = raw("enc.conv2.w");
+            for (int o = 0; o < d; ++o)
+                for (int c = 0; c < d; ++c)
+                    for (int t = 0; t < 3; ++t) w2[(size_t)o * 3 * d + t * d + c] = s2[((size_t)o * d + c) * 3 + t];
+            W2r_ = upload_new(w2);
+        }
+        cb1_ = vecf("enc.conv1.b");
+        cb2_ = vecf("enc.conv2.b");
+        for (int i = 0; i < Le_; ++i) {
+            const std::string p = "enc." + std::to_string(i);
+            EncLayerW<T> L;
+            L.ln1g = vecf(p + ".attn_ln.g"); L.ln1b = vecf(p + ".attn_ln.b");
+            L.Wqk = cat({p + ".attn.q.w", p + ".attn.k.w"});
+            L.bq = vecf(p + ".attn.q.b");
+            L.Wv = mat(p + ".attn.v.w"); L.bv = vecf(p + ".attn.v.b");
+            L.Wo = mat(p + ".attn.o.w"); L.bo = vecf(p + ".attn.o.b");
+            L.ln2g = vecf(p + ".mlp_ln.g"); L.ln2b = vecf(p + ".mlp_ln.b");
+            L.W1 = mat(p + ".mlp.fc1.w"); L.b1 = vecf(p + ".mlp.fc1.b");
+            L.W2 = mat(p + ".mlp.fc2.w"); L.b2 = vecf(p + ".mlp.fc2.b");
+            enc_.push_back(L);
+        }
+        lnpg_ = vecf("enc.ln_post.g");
+        lnpb_ = vecf("enc.ln_post.b");
+        tok_emb_ = mat("dec.tok_emb");
+        pos_emb_ = mat("dec.pos_emb");
+        std::vector<std::string> ck, cv;
+        std::vector<float> bcv;
+        for (int i = 0; i < Ld_; ++i) {
+            const std::string p = "dec." + std::to_string(i);
+            DecLayerW<T> L;
+            L.ln1g = vecf(p + ".attn_ln.g"); L.ln1b = vecf(p + ".attn_ln.b");
+            L.Wqkv = cat({p + ".attn.q.w", p + ".attn.k.w", p + ".attn.v.w"});
+            L.bq = vecf(p + ".attn.q.b"); L.bv = vecf(p + ".attn.v.b");
+            L.Wo = mat(p + ".attn.o.w"); L.bo = vecf(p + ".attn.o.b");
+            L.ln2g = vecf(p + ".cross_ln.g"); L.ln2b = vecf(p + ".cross_ln.b");
+            L.Wcq = mat(p + ".cross.q.w"); L.cbq = vecf(p + ".cross.q.b");
+            L.Wco = mat(p + ".cross.o.w"); L.cbo = vecf(p + ".cross.o.b");
+            L.ln3g = vecf(p + ".mlp_ln.g"); L.ln3b = vecf(p + ".mlp_ln.b");
+            L.W1 = mat(p + ".mlp.fc1.w"); L.b1 = vecf(p + ".mlp.fc1.b");
+            L.W2 = mat(p + ".mlp.fc2.w"); L.b2 = vecf(p + ".mlp.fc2.b");
+            dec_.push_back(L);
+            ck.push_back(p + ".cross.k.w");
+            cv.push_back(p + ".cross.v.w");
+            const T* b = raw(p + ".cross.v.b");
+            for (int j = 0; j < d; ++j) bcv.push_back(HostElem<T>::to_f(b, j));
+        }
+        WcK_ = cat(ck);
+        WcV_ = cat(cv);
+        bcV_ = upload_new(bcv);
+        lnfg_ = vecf("dec.ln.g");
+        lnfb_ = vecf("dec.ln.b");
+        basis_ = upload_new(dft_basis());
+        melfb_ = upload_new(mel_bank(nm_));
+        pe_ = upload_new(sinusoids(N_CTX, d));
+    }
+
+    void alloc_state() {
+        const size_t d = d_, H = H_, EB = EB_, S = S_, Ld = Ld_;
+        stage_audio_ = dalloc<float>(EB * 480000);
+        segsrc_ = dalloc<SegSrc>(EB);
+        nvalid_ = dalloc<int>(EB * (3 + 448));
+        slot_of_ = nvalid_ + EB;
+        seat_np_ = slot_of_ + EB;
+        seat_prompts_ = seat_np_ + EB;
+        xpad_ = dalloc<float>(EB * 480400);
+        power_ = dalloc<float>(EB * 3000 * 201);
+        logmel_ = dalloc<float>(EB * 3000 * nm_);
+        ypad_ = dalloc<T>(EB * 3002 * CP);
+        h1_ = dalloc<T>(EB * 3002 * d);
+        x_ = dalloc<float>(EB * N_CTX * d);
+        zb_ = dalloc<T>(EB * N_CTX * d);
+        qh_ = dalloc<T>(EB * H * TQ * 64);
+        kh_ = dalloc<T>(EB * H * TQ * 64);
+        vt_ = dalloc<T>(EB * H * 64 * TQ);
+        ob_ = dalloc<T>(EB * N_CTX * d);
+        hb_ = dalloc<T>(EB * N_CTX * 4 * d);
+        seq_ = dalloc<int>(S * 448);
+        gen_ = dalloc<int>(S * 448);
+        pos_ = dalloc<int>(S);
+        npr_ = dalloc<int>(S);
+        list_ = dalloc<int>(S);
+        forced_ = dalloc<int>(S);
+        outtok_ = dalloc<int>(S);
+        kts_ = dalloc<T>(Ld * S * H * 64 * TS);
+        vs_ = dalloc<T>(Ld * S * H * TS * 64);
+        ktc_ = dalloc<T>(Ld * S * H * 64 * TC);
+        vc_ = dalloc<T>(Ld * S * H * TC * 64);
+        dx_ = dalloc<float>(S * d);
+        dz_ = dalloc<T>(S * d);
+        dq_ = dalloc<T>(S * d);
+        datt_ = dalloc<T>(S * d);
+        dh_ = dalloc<T>(S * 4 * d);
+        logits_ = dalloc<float>(S * (size_t)V_);
+        part_ = dalloc<float>(S * H * CROSS_CHUNKS * 66);
+    }
+};
+
+std::unique_ptr<Engine> make_engine(const whisper_params& p, const void* blob, size_t bytes, int device) {
+    if (p.dtype == WHISPER_DTYPE_BF16) return std::unique_ptr<Engine>(new EngineT<bf16>(p, blob, bytes, device));
+    return std::unique_ptr<Engine>(new EngineT<float>(p, blob, bytes, device));
+}
+
+}  // namespace wmi

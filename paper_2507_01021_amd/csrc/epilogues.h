@@ -1,0 +1,221 @@
+// GEMM epilogues: each receives four consecutive output rows i0..i0+3 (the
+// A-operand dimension) of column j in batch z and writes them where the next
+// stage reads them. All biases and norms are fp32; T is the activation
+// storage type (float or bf16).
+//
+// Encoder buffers (nb segments, token m = z * 1500 + t):
+//   Ypad  [nb][3002][128]   normalised log-mel, row 1 + frame, zero rows 0 and 3001
+//   H1pad [nb][3002][d]     first conv output, row 1 + t, zero row 0
+//   x     [nb * 1500][d]    fp32 residual stream
+//   Qh,Kh [nb][H][TQ][64]   per-head queries (scaled by 1/8) and keys
+//   Vt    [nb][H][64][TQ]   per-head values, transposed
+// Decoder caches (slot s, layer l, head h):
+//   self  Kt [l][s][h][64][TS], V [l][s][h][TS][64]
+//   cross Kt [l][s][h][64][TC], V [l][s][h][TC][64]
+#pragma once
+
+#include "common.h"
+
+namespace wmi {
+
+constexpr int N_CTX = 1500;  // encoder positions of a 30 s window
+constexpr int TQ = 1536;     // padded encoder positions per head
+constexpr int TS = 512;      // self-attention cache stride (>= 448)
+constexpr int TC = 1536;     // cross-attention cache stride (>= 1500)
+constexpr int CP = 128;      // padded mel channels of the conv input
+
+// DFT -> power: rows (2k, 2k+1) are the cosine and sine parts of bin k.
+struct EpiPower {
+    float* power;  // [batch * 3000][201]
+    __device__ void operator()(int i, int j, int z, float a, float b, float c, float d) const {
+        const int k = i >> 1;
+        float* p = power + ((long long)z * 3000 + j) * 201 + k;
+        p[0] = a * a + b * b;
+        if (k + 1 < 201) p[1] = c * c + d * d;
+    }
+};
+
+// Mel projection -> log10 with floor 1e-10. out [rows][n_mels].
+struct EpiLogMel {
+    float* out;
+    int n_mels;
+    __device__ void operator()(int i, int j, int, float a, float b, float c, float d) const {
+        st4(out + (long long)j * n_mels + i, log10f(fmaxf(a, 1e-10f)), log10f(fmaxf(b, 1e-10f)),
+            log10f(fmaxf(c, 1e-10f)), log10f(fmaxf(d, 1e-10f)));
+    }
+};
+
+template <class T>
+struct EpiConv1 {  // i = channel, j = frame
+    const float* bias;
+    T* h1;  // H1pad
+    int d;
+    __device__ void operator()(int i, int j, int z, float a, float b, float c, float e) const {
+        const float* bb = bias + i;
+        st4(h1 + ((long long)z * 3002 + j + 1) * d + i, gelu_erf(a + bb[0]), gelu_erf(b + bb[1]),
+            gelu_erf(c + bb[2]), gelu_erf(e + bb[3]));
+    }
+};
+
+struct EpiConv2 {  // i = channel, j = position; adds the sinusoid table
+    const float* bias;
+    const float* pe;  // [1500][d]
+    float* x;
+    int d;
+    __device__ void operator()(int i, int j, int z, float a, float b, float c, float e) const {
+        const float* bb = bias + i;
+        const float4 p = ld4(pe + (long long)j * d + i);
+        st4(x + ((long long)z * N_CTX + j) * d + i, gelu_erf(a + bb[0]) + p.x, gelu_erf(b + bb[1]) + p.y,
+            gelu_erf(c + bb[2]) + p.z, gelu_erf(e + bb[3]) + p.w);
+    }
+};
+
+template <class T>
+struct EpiQK {  // A = [Wq; Wk] (2d rows), B = tokens
+    const float* bq;
+    T* q;
+    T* k;
+    int d, H;
+    __device__ void operator()(int i, int m, int, float a, float b, float c, float e) const {
+        const int bseg = m / N_CTX, t = m - bseg * N_CTX;
+        if (i < d) {
+            const int h = i >> 6, jj = i & 63;
+            const float* bb = bq + i;
+            st4(q + (((long long)bseg * H + h) * TQ + t) * 64 + jj, (a + bb[0]) * 0.125f,
+                (b + bb[1]) * 0.125f, (c + bb[2]) * 0.125f, (e + bb[3]) * 0.125f);
+        } else {
+            const int f = i - d, h = f >> 6, jj = f & 63;
+            st4(k + (((long long)bseg * H + h) * TQ + t) * 64 + jj, a, b, c, e);
+        }
+    }
+};
+
+template <class T>
+struct EpiVt {  // A = tokens (4 consecutive positions), B = Wv
+    const float* bv;
+    T* vt;
+    int H;
+    __device__ void operator()(int m, int f, int, float a, float b, float c, float e) const {
+        const int bseg = m / N_CTX, t = m - bseg * N_CTX;
+        const int h = f >> 6, jj = f & 63;
+        const float bb = bv[f];
+        st4(vt + (((long long)bseg * H + h) * 64 + jj) * TQ + t, a + bb, b + bb, c + bb, e + bb);
+    }
+};
+
+struct EpiResid {  // x[j][i..i+3] += v + bias
+    const float* bias;
+    float* x;
+    int ld;
+    __device__ void operator()(int i, int j, int, float a, float b, float c, float e) const {
+        float* p = x + (long long)j * ld + i;
+        const float4 o = ld4(p);
+        const float* bb = bias + i;
+        st4(p, o.x + a + bb[0], o.y + b + bb[1], o.z + c + bb[2], o.w + e + bb[3]);
+    }
+};
+
+template <class T>
+struct EpiGelu {  // out[j][i..i+3] = gelu(v + bias)
+    const float* bias;
+    T* out;
+    int ld;
+    __device__ void operator()(int i, int j, int, float a, float b, float c, float e) const {
+        const float* bb = bias + i;
+        st4(out + (long long)j * ld + i, gelu_erf(a + bb[0]), gelu_erf(b + bb[1]), gelu_erf(c + bb[2]),
+            gelu_erf(e + bb[3]));
+    }
+};
+
+template <class T>
+struct EpiCrossK {  // A = encoder output (4 consecutive positions), B = [Wk of every layer]
+    T* kt;               // cross K cache
+    const int* slot_of;  // batch entry -> slot
+    int d, H, S;
+    __device__ void operator()(int m, int n, int, float a, float b, float c, float e) const {
+        const int bseg = m / N_CTX, t = m - bseg * N_CTX;
+        const int l = n / d, f = n - l * d, h = f >> 6, jj = f & 63;
+        const long long base = (((long long)l * S + slot_of[bseg]) * H + h) * 64 + jj;
+        st4(kt + base * TC + t, a, b, c, e);
+    }
+};
+
+template <class T>
+struct EpiCrossV {  // A = [Wv of every layer], B = encoder output
+    const float* bv;  // [L * d]
+    T* v;             // cross V cache
+    const int* slot_of;
+    int d, H, S;
+    __device__ void operator()(int n, int m, int, float a, float b, float c, float e) const {
+        const int bseg = m / N_CTX, t = m - bseg * N_CTX;
+        const int l = n / d, f = n - l * d, h = f >> 6, jj = f & 63;
+        const long long row = (((long long)l * S + slot_of[bseg]) * H + h) * TC + t;
+        const float* bb = bv + n;
+        st4(v + row * 64 + jj, a + bb[0], b + bb[1], c + bb[2], e + bb[3]);
+    }
+};
+
+// Decoder: A = [Wq; Wk; Wv] of one layer, B = normalised rows (row r -> slot list[r]).
+// Queries go to q (scaled by 1/8); this position's key and value are appended
+// to the slot's self-attention cache.
+template <class T>
+struct EpiDecQKV {
+    const float* bq;
+    const float* bv;
+    T* q;
+    T* kt;  // self K cache of this layer: [S][H][64][TS]
+    T* v;   // self V cache of this layer: [S][H][TS][64]
+    const int* list;
+    const int* pos;
+    int d, H;
+    __device__ void operator()(int i, int r, int, float a, float b, float c, float e) const {
+        if (i < d) {
+            const float* bb = bq + i;
+            st4(q + (long long)r * d + i, (a + bb[0]) * 0.125f, (b + bb[1]) * 0.125f,
+                (c + bb[2]) * 0.125f, (e + bb[3]) * 0.125f);
+            return;
+        }
+        const int s = list[r], p = pos[s];
+        if (i < 2 * d) {
+            const int f = i - d, h = f >> 6, jj = f & 63;
+            T* base = kt + (((long long)s * H + h) * 64 + jj) * TS + p;
+            stf(base, a);
+            stf(base + TS, b);
+            stf(base + 2 * TS, c);
+            stf(base + 3 * TS, e);
+        } else {
+            const int f = i - 2 * d, h = f >> 6, jj = f & 63;
+            const float* bb = bv + f;
+            st4(v + (((long long)s * H + h) * TS + p) * 64 + jj, a + bb[0], b + bb[1], c + bb[2], e + bb[3]);
+        }
+    }
+};
+
+template <class T>
+struct EpiQ {  // cross-attention queries, scaled by 1/8
+    const float* bias;
+    T* q;
+    int d;
+    __device__ void operator()(int i, int r, int, float a, float b, float c, float e) const {
+        const float* bb = bias + i;
+        st4(q + (long long)r * d + i, (a + bb[0]) * 0.125f, (b + bb[1]) * 0.125f, (c + bb[2]) * 0.125f,
+            (e + bb[3]) * 0.125f);
+    }
+};
+
+struct EpiLogits {  // out[r][i..i+3] (fp32), rows beyond n_vocab dropped
+    float* out;
+    int V;
+    __device__ void operator()(int i, int r, int, float a, float b, float c, float e) const {
+        float* p = out + (long long)r * V + i;
+        if (i + 3 < V) {
+            p[0] = a; p[1] = b; p[2] = c; p[3] = e;
+        } else {
+            if (i < V) p[0] = a;
+            if (i + 1 < V) p[1] = b;
+            if (i + 2 < V) p[2] = c;
+        }
+    }
+};
+
+}  // namespace wmi

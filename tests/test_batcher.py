@@ -1,0 +1,105 @@
+"""The continuous batcher (central priority queue + slot refill, Section
+2.2), run inside the library against its host-only fake engine and checked
+against a brute-force simulation of the same policy."""
+import os
+
+import numpy as np
+import pytest
+
+from paper_2507_01021_amd import binding, synth
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        pytest.skip("library not built")
+    return binding.load()
+
+
+def fake_tokens(seg_id, n):
+    return [(seg_id * 7919 + j * 104729) % 50000 for j in range(n)]
+
+
+def simulate(arrival, user, seg, new, slots, eb, R):
+    """Brute force: every engine call the policy makes, in order."""
+    n = len(arrival)
+    queue = sorted(range(n), key=lambda i: (arrival[i], user[i], seg[i], i))
+    free = list(range(slots))
+    seg_of = [-1] * slots
+    left = [0] * slots
+    events = []
+    while True:
+        active = slots - len(free)
+        if queue and free and (len(free) >= R or active < R):
+            while queue and free:
+                k = 0
+                while queue and free and k < eb:
+                    i = queue.pop(0)
+                    s = min(free)
+                    free.remove(s)
+                    seg_of[s], left[s] = i, 1 + new[i] - 1
+                    events.append((0, s, i))
+                    k += 1
+        active = slots - len(free)
+        if active == 0:
+            break
+        lst = [s for s in range(slots) if seg_of[s] >= 0]
+        events.append((1, len(lst), 0))
+        for s in lst:
+            left[s] -= 1
+            if left[s] == 0:
+                seg_of[s] = -1
+                free.append(s)
+    return events
+
+
+def workload(n, users, seed):
+    segs = synth.poisson_users(synth.TINY, users, n, 5.0, 1, 9, seed=seed) if n else []
+    return ([s.arrival_us for s in segs], [s.user_id for s in segs], [s.segment_id for s in segs],
+            [s.max_new_tokens for s in segs])
+
+
+@pytest.mark.parametrize("n,users,slots,eb,R", [(1, 1, 1, 1, 1), (7, 2, 3, 2, 1), (40, 8, 8, 3, 4),
+                                               (64, 8, 16, 16, 16), (30, 5, 40, 7, 16)])
+def test_schedule_matches_bruteforce(lib, n, users, slots, eb, R):
+    a, u, s, m = workload(n, users, seed=n)
+    toks, res, ev = binding.test_batcher(a, u, s, m, slots, eb, R)
+    assert [tuple(e) for e in ev] == simulate(a, u, s, m, slots, eb, R)
+    off = np.concatenate([[0], np.cumsum(m)[:-1]])
+    for i in range(n):
+        assert res[i] == (s[i], off[i], u[i], 0, m[i])
+        assert list(toks[off[i]: off[i] + m[i]]) == fake_tokens(s[i], m[i])
+
+
+def test_every_segment_served_once_and_results_independent_of_policy(lib):
+    a, u, s, m = workload(50, 6, seed=3)
+    ref = None
+    for slots, eb, R in [(1, 1, 1), (4, 2, 2), (16, 16, 16), (50, 5, 3), (7, 7, 100)]:
+        toks, res, ev = binding.test_batcher(a, u, s, m, slots, eb, R)
+        enc = [e for e in ev if e[0] == 0]
+        assert sorted(e[2] for e in enc) == list(range(50))      # each segment encoded exactly once
+        assert max(e[1] for e in enc) < slots
+        # steps = longest chain of per-slot work; every active slot advances each step
+        assert sum(e[1] for e in ev if e[0] == 1) == sum(m)       # n_prompt = 1 -> m steps each
+        if ref is None:
+            ref = (toks.copy(), res)
+        else:
+            assert np.array_equal(toks, ref[0]) and res == ref[1]
+
+
+def test_queue_order_is_arrival_then_user_then_id(lib):
+    a = [5, 5, 1, 5, 0]
+    u = [2, 1, 9, 1, 3]
+    s = [10, 11, 12, 9, 13]
+    m = [1, 1, 1, 1, 1]
+    _, _, ev = binding.test_batcher(a, u, s, m, 1, 1, 1)
+    assert [e[2] for e in ev if e[0] == 0] == [4, 2, 3, 1, 0]
+
+
+def test_bad_arguments(lib):
+    with pytest.raises(binding.WhisperError):
+        binding.test_batcher([0], [0], [0], [0], 1, 1, 1)
+    with pytest.raises(binding.WhisperError):
+        binding.test_batcher([0], [0], [0], [1], 0, 1, 1)
+    toks, res, ev = binding.test_batcher([], [], [], [], 2, 1, 1)
+    assert len(res) == 0 and len(ev) == 0

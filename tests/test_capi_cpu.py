@@ -1,0 +1,104 @@
+"""Host-side checks of the C-ABI library (no GPU needed): it loads, exports
+every function the header declares, parses weight blobs, and rejects bad
+arguments before touching a device."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2507_01021_amd import binding, synth
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "whisper_mi355x.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        pytest.skip("library not built (python -m paper_2507_01021_amd.build)")
+    return binding.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(whisper_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declarations_match_binding():
+    assert declared_functions() == sorted(binding.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """The ctypes mirrors have the sizes and offsets a C compiler gives the
+    header's structs."""
+    fields = {"whisper_params": [f for f, _ in binding.whisper_params._fields_],
+              "whisper_segment": [f for f, _ in binding.whisper_segment._fields_],
+              "whisper_result": [f for f, _ in binding.whisper_result._fields_]}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HEADER}"', "int main(void) {"]
+    for st, fs in fields.items():
+        lines.append(f'printf("{st} %zu\\n", sizeof({st}));')
+        for f in fs:
+            lines.append(f'printf("{st}.{f} %zu\\n", offsetof({st}, {f}));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    import subprocess
+    subprocess.run(["gcc", "-o", str(exe), str(src)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                  check=True).stdout.splitlines())
+    for st, fs in fields.items():
+        cls = getattr(binding, st)
+        assert int(got[st]) == C.sizeof(cls), st
+        for f in fs:
+            assert int(got[f"{st}.{f}"]) == getattr(cls, f).offset, (st, f)
+
+
+def test_params_from_blob(lib):
+    s = synth.TINY.with_(n_vocab=300, n_enc=1, n_dec=1)
+    blob = synth.pack_blob(synth.make_weights(s, 0))
+    p = binding.params_from_blob(blob)
+    assert (p.n_mels, p.n_audio_state, p.n_audio_head, p.n_audio_layer, p.n_vocab, p.n_text_layer,
+            p.dtype, p.max_slots) == (80, 384, 6, 1, 300, 1, 0, 32)
+    bad = blob.copy()
+    bad[0] = ord("X")
+    with pytest.raises(binding.WhisperError) as e:
+        binding.params_from_blob(bad)
+    assert e.value.status == binding.E_FORMAT
+
+
+@pytest.mark.parametrize("field,value", [("max_slots", 0), ("max_slots", 129), ("pad_mode", 2),
+                                         ("max_encode_batch", 99), ("refill_min", -1)])
+def test_create_rejects_bad_params_before_device(lib, field, value):
+    s = synth.TINY.with_(n_vocab=300, n_enc=1, n_dec=1)
+    blob = synth.pack_blob(synth.make_weights(s, 0))
+    p = binding.params_from_blob(blob)
+    setattr(p, field, value)
+    h = C.c_void_p()
+    st = lib.whisper_ctx_create(C.byref(p), blob.ctypes.data, blob.nbytes, 0, C.byref(h))
+    assert st == binding.E_INVAL and not h.value
+    assert lib.whisper_last_error(None)
+
+
+def test_create_rejects_params_not_matching_blob(lib):
+    s = synth.TINY.with_(n_vocab=300, n_enc=1, n_dec=1)
+    blob = synth.pack_blob(synth.make_weights(s, 0))
+    p = binding.params_from_blob(blob)
+    p.n_vocab = 301
+    h = C.c_void_p()
+    assert lib.whisper_ctx_create(C.byref(p), blob.ctypes.data, blob.nbytes, 0, C.byref(h)) == binding.E_FORMAT
+
+
+def test_null_context_calls_fail_cleanly(lib):
+    assert lib.whisper_batch_encode(None, None, 1, None) == binding.E_INVAL
+    assert lib.whisper_batch_decode_step(None, None, 1, None, None, None) == binding.E_INVAL
+    assert lib.whisper_batch_transcribe(None, None, 1, None, 0, None) == binding.E_INVAL
+    lib.whisper_ctx_destroy(None)
