@@ -516,11 +516,13 @@ class EngineT final : public Engine {
         const int d = d_, M = nb * N_CTX;
         // small per-pass arrays: sources, valid frames, slots, prompts
         std::vector<SegSrc> src(nb);
-        std::vector<int> small((size_t)nb * (3 + 448), 0);  // nvalid | slot_of | n_prompt | prompts
+        // nvalid | slot_of | n_prompt | prompts, each block EB entries long (the
+        // device pointers nvalid_, slot_of_, seat_np_, seat_prompts_ use that stride)
+        std::vector<int> small((size_t)EB_ * (3 + 448), 0);
         int* nv = small.data();
-        int* so = nv + nb;
-        int* npv = so + nb;
-        int* pr = npv + nb;
+        int* so = nv + EB_;
+        int* npv = so + EB_;
+        int* pr = npv + EB_;
         for (int i = 0; i < nb; ++i) {
             const SegmentDesc& s = segs[i];
             if (s.on_device) {
