@@ -192,7 +192,6 @@ struct DecLayerW {
     T *Wqkv, *Wo, *Wcq, *Wco, *W1, *W2;
 };
 
-constexpr int CROSS_CHUNKS = (N_CTX + 255) / 256;
 
 template <class T>
 class EngineT final : public Engine {
@@ -250,37 +249,37 @@ class EngineT final : public Engine {
         }
         if (forced) upload(1, forced_, forced, n * sizeof(int));
         const int d = d_;
+        const int ks1 = split_k(d), ks4 = split_k(4 * d);
         prof_begin(WHISPER_K_DEC_STEP);
-        hipLaunchKernelGGL(embed_kernel<T>, dim3(n), dim3(256), 0, st_, tok_emb_, pos_emb_, list_, pos_, seq_, dx_, d);
+        WMI_SWITCH_E(d, hipLaunchKernelGGL((embed_ln_kernel<T, E>), dim3(n), dim3(64), 0, st_, tok_emb_, pos_emb_,
+                                           list_, pos_, seq_, dx_, dz_, dec_[0].ln1g, dec_[0].ln1b));
         for (int l = 0; l < Ld_; ++l) {
             const DecLayerW<T>& L = dec_[l];
             const long long sl = (long long)l * S_ * H_ * 64;
-            ln(dx_, dz_, L.ln1g, L.ln1b, n);
-            proj(L.Wqkv, 3 * d, dz_, n, d,
+            proj(L.Wqkv, 3 * d, dz_, n, d, 1,
                  EpiDecQKV<T>{L.bq, L.bv, dq_, kts_ + sl * TS, vs_ + sl * TS, list_, pos_, d, H_});
-            DecAttnArgs sa{dq_, kts_ + sl * TS, vs_ + sl * TS, datt_, part_, list_, pos_, 0, TS, H_, d, 1};
+            DecAttnArgs sa{dq_, kts_ + sl * TS, vs_ + sl * TS, datt_, list_, pos_, TS, H_, d};
             prof_begin(WHISPER_K_SELF_ATTN);
-            hipLaunchKernelGGL((dec_attn_kernel<T, 8>), dim3(1, H_, n), dim3(64), 0, st_, sa);
+            hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, st_, sa);
             prof_end(WHISPER_K_SELF_ATTN);
-            proj(L.Wo, d, datt_, n, d, EpiResid{L.bo, dx_, d});
-            ln(dx_, dz_, L.ln2g, L.ln2b, n);
-            proj(L.Wcq, d, dz_, n, d, EpiQ<T>{L.cbq, dq_, d});
-            DecAttnArgs ca{dq_, ktc_ + sl * TC, vc_ + sl * TC, datt_, part_, list_, nullptr, N_CTX, TC, H_, d,
-                           CROSS_CHUNKS};
+            proj(L.Wo, d, datt_, n, d, ks1, EpiPartial{gpart_, d, n});
+            resid_ln(ks1, n, L.bo, L.ln2g, L.ln2b);
+            proj(L.Wcq, d, dz_, n, d, 1, EpiQ<T>{L.cbq, dq_, d});
+            DecAttnArgs ca{dq_, ktc_ + sl * TC, vc_ + sl * TC, datt_, list_, nullptr, TC, H_, d};
             prof_begin(WHISPER_K_CROSS_ATTN);
-            hipLaunchKernelGGL((dec_attn_kernel<T, 4>), dim3(CROSS_CHUNKS, H_, n), dim3(64), 0, st_, ca);
+            hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, st_, ca);
             prof_end(WHISPER_K_CROSS_ATTN);
-            hipLaunchKernelGGL(dec_attn_combine_kernel<T>, dim3(H_, n), dim3(64), 0, st_, part_, datt_, H_, d,
-                               CROSS_CHUNKS);
-            proj(L.Wco, d, datt_, n, d, EpiResid{L.cbo, dx_, d});
-            ln(dx_, dz_, L.ln3g, L.ln3b, n);
-            proj(L.W1, 4 * d, dz_, n, d, EpiGelu<T>{L.b1, dh_, 4 * d});
-            proj(L.W2, d, dh_, n, 4 * d, EpiResid{L.b2, dx_, d});
+            proj(L.Wco, d, datt_, n, d, ks1, EpiPartial{gpart_, d, n});
+            resid_ln(ks1, n, L.cbo, L.ln3g, L.ln3b);
+            proj(L.W1, 4 * d, dz_, n, d, 1, EpiGelu<T>{L.b1, dh_, 4 * d});
+            proj(L.W2, d, dh_, n, 4 * d, ks4, EpiPartial{gpart_, d, n});
+            const bool last = l + 1 == Ld_;
+            resid_ln(ks4, n, L.b2, last ? lnfg_ : dec_[l + 1].ln1g, last ? lnfb_ : dec_[l + 1].ln1b);
         }
-        ln(dx_, dz_, lnfg_, lnfb_, n);
-        proj(tok_emb_, V_, dz_, n, d, EpiLogits{logits_, V_});
-        hipLaunchKernelGGL(argmax_step_kernel, dim3(n), dim3(256), 0, st_, logits_, V_, list_, pos_, npr_, seq_, gen_,
-                           forced ? forced_ : nullptr, outtok_);
+        proj(tok_emb_, V_, dz_, n, d, 1, EpiLogits{logits_, V_});
+        hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, st_, logits_, V_, best_);
+        hipLaunchKernelGGL(argmax_step_kernel, dim3((n + 63) / 64), dim3(64), 0, st_, best_, n, list_, pos_, npr_,
+                           seq_, gen_, forced ? forced_ : nullptr, outtok_);
         prof_end(WHISPER_K_DEC_STEP);
         WMI_HIP(hipGetLastError());
         if (out_tok) WMI_HIP(hipMemcpyAsync(out_tok, outtok_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
@@ -411,7 +410,8 @@ class EngineT final : public Engine {
     // decoder state and workspace
     int *seq_, *gen_, *pos_, *npr_, *list_, *forced_, *outtok_;
     T *kts_, *vs_, *ktc_, *vc_, *dz_, *dq_, *datt_, *dh_;
-    float *dx_, *logits_, *part_;
+    float *dx_, *logits_, *gpart_;
+    unsigned long long* best_;
     std::vector<int> list_host_;
     // host staging
     Stage stage_[3];
@@ -495,8 +495,21 @@ class EngineT final : public Engine {
 
     // -------------------------------------------------------------- kernels
     void ln(const float* x, T* y, const float* g, const float* b, int rows) {
-        hipLaunchKernelGGL(layer_norm_kernel<T>, dim3((rows + 3) / 4), dim3(256), 0, st_, x, y, g, b, rows, d_);
+        WMI_SWITCH_E(d_, hipLaunchKernelGGL((layer_norm_kernel<T, E>), dim3((rows + 3) / 4), dim3(256), 0, st_, x,
+                                            y, g, b, rows));
     }
+    // decoder: x += split-K partials + bias, then z = LN(x)
+    void resid_ln(int KS, int n, const float* bias, const float* g, const float* b) {
+        if (KS == 4) {
+            WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 4>), dim3(n), dim3(64), 0, st_, gpart_, n,
+                                                bias, dx_, dz_, g, b));
+        } else {
+            WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 1>), dim3(n), dim3(64), 0, st_, gpart_, n,
+                                                bias, dx_, dz_, g, b));
+        }
+    }
+    // split factor of a decode projection with reduction length K
+    static int split_k(int K) { return (K / 32) % 4 == 0 ? 4 : 1; }
 
     template <class Epi>
     void gemm(const T* A, int lda, long long sA, const T* B, int ldb, long long sB, int MA, int MB, int K, int batch,
@@ -507,9 +520,9 @@ class EngineT final : public Engine {
 
     // decode projection: rows = weight rows (MA), n activation rows of width K
     template <class Epi>
-    void proj(const T* W, int MA, const T* X, int n, int K, const Epi& epi) {
-        if constexpr (std::is_same<T, bf16>::value) skinny_bf16(W, MA, X, n, K, epi, st_);
-        else gemm_simt(W, K, 0, X, K, 0, MA, n, K, 1, epi, st_);
+    void proj(const T* W, int MA, const T* X, int n, int K, int KS, const Epi& epi) {
+        if constexpr (std::is_same<T, bf16>::value) skinny_bf16(W, MA, X, n, K, KS, epi, st_);
+        else gemm_simt(W, K, K / KS, X, K, K / KS, MA, n, K / KS, KS, epi, st_);
     }
 
     void encode_pass(const SegmentDesc* segs, int nb, const int* slots) {
@@ -714,7 +727,8 @@ class EngineT final : public Engine {
         datt_ = dalloc<T>(S * d);
         dh_ = dalloc<T>(S * 4 * d);
         logits_ = dalloc<float>(S * (size_t)V_);
-        part_ = dalloc<float>(S * H * CROSS_CHUNKS * 66);
+        gpart_ = dalloc<float>(4 * S * d);
+        best_ = dalloc<unsigned long long>(S);
     }
 };
 

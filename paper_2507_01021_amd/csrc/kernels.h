@@ -75,48 +75,107 @@ __global__ __launch_bounds__(1024) void mel_norm_kernel(float* __restrict__ logm
 }
 
 // ------------------------------------------------------------- layer norm
+//
+// One wavefront per row of width d = 64 * E: fp32 mean and biased variance
+// (two passes over registers), eps 1e-5, gain and bias. E is a compile-time
+// constant so every load of a row is issued before the first use.
 
-// One wavefront per row of width d (d % 64 == 0, d <= 2048): fp32 mean and
-// biased variance, eps 1e-5, gain and bias.
-template <class T>
-__global__ __launch_bounds__(256) void layer_norm_kernel(const float* __restrict__ x, T* __restrict__ y,
-                                                         const float* __restrict__ g, const float* __restrict__ b,
-                                                         int rows, int d) {
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-    if (row >= rows) return;
-    const float* xr = x + (long long)row * d;
-    const int E = d >> 6;
-    float v[32];
+template <int E, class T>
+__device__ __forceinline__ void ln_row_store(const float (&v)[E], int lane, int d, const float* __restrict__ g,
+                                             const float* __restrict__ b, T* __restrict__ yr) {
     float s = 0.f;
 #pragma unroll
-    for (int e = 0; e < 32; ++e)
-        if (e < E) { v[e] = xr[lane + 64 * e]; s += v[e]; }
+    for (int e = 0; e < E; ++e) s += v[e];
     const float mean = wave_sum(s) / d;
     float q = 0.f;
 #pragma unroll
-    for (int e = 0; e < 32; ++e)
-        if (e < E) { const float c = v[e] - mean; q += c * c; }
+    for (int e = 0; e < E; ++e) { const float c = v[e] - mean; q += c * c; }
     const float rstd = rsqrtf(wave_sum(q) / d + 1e-5f);
-    T* yr = y + (long long)row * d;
+    float gg[E], bb[E];
 #pragma unroll
-    for (int e = 0; e < 32; ++e)
-        if (e < E) {
-            const int c = lane + 64 * e;
-            stf(yr + c, (v[e] - mean) * rstd * g[c] + b[c]);
-        }
+    for (int e = 0; e < E; ++e) { gg[e] = g[lane + 64 * e]; bb[e] = b[lane + 64 * e]; }
+#pragma unroll
+    for (int e = 0; e < E; ++e) stf(yr + lane + 64 * e, (v[e] - mean) * rstd * gg[e] + bb[e]);
 }
 
-// ------------------------------------------------------------- decoder embedding
+template <class T, int E>
+__global__ __launch_bounds__(256) void layer_norm_kernel(const float* __restrict__ x, T* __restrict__ y,
+                                                         const float* __restrict__ g, const float* __restrict__ b,
+                                                         int rows) {
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    constexpr int d = 64 * E;
+    const float* xr = x + (long long)row * d;
+    float v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) v[e] = xr[lane + 64 * e];
+    ln_row_store<E>(v, lane, d, g, b, y + (long long)row * d);
+}
 
-template <class T>
-__global__ __launch_bounds__(256) void embed_kernel(const T* __restrict__ tok_emb, const T* __restrict__ pos_emb,
-                                                    const int* __restrict__ list, const int* __restrict__ pos,
-                                                    const int* __restrict__ seq, float* __restrict__ x, int d) {
-    const int r = blockIdx.x, s = list[r], p = pos[s];
+// Decoder input: x = token embedding + position embedding (fp32), then the
+// first layer's layer norm.
+template <class T, int E>
+__global__ __launch_bounds__(64) void embed_ln_kernel(const T* __restrict__ tok_emb, const T* __restrict__ pos_emb,
+                                                      const int* __restrict__ list, const int* __restrict__ pos,
+                                                      const int* __restrict__ seq, float* __restrict__ x,
+                                                      T* __restrict__ z, const float* __restrict__ g,
+                                                      const float* __restrict__ b) {
+    constexpr int d = 64 * E;
+    const int r = blockIdx.x, lane = threadIdx.x, s = list[r], p = pos[s];
     const int tok = seq[s * 448 + p];
-    for (int c = threadIdx.x; c < d; c += blockDim.x)
-        x[(long long)r * d + c] = ldf(tok_emb + (long long)tok * d + c) + ldf(pos_emb + (long long)p * d + c);
+    float v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int c = lane + 64 * e;
+        v[e] = ldf(tok_emb + (long long)tok * d + c) + ldf(pos_emb + (long long)p * d + c);
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) x[(long long)r * d + lane + 64 * e] = v[e];
+    ln_row_store<E>(v, lane, d, g, b, z + (long long)r * d);
 }
+
+// Residual update from split-K partial sums, then the next layer norm:
+// x[r] += sum_ks part[ks][r] + bias (partials added in ks order), z[r] = LN(x[r]).
+template <class T, int E, int KS>
+__global__ __launch_bounds__(64) void resid_ln_kernel(const float* __restrict__ part, int n,
+                                                      const float* __restrict__ bias, float* __restrict__ x,
+                                                      T* __restrict__ z, const float* __restrict__ g,
+                                                      const float* __restrict__ b) {
+    constexpr int d = 64 * E;
+    const int r = blockIdx.x, lane = threadIdx.x;
+    float v[E], bs[E], pk[KS][E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        v[e] = x[(long long)r * d + lane + 64 * e];
+        bs[e] = bias[lane + 64 * e];
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < E; ++e) pk[ks][e] = part[((long long)ks * n + r) * d + lane + 64 * e];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        float acc = pk[0][e];
+#pragma unroll
+        for (int ks = 1; ks < KS; ++ks) acc += pk[ks][e];
+        v[e] += acc + bs[e];
+        x[(long long)r * d + lane + 64 * e] = v[e];
+    }
+    ln_row_store<E>(v, lane, d, g, b, z + (long long)r * d);
+}
+
+// Dispatch on the row width d = 64 * E.
+#define WMI_SWITCH_E(d, ...)                                       \
+    switch ((d) >> 6) {                                            \
+        case 6: { constexpr int E = 6; __VA_ARGS__; break; }       \
+        case 8: { constexpr int E = 8; __VA_ARGS__; break; }       \
+        case 12: { constexpr int E = 12; __VA_ARGS__; break; }     \
+        case 16: { constexpr int E = 16; __VA_ARGS__; break; }     \
+        case 20: { constexpr int E = 20; __VA_ARGS__; break; }     \
+        case 24: { constexpr int E = 24; __VA_ARGS__; break; }     \
+        case 32: { constexpr int E = 32; __VA_ARGS__; break; }     \
+        default: throw ArgError(-1, "width must be 64 * {6,8,12,16,20,24,32}"); \
+    }
 
 // ------------------------------------------------------------- encoder attention (bf16 MFMA)
 //
@@ -357,70 +416,93 @@ struct DecAttnArgs {
     const void* kt;     // cache K^T of this layer: [S][H][64][TP]
     const void* v;      // cache V of this layer:   [S][H][TP][64]
     void* out;          // [n][d]
-    float* part;        // [n][H][n_chunks][66]
     const int* list;    // row -> slot
-    const int* pos;     // slot -> position (self-attention), or nullptr
-    int fixed_len;      // keys when pos is nullptr
-    int TP, H, d, n_chunks;
+    const int* pos;     // slot -> position (self-attention)
+    int TP, H, d;
 };
 
-template <class T, int PPL>
-__global__ __launch_bounds__(64) void dec_attn_kernel(DecAttnArgs a) {
+// Self-attention of one decode position over the slot's cached positions
+// 0..pos (causal by construction). Workgroup = 4 waves per (row, head):
+//   scores: wave w sums dims 16w..16w+15 for all positions (lane owns 8
+//     consecutive positions, 16 loads in flight), partials added in LDS;
+//   softmax: every wave holds all scores (fp32, wavefront reductions);
+//   P V: wave w takes positions 128w..128w+127, 8 lanes per 128-byte V row,
+//     partial outputs added in LDS.
+template <class T>
+__global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     __shared__ float qs[64];
-    __shared__ float ps[64 * PPL];
-    const int c = blockIdx.x, h = blockIdx.y, r = blockIdx.z, lane = threadIdx.x;
+    __shared__ float sp[4][512];
+    __shared__ float op[4][64];
+    const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int slot = a.list[r];
-    const int len = a.pos ? a.pos[slot] + 1 : a.fixed_len;
-    const int start = c * 64 * PPL;
+    const int len = a.pos[slot] + 1;
     const T* q = reinterpret_cast<const T*>(a.q) + (long long)r * a.d + h * 64;
-    qs[lane] = ldf(q + lane);
+    if (tid < 64) qs[tid] = ldf(q + tid);
     __syncthreads();
     const long long head = (long long)slot * a.H + h;
     const T* kt = reinterpret_cast<const T*>(a.kt) + head * 64 * a.TP;
     const T* vv = reinterpret_cast<const T*>(a.v) + head * a.TP * 64;
-
-    float s[PPL];
+    const int p0 = lane * 8;
+    float s[8];
 #pragma unroll
-    for (int i = 0; i < PPL; ++i) s[i] = 0.f;
-    const int p0 = start + lane * PPL;
+    for (int i = 0; i < 8; ++i) s[i] = 0.f;
     if (p0 < len) {
-#pragma unroll 8
-        for (int j = 0; j < 64; ++j) {
-            float kv[PPL];
-            load_vec<T>(kt + (long long)j * a.TP + p0, kv, PPL);
-            const float qj = qs[j];
+        float kv[16][8];
 #pragma unroll
-            for (int i = 0; i < PPL; ++i) s[i] = fmaf(qj, kv[i], s[i]);
+        for (int j = 0; j < 16; ++j) load_vec<T>(kt + (long long)(16 * w + j) * a.TP + p0, kv[j], 8);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const float qj = qs[16 * w + j];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) s[i] = fmaf(qj, kv[j][i], s[i]);
         }
     }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sp[w][p0 + i] = s[i];
+    __syncthreads();
     float mx = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < PPL; ++i) {
-        s[i] = (p0 + i < len) ? s[i] * LOG2E : -INFINITY;
+    for (int i = 0; i < 8; ++i) {
+        const float t = ((sp[0][p0 + i] + sp[1][p0 + i]) + sp[2][p0 + i]) + sp[3][p0 + i];
+        s[i] = (p0 + i < len) ? t * LOG2E : -INFINITY;
         mx = fmaxf(mx, s[i]);
     }
     mx = wave_max(mx);
     float lsum = 0.f;
 #pragma unroll
-    for (int i = 0; i < PPL; ++i) {
-        const float p = (p0 + i < len) ? exp2f(s[i] - mx) : 0.f;
-        ps[lane * PPL + i] = p;
-        lsum += p;
+    for (int i = 0; i < 8; ++i) {
+        s[i] = (p0 + i < len) ? exp2f(s[i] - mx) : 0.f;
+        lsum += s[i];
     }
     lsum = wave_sum(lsum);
+    __syncthreads();  // every wave has read the partial scores
+    if (w == 0) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sp[0][p0 + i] = s[i];
+    }
     __syncthreads();
-    // P V: lane covers dims dg*8..+7 of positions pg, pg + 8, ...
     const int dg = lane & 7, pg = lane >> 3;
     float o[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[i] = 0.f;
-    const int nloc = min(64 * PPL, len - start);
-    for (int pp = pg; pp < nloc; pp += 8) {
-        float vr[8];
-        load_vec<T>(vv + (long long)(start + pp) * 64 + dg * 8, vr, 8);
-        const float p = ps[pp];
+    const int lo = 128 * w, hi = min(len, lo + 128);
+    if (lo < hi) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) o[i] = fmaf(p, vr[i], o[i]);
+        for (int b0 = 0; b0 < 128; b0 += 64) {
+            float vr[8][8];
+            float pw[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int pp = lo + b0 + pg + 8 * u;
+                const int pc = min(pp, hi - 1);
+                load_vec<T>(vv + (long long)pc * 64 + dg * 8, vr[u], 8);
+                pw[u] = pp < hi ? sp[0][pc] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int i = 0; i < 8; ++i) o[i] = fmaf(pw[u], vr[u][i], o[i]);
+        }
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -428,69 +510,170 @@ __global__ __launch_bounds__(64) void dec_attn_kernel(DecAttnArgs a) {
         o[i] += __shfl_xor(o[i], 16, 64);
         o[i] += __shfl_xor(o[i], 32, 64);
     }
-    if (a.n_chunks == 1) {
-        if (lane < 8) {
-            const float inv = 1.0f / lsum;
-            T* out = reinterpret_cast<T*>(a.out) + (long long)r * a.d + h * 64 + dg * 8;
-            st4(out, o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
-            st4(out + 4, o[4] * inv, o[5] * inv, o[6] * inv, o[7] * inv);
-        }
-        return;
-    }
-    float* pr = a.part + (((long long)r * a.H + h) * a.n_chunks + c) * 66;
-    if (lane == 0) { pr[0] = mx; pr[1] = lsum; }
     if (lane < 8) {
-        st4(pr + 2 + dg * 8, o[0], o[1], o[2], o[3]);
-        st4(pr + 6 + dg * 8, o[4], o[5], o[6], o[7]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) op[w][dg * 8 + i] = o[i];
+    }
+    __syncthreads();
+    if (tid < 64) {
+        const float v = ((op[0][tid] + op[1][tid]) + op[2][tid]) + op[3][tid];
+        stf(reinterpret_cast<T*>(a.out) + (long long)r * a.d + h * 64 + tid, v / lsum);
     }
 }
 
-// Combine chunk partials: out = sum_c 2^(m_c - M) o_c / sum_c 2^(m_c - M) l_c.
+// Cross-attention of one decode position over the 1500 cached encoder
+// positions. Workgroup = CW waves per (row, head), wave w takes positions
+// 256w..256w+255: scores with K^T rows (lane owns 4 consecutive positions,
+// 16 dims' loads in flight), softmax over the chunk, P V with V rows (8
+// lanes per 128-byte row, 8 rows in flight); the chunk results (max, sum,
+// 64 outputs) are merged in LDS in wave order.
+constexpr int CW = (N_CTX + 255) / 256;
+
 template <class T>
-__global__ __launch_bounds__(64) void dec_attn_combine_kernel(const float* __restrict__ part, T* __restrict__ out,
-                                                              int H, int d, int n_chunks) {
-    const int h = blockIdx.x, r = blockIdx.y, j = threadIdx.x;
-    const float* pr = part + ((long long)r * H + h) * n_chunks * 66;
-    float M = -INFINITY;
-    for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, pr[c * 66]);
-    float L = 0.f, o = 0.f;
-    for (int c = 0; c < n_chunks; ++c) {
-        const float m = pr[c * 66];
-        const float w = m == -INFINITY ? 0.f : exp2f(m - M);
-        L += w * pr[c * 66 + 1];
-        o += w * pr[c * 66 + 2 + j];
+__global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {
+    __shared__ float qs[64];
+    __shared__ float ps[CW][256];
+    __shared__ float ml[CW][2];
+    __shared__ float op[CW][64];
+    const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int slot = a.list[r];
+    const T* q = reinterpret_cast<const T*>(a.q) + (long long)r * a.d + h * 64;
+    if (tid < 64) qs[tid] = ldf(q + tid);
+    __syncthreads();
+    const long long head = (long long)slot * a.H + h;
+    const T* kt = reinterpret_cast<const T*>(a.kt) + head * 64 * a.TP;
+    const T* vv = reinterpret_cast<const T*>(a.v) + head * a.TP * 64;
+    const int start = 256 * w;
+    const int p0 = start + lane * 4;
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+    if (p0 < N_CTX) {
+#pragma unroll 1
+        for (int j0 = 0; j0 < 64; j0 += 16) {
+            float kv[16][4];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) load_vec<T>(kt + (long long)(j0 + j) * a.TP + p0, kv[j], 4);
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const float qj = qs[j0 + j];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) s[i] = fmaf(qj, kv[j][i], s[i]);
+            }
+        }
     }
-    stf(out + (long long)r * d + h * 64 + j, o / L);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        s[i] = (p0 + i < N_CTX) ? s[i] * LOG2E : -INFINITY;
+        mx = fmaxf(mx, s[i]);
+    }
+    mx = wave_max(mx);
+    float lsum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float p = (p0 + i < N_CTX) ? exp2f(s[i] - mx) : 0.f;
+        ps[w][lane * 4 + i] = p;
+        lsum += p;
+    }
+    lsum = wave_sum(lsum);
+    __syncthreads();
+    const int dg = lane & 7, pg = lane >> 3;
+    float o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = 0.f;
+    const int nloc = min(256, N_CTX - start);
+#pragma unroll 1
+    for (int b0 = 0; b0 < 256; b0 += 64) {
+        float vr[8][8];
+        float pw[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int pp = b0 + pg + 8 * u;
+            const int pc = min(pp, nloc - 1);
+            load_vec<T>(vv + (long long)(start + pc) * 64 + dg * 8, vr[u], 8);
+            pw[u] = pp < nloc ? ps[w][pc] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) o[i] = fmaf(pw[u], vr[u][i], o[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        o[i] += __shfl_xor(o[i], 8, 64);
+        o[i] += __shfl_xor(o[i], 16, 64);
+        o[i] += __shfl_xor(o[i], 32, 64);
+    }
+    if (lane < 8) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) op[w][dg * 8 + i] = o[i];
+    }
+    if (lane == 0) { ml[w][0] = mx; ml[w][1] = lsum; }
+    __syncthreads();
+    if (tid < 64) {
+        float M = ml[0][0];
+#pragma unroll
+        for (int c = 1; c < CW; ++c) M = fmaxf(M, ml[c][0]);
+        float L = 0.f, acc = 0.f;
+#pragma unroll
+        for (int c = 0; c < CW; ++c) {
+            const float wgt = exp2f(ml[c][0] - M);
+            L += wgt * ml[c][1];
+            acc += wgt * op[c][tid];
+        }
+        stf(reinterpret_cast<T*>(a.out) + (long long)r * a.d + h * 64 + tid, acc / L);
+    }
 }
 
 // ------------------------------------------------------------- skinny decode GEMM (bf16 MFMA)
 //
 // C[i][r] = sum_k W[i][k] X[r][k] for a few rows r (active decode slots,
 // n <= 16 * NT) and many weight rows i: each weight byte is read once.
-// Workgroup = 4 waves over 16 * RT weight rows; the waves split K in
-// interleaved 32-wide steps and their partial sums are added in LDS in a
-// fixed order (so a row's result never depends on the other rows present).
-template <int RT, int NT, class Epi>
-__global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict__ W, int MA,
-                                                          const bf16* __restrict__ X, int n, int K, Epi epi) {
+// Grid (row tiles, KS): workgroup (tile, ks) covers 16 * RT weight rows and
+// K columns [ks * K, (ks + 1) * K) of rows of length ldw / ldx. Its 4 waves
+// take interleaved 32-wide k-steps, U steps' loads issued before their
+// MFMAs; the wave partial sums are added in LDS in a fixed order, so a row's
+// result never depends on which other rows are present. The epilogue gets
+// z = ks (split-K partials go to EpiPartial).
+template <int RT, int NT, int U, class Epi>
+__global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict__ W, int ldw, int MA,
+                                                          const bf16* __restrict__ X, int ldx, int n, int K, Epi epi) {
     __shared__ float red[3][RT * NT * 4][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int fr = lane & 15, fc = lane >> 4;
     const int i0 = blockIdx.x * 16 * RT;
+    const int kbase = blockIdx.y * K;
     const bf16* wp[RT];
 #pragma unroll
-    for (int t = 0; t < RT; ++t) wp[t] = W + (long long)min(i0 + t * 16 + fr, MA - 1) * K + fc * 8;
+    for (int t = 0; t < RT; ++t) wp[t] = W + (long long)min(i0 + t * 16 + fr, MA - 1) * ldw + kbase + fc * 8;
     const bf16* xp[NT];
 #pragma unroll
-    for (int u = 0; u < NT; ++u) xp[u] = X + (long long)min(u * 16 + fr, n - 1) * K + fc * 8;
+    for (int u = 0; u < NT; ++u) xp[u] = X + (long long)min(u * 16 + fr, n - 1) * ldx + kbase + fc * 8;
     mfma_f32x4 acc[RT][NT];
 #pragma unroll
     for (int t = 0; t < RT; ++t)
 #pragma unroll
         for (int u = 0; u < NT; ++u) acc[t][u] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
     const int nks = K >> 5;
-#pragma unroll 4
-    for (int s = wave; s < nks; s += 4) {
+    int s = wave;
+    for (; s + 4 * (U - 1) < nks; s += 4 * U) {
+        mfma_bf16x8 a[U][RT], b[U][NT];
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+            const int k = (s + 4 * q) * 32;
+#pragma unroll
+            for (int t = 0; t < RT; ++t) a[q][t] = *reinterpret_cast<const mfma_bf16x8*>(wp[t] + k);
+#pragma unroll
+            for (int u = 0; u < NT; ++u) b[q][u] = *reinterpret_cast<const mfma_bf16x8*>(xp[u] + k);
+        }
+#pragma unroll
+        for (int q = 0; q < U; ++q)
+#pragma unroll
+            for (int t = 0; t < RT; ++t)
+#pragma unroll
+                for (int u = 0; u < NT; ++u)
+                    acc[t][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q][t], b[q][u], acc[t][u], 0, 0, 0);
+    }
+    for (; s < nks; s += 4) {
         const int k = s * 32;
         mfma_bf16x8 a[RT], b[NT];
 #pragma unroll
@@ -523,70 +706,100 @@ __global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict
                 v[e] = ((acc[t][u][e] + red[0][idx][lane]) + red[1][idx][lane]) + red[2][idx][lane];
             }
             const int i = i0 + t * 16 + fc * 4, r = u * 16 + fr;
-            if (i < MA && r < n) epi(i, r, 0, v[0], v[1], v[2], v[3]);
+            if (i < MA && r < n) epi(i, r, blockIdx.y, v[0], v[1], v[2], v[3]);
         }
 }
 
+// Split-K partial sums: part[ks][r][i..i+3] (row length N).
+struct EpiPartial {
+    float* part;
+    int N, n;
+    __device__ void operator()(int i, int r, int ks, float a, float b, float c, float e) const {
+        st4(part + ((long long)ks * n + r) * N + i, a, b, c, e);
+    }
+};
+
+// W: [MA][KS * K] weight rows, X: [n][KS * K]; KS workgroups split K.
 template <class Epi>
-inline void skinny_bf16(const bf16* W, int MA, const bf16* X, int n, int K, const Epi& epi, hipStream_t st) {
-    if (K % 32 || n <= 0 || n > 128 || MA <= 0) throw ArgError(-1, "skinny_bf16: unsupported shape");
+inline void skinny_bf16(const bf16* W, int MA, const bf16* X, int n, int K, int KS, const Epi& epi, hipStream_t st) {
+    if (KS < 1 || K % (32 * KS) || n <= 0 || n > 128 || MA <= 0) throw ArgError(-1, "skinny_bf16: unsupported shape");
+    const int Kc = K / KS;
     const bool big = MA >= 16384;  // output head: 32 rows per workgroup
-#define WMI_SKINNY(RT, NT)                                                                       \
-    hipLaunchKernelGGL((skinny_bf16_kernel<RT, NT, Epi>), dim3((MA + 16 * RT - 1) / (16 * RT)), \
-                       dim3(256), 0, st, W, MA, X, n, K, epi)
+#define WMI_SKINNY(RT, NT, U)                                                                              \
+    hipLaunchKernelGGL((skinny_bf16_kernel<RT, NT, U, Epi>), dim3((MA + 16 * RT - 1) / (16 * RT), KS),    \
+                       dim3(256), 0, st, W, K, MA, X, K, n, Kc, epi)
     if (big) {
-        if (n <= 16) WMI_SKINNY(2, 1); else if (n <= 32) WMI_SKINNY(2, 2);
-        else if (n <= 64) WMI_SKINNY(2, 4); else WMI_SKINNY(2, 8);
+        if (n <= 16) WMI_SKINNY(2, 1, 4); else if (n <= 32) WMI_SKINNY(2, 2, 4);
+        else if (n <= 64) WMI_SKINNY(2, 4, 2); else WMI_SKINNY(2, 8, 2);
     } else {
-        if (n <= 16) WMI_SKINNY(1, 1); else if (n <= 32) WMI_SKINNY(1, 2);
-        else if (n <= 64) WMI_SKINNY(1, 4); else WMI_SKINNY(1, 8);
+        if (n <= 16) WMI_SKINNY(1, 1, 8); else if (n <= 32) WMI_SKINNY(1, 2, 8);
+        else if (n <= 64) WMI_SKINNY(1, 4, 4); else WMI_SKINNY(1, 8, 2);
     }
 #undef WMI_SKINNY
 }
 
 // ------------------------------------------------------------- greedy step
 //
-// One workgroup per row: argmax of the logits (lowest id on exact ties);
-// records it, feeds it (or the forced token) as the slot's next input once
-// the prompt is consumed, and advances the slot's position.
-__global__ __launch_bounds__(256) void argmax_step_kernel(const float* __restrict__ logits, int V,
-                                                          const int* __restrict__ list, int* __restrict__ pos,
-                                                          const int* __restrict__ n_prompt, int* __restrict__ seq,
-                                                          int* __restrict__ gen, const int* __restrict__ forced,
-                                                          int* __restrict__ out_tok) {
-    const int r = blockIdx.x, t = threadIdx.x;
+// argmax over the logits in two kernels: (1) grid (chunks, rows), each
+// workgroup reduces a chunk of one row and folds it into best[r] with a
+// 64-bit atomic max of (order-preserving value bits << 32 | ~index), which
+// picks the largest value and, among equal values, the lowest index, in any
+// order of arrival; (2) one thread per row reads best[r], resets it, records
+// the token, feeds it (or the forced token) as the next input once the
+// prompt is consumed, and advances the slot's position.
+constexpr int ARGMAX_CHUNKS = 16;
+
+__device__ inline unsigned long long amax_key(float v, int i) {
+    return ((unsigned long long)f2ord(v) << 32) | (unsigned long long)(0xffffffffu - (unsigned)i);
+}
+
+__global__ __launch_bounds__(256) void argmax_partial_kernel(const float* __restrict__ logits, int V,
+                                                             unsigned long long* __restrict__ best) {
+    const int r = blockIdx.y, t = threadIdx.x;
+    const int per = (V + ARGMAX_CHUNKS - 1) / ARGMAX_CHUNKS;
+    const int lo = blockIdx.x * per, hi = min(V, lo + per);
     const float* lg = logits + (long long)r * V;
-    float best = -INFINITY;
-    int bi = 0x7fffffff;
-    for (int i = t; i < V; i += 256) {
-        const float v = lg[i];
-        if (v > best) { best = v; bi = i; }  // i increases: first maximum kept
+    unsigned long long k = 0;
+    for (int i = lo + t; i < hi; i += 256 * 4) {
+        float v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = (i + 256 * q < hi) ? lg[i + 256 * q] : -INFINITY;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (i + 256 * q < hi) { const unsigned long long c = amax_key(v[q], i + 256 * q); k = c > k ? c : k; }
     }
-    __shared__ float sv[256];
-    __shared__ int si[256];
-    sv[t] = best;
-    si[t] = bi;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long c = __shfl_xor(k, o, 64);
+        k = c > k ? c : k;
+    }
+    __shared__ unsigned long long sk[4];
+    if ((t & 63) == 0) sk[t >> 6] = k;
     __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if (t < w) {
-            const float ov = sv[t + w];
-            const int oi = si[t + w];
-            if (ov > sv[t] || (ov == sv[t] && oi < si[t])) { sv[t] = ov; si[t] = oi; }
-        }
-        __syncthreads();
-    }
     if (t == 0) {
-        const int s = list[r], p = pos[s], np = n_prompt[s];
-        const int tok = si[0];
-        if (p >= np - 1) {
-            gen[s * 448 + (p - (np - 1))] = tok;
-            seq[s * 448 + p + 1] = forced ? forced[r] : tok;
-            out_tok[r] = tok;
-        } else {
-            out_tok[r] = -1;
-        }
-        pos[s] = p + 1;
+        unsigned long long m = sk[0];
+        for (int w = 1; w < 4; ++w) m = sk[w] > m ? sk[w] : m;
+        atomicMax(best + r, m);
     }
+}
+
+__global__ void argmax_step_kernel(unsigned long long* __restrict__ best, int n, const int* __restrict__ list,
+                                   int* __restrict__ pos, const int* __restrict__ n_prompt, int* __restrict__ seq,
+                                   int* __restrict__ gen, const int* __restrict__ forced, int* __restrict__ out_tok) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n) return;
+    const unsigned long long k = best[r];
+    best[r] = 0ull;
+    const int tok = (int)(0xffffffffu - (unsigned)(k & 0xffffffffull));
+    const int s = list[r], p = pos[s], np = n_prompt[s];
+    if (p >= np - 1) {
+        gen[s * 448 + (p - (np - 1))] = tok;
+        seq[s * 448 + p + 1] = forced ? forced[r] : tok;
+        out_tok[r] = tok;
+    } else {
+        out_tok[r] = -1;
+    }
+    pos[s] = p + 1;
 }
 
 // Seat prompts: for entry e, slot slots[e] gets tokens prompts[e * 448 ...].
