@@ -64,6 +64,24 @@ def fixed_schedule(segs):
     return steps
 
 
+def counter_traffic(workload):
+    """HBM bytes per launch of the cross-attention kernel from the committed
+    rocprofv3 FETCH_SIZE/WRITE_SIZE summary (scaled by the copy-kernel
+    calibration), or None when the kernel's source has changed since the
+    counters were taken or no summary exists for this workload."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"cross_attn_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    fields = dict(l.split(": ", 1) for l in open(path).read().splitlines() if ": " in l and " " not in l.split(": ")[0])
+    src = open(os.path.join(ROOT, "paper_2507_01021_amd", "csrc", "kernels.h")).read()
+    i = src.index("__global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {")
+    j = src.index("\n}\n", i)
+    if hashlib.sha256(src[i:j].encode()).hexdigest()[:16] != fields.get("kernel_source_sha256_16", "").strip():
+        return None
+    return float(fields["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(shape, W, segs):
     """The oracle, as is, on a bounded sample: one segment's front end, conv
     stem, two encoder layers, two layers of cross-attention keys/values and
@@ -125,6 +143,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
+    ap.add_argument("--max-new", type=int, default=0,
+                    help="profiling runs only: decode this many tokens per segment instead of the workload's")
     a = ap.parse_args()
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {a.gpus}): segments are independent, "
@@ -136,6 +156,9 @@ def main():
     from paper_2507_01021_amd import binding, synth
 
     shape, segs, slots = synth.workload(a.workload)
+    if a.max_new:
+        for s in segs:
+            s.max_new_tokens = a.max_new
     W = synth.make_weights(shape, 0)
     blob = synth.pack_blob(W)
     dev_audio = [torch.from_numpy(s.audio).to("cuda:0") for s in segs]
@@ -159,8 +182,9 @@ def main():
     assert all(r["status"] == 0 and r["tokens"].size == s.max_new_tokens for r, s in zip(res, segs))
 
     if a.calib_copy_mib:
-        x = torch.empty(a.calib_copy_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda:0")
+        x = torch.ones(a.calib_copy_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda:0")
         y = torch.empty_like(x)
+        torch.cuda.synchronize()
         y.copy_(x)
         torch.cuda.synchronize()
 
@@ -172,7 +196,7 @@ def main():
     ca_avg_s = ca_ms / 1e3 / max(ca_n, 1)
     achieved = ca_bytes / ca_avg_s / 1e9
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-            "frac": round(achieved / (PEAK_HBM / 1e9), 4), "traffic": None,
+            "frac": round(achieved / (PEAK_HBM / 1e9), 4), "traffic": counter_traffic(a.workload),
             "kernel": "cross_attn_kernel<bf16> (decode-step cross-attention over the 1500 cached positions)",
             "bytes_per_launch": ca_bytes, "avg_launch_us": round(ca_avg_s * 1e6, 2), "launches": ca_n}
 
