@@ -69,7 +69,18 @@ __device__ inline float4 ld4(const bf16* p) {
     return make_float4(a.f, b.f, c.f, d.f);
 }
 
-__device__ inline float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, formula
+// 7.1.26 (absolute error below 1.5e-7): for z >= 0,
+// erf(z) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-z^2), t = 1 / (1 + p z).
+__device__ inline float erf_as(float z) {
+    const float az = fabsf(z);
+    const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * az);
+    const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+    const float r = 1.0f - poly * __expf(-az * az);
+    return copysignf(r, z);
+}
+// GELU, erf form: x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)).
+__device__ inline float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f)); }
 
 __device__ inline float wave_sum(float v) {
 #pragma unroll

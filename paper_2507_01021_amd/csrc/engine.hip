@@ -17,6 +17,7 @@
 //   residual, LN, fc1 + GELU, fc2 + residual -> final LN -> logits against
 //   the token embedding -> argmax, next input, position advance.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -204,6 +205,7 @@ class EngineT final : public Engine {
         WMI_HIP(hipSetDevice(dev_));
         WMI_HIP(hipStreamCreateWithFlags(&own_stream_, hipStreamNonBlocking));
         st_ = own_stream_;
+        if (const char* g = getenv("WHISPER_STEP_GRAPHS")) graphs_ = g[0] != '0';
         load_weights(blob, bytes);
         alloc_state();
         WMI_HIP(hipDeviceSynchronize());
@@ -215,6 +217,7 @@ class EngineT final : public Engine {
         for (auto& pr : prof_)
             for (auto& e : pr.used) { (void)hipEventDestroy(e.first); (void)hipEventDestroy(e.second); }
         for (auto e : event_pool_) (void)hipEventDestroy(e);
+        for (auto& g : step_graphs_) (void)hipGraphExecDestroy(g.second);
         for (auto& s : stage_) {
             if (s.ev) (void)hipEventDestroy(s.ev);
             if (s.host) (void)hipHostFree(s.host);
@@ -248,6 +251,37 @@ class EngineT final : public Engine {
             upload(0, list_, slots, n * sizeof(int));
         }
         if (forced) upload(1, forced_, forced, n * sizeof(int));
+        // Plain steps (no teacher forcing, no per-step outputs, no kernel
+        // timing) replay a captured graph of the whole step; the graph only
+        // depends on n because the slot list lives in device memory.
+        bool timed = false;
+        for (auto& pr : prof_) timed = timed || pr.on;
+        if (graphs_ && !forced && !out_tok && !out_logits && !timed) {
+            auto it = step_graphs_.find(n);
+            if (it == step_graphs_.end()) {
+                hipGraph_t g = nullptr;
+                hipGraphExec_t ge = nullptr;
+                WMI_HIP(hipStreamBeginCapture(st_, hipStreamCaptureModeRelaxed));
+                launch_step(n, false);
+                WMI_HIP(hipStreamEndCapture(st_, &g));
+                const hipError_t e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+                (void)hipGraphDestroy(g);
+                WMI_HIP(e);
+                it = step_graphs_.emplace(n, ge).first;
+            }
+            WMI_HIP(hipGraphLaunch(it->second, st_));
+        } else {
+            launch_step(n, forced != nullptr);
+        }
+        WMI_HIP(hipGetLastError());
+        if (out_tok) WMI_HIP(hipMemcpyAsync(out_tok, outtok_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
+        if (out_logits)
+            WMI_HIP(hipMemcpyAsync(out_logits, logits_, (size_t)n * V_ * sizeof(float), hipMemcpyDeviceToHost, st_));
+        if (sync_ || out_tok || out_logits || forced) WMI_HIP(hipStreamSynchronize(st_));
+    }
+
+    // The kernels of one decode step for the first n entries of the slot list.
+    void launch_step(int n, bool forced) {
         const int d = d_;
         const int ks1 = split_k(d), ks4 = split_k(4 * d);
         prof_begin(WHISPER_K_DEC_STEP);
@@ -281,11 +315,6 @@ class EngineT final : public Engine {
         hipLaunchKernelGGL(argmax_step_kernel, dim3((n + 63) / 64), dim3(64), 0, st_, best_, n, list_, pos_, npr_,
                            seq_, gen_, forced ? forced_ : nullptr, outtok_);
         prof_end(WHISPER_K_DEC_STEP);
-        WMI_HIP(hipGetLastError());
-        if (out_tok) WMI_HIP(hipMemcpyAsync(out_tok, outtok_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
-        if (out_logits)
-            WMI_HIP(hipMemcpyAsync(out_logits, logits_, (size_t)n * V_ * sizeof(float), hipMemcpyDeviceToHost, st_));
-        if (sync_ || out_tok || out_logits || forced) WMI_HIP(hipStreamSynchronize(st_));
     }
 
     void read_tokens(int slot, int count, int32_t* dst) override {
@@ -413,6 +442,8 @@ class EngineT final : public Engine {
     float *dx_, *logits_, *gpart_;
     unsigned long long* best_;
     std::vector<int> list_host_;
+    bool graphs_ = true;
+    std::map<int, hipGraphExec_t> step_graphs_;
     // host staging
     Stage stage_[3];
     int32_t* tokpin_ = nullptr;

@@ -24,10 +24,19 @@ constexpr int TS = 512;      // self-attention cache stride (>= 448)
 constexpr int TC = 1536;     // cross-attention cache stride (>= 1500)
 constexpr int CP = 128;      // padded mel channels of the conv input
 
+// Epilogues run in two phases so a lane's loads are issued together: pre()
+// loads whatever the store needs (bias, residual, table, slot) into an
+// EpiPre, then operator() computes and stores. Unused fields cost nothing.
+struct EpiPre {
+    float4 a, b;
+    int s;
+};
+
 // DFT -> power: rows (2k, 2k+1) are the cosine and sine parts of bin k.
 struct EpiPower {
     float* power;  // [batch * 3000][201]
-    __device__ void operator()(int i, int j, int z, float a, float b, float c, float d) const {
+    __device__ EpiPre pre(int, int, int) const { return EpiPre{}; }
+    __device__ void operator()(int i, int j, int z, float a, float b, float c, float d, const EpiPre&) const {
         const int k = i >> 1;
         float* p = power + ((long long)z * 3000 + j) * 201 + k;
         p[0] = a * a + b * b;
@@ -39,7 +48,8 @@ struct EpiPower {
 struct EpiLogMel {
     float* out;
     int n_mels;
-    __device__ void operator()(int i, int j, int, float a, float b, float c, float d) const {
+    __device__ EpiPre pre(int, int, int) const { return EpiPre{}; }
+    __device__ void operator()(int i, int j, int, float a, float b, float c, float d, const EpiPre&) const {
         st4(out + (long long)j * n_mels + i, log10f(fmaxf(a, 1e-10f)), log10f(fmaxf(b, 1e-10f)),
             log10f(fmaxf(c, 1e-10f)), log10f(fmaxf(d, 1e-10f)));
     }
@@ -50,10 +60,10 @@ struct EpiConv1 {  // i = channel, j = frame
     const float* bias;
     T* h1;  // H1pad
     int d;
-    __device__ void operator()(int i, int j, int z, float a, float b, float c, float e) const {
-        const float* bb = bias + i;
-        st4(h1 + ((long long)z * 3002 + j + 1) * d + i, gelu_erf(a + bb[0]), gelu_erf(b + bb[1]),
-            gelu_erf(c + bb[2]), gelu_erf(e + bb[3]));
+    __device__ EpiPre pre(int i, int, int) const { EpiPre p{}; p.a = ld4(bias + i); return p; }
+    __device__ void operator()(int i, int j, int z, float a, float b, float c, float e, const EpiPre& p) const {
+        st4(h1 + ((long long)z * 3002 + j + 1) * d + i, gelu_erf(a + p.a.x), gelu_erf(b + p.a.y),
+            gelu_erf(c + p.a.z), gelu_erf(e + p.a.w));
     }
 };
 
@@ -62,11 +72,15 @@ struct EpiConv2 {  // i = channel, j = position; adds the sinusoid table
     const float* pe;  // [1500][d]
     float* x;
     int d;
-    __device__ void operator()(int i, int j, int z, float a, float b, float c, float e) const {
-        const float* bb = bias + i;
-        const float4 p = ld4(pe + (long long)j * d + i);
-        st4(x + ((long long)z * N_CTX + j) * d + i, gelu_erf(a + bb[0]) + p.x, gelu_erf(b + bb[1]) + p.y,
-            gelu_erf(c + bb[2]) + p.z, gelu_erf(e + bb[3]) + p.w);
+    __device__ EpiPre pre(int i, int j, int) const {
+        EpiPre p{};
+        p.a = ld4(bias + i);
+        p.b = ld4(pe + (long long)j * d + i);
+        return p;
+    }
+    __device__ void operator()(int i, int j, int z, float a, float b, float c, float e, const EpiPre& p) const {
+        st4(x + ((long long)z * N_CTX + j) * d + i, gelu_erf(a + p.a.x) + p.b.x, gelu_erf(b + p.a.y) + p.b.y,
+            gelu_erf(c + p.a.z) + p.b.z, gelu_erf(e + p.a.w) + p.b.w);
     }
 };
 
@@ -76,13 +90,17 @@ struct EpiQK {  // A = [Wq; Wk] (2d rows), B = tokens
     T* q;
     T* k;
     int d, H;
-    __device__ void operator()(int i, int m, int, float a, float b, float c, float e) const {
+    __device__ EpiPre pre(int i, int, int) const {
+        EpiPre p{};
+        if (i < d) p.a = ld4(bq + i);
+        return p;
+    }
+    __device__ void operator()(int i, int m, int, float a, float b, float c, float e, const EpiPre& p) const {
         const int bseg = m / N_CTX, t = m - bseg * N_CTX;
         if (i < d) {
             const int h = i >> 6, jj = i & 63;
-            const float* bb = bq + i;
-            st4(q + (((long long)bseg * H + h) * TQ + t) * 64 + jj, (a + bb[0]) * 0.125f,
-                (b + bb[1]) * 0.125f, (c + bb[2]) * 0.125f, (e + bb[3]) * 0.125f);
+            st4(q + (((long long)bseg * H + h) * TQ + t) * 64 + jj, (a + p.a.x) * 0.125f, (b + p.a.y) * 0.125f,
+                (c + p.a.z) * 0.125f, (e + p.a.w) * 0.125f);
         } else {
             const int f = i - d, h = f >> 6, jj = f & 63;
             st4(k + (((long long)bseg * H + h) * TQ + t) * 64 + jj, a, b, c, e);
@@ -95,10 +113,11 @@ struct EpiVt {  // A = tokens (4 consecutive positions), B = Wv
     const float* bv;
     T* vt;
     int H;
-    __device__ void operator()(int m, int f, int, float a, float b, float c, float e) const {
+    __device__ EpiPre pre(int, int f, int) const { EpiPre p{}; p.a.x = bv[f]; return p; }
+    __device__ void operator()(int m, int f, int, float a, float b, float c, float e, const EpiPre& p) const {
         const int bseg = m / N_CTX, t = m - bseg * N_CTX;
         const int h = f >> 6, jj = f & 63;
-        const float bb = bv[f];
+        const float bb = p.a.x;
         st4(vt + (((long long)bseg * H + h) * 64 + jj) * TQ + t, a + bb, b + bb, c + bb, e + bb);
     }
 };
@@ -107,11 +126,14 @@ struct EpiResid {  // x[j][i..i+3] += v + bias
     const float* bias;
     float* x;
     int ld;
-    __device__ void operator()(int i, int j, int, float a, float b, float c, float e) const {
-        float* p = x + (long long)j * ld + i;
-        const float4 o = ld4(p);
-        const float* bb = bias + i;
-        st4(p, o.x + a + bb[0], o.y + b + bb[1], o.z + c + bb[2], o.w + e + bb[3]);
+    __device__ EpiPre pre(int i, int j, int) const {
+        EpiPre p{};
+        p.a = ld4(bias + i);
+        p.b = ld4(x + (long long)j * ld + i);
+        return p;
+    }
+    __device__ void operator()(int i, int j, int, float a, float b, float c, float e, const EpiPre& p) const {
+        st4(x + (long long)j * ld + i, p.b.x + a + p.a.x, p.b.y + b + p.a.y, p.b.z + c + p.a.z, p.b.w + e + p.a.w);
     }
 };
 
@@ -120,10 +142,10 @@ struct EpiGelu {  // out[j][i..i+3] = gelu(v + bias)
     const float* bias;
     T* out;
     int ld;
-    __device__ void operator()(int i, int j, int, float a, float b, float c, float e) const {
-        const float* bb = bias + i;
-        st4(out + (long long)j * ld + i, gelu_erf(a + bb[0]), gelu_erf(b + bb[1]), gelu_erf(c + bb[2]),
-            gelu_erf(e + bb[3]));
+    __device__ EpiPre pre(int i, int, int) const { EpiPre p{}; p.a = ld4(bias + i); return p; }
+    __device__ void operator()(int i, int j, int, float a, float b, float c, float e, const EpiPre& p) const {
+        st4(out + (long long)j * ld + i, gelu_erf(a + p.a.x), gelu_erf(b + p.a.y), gelu_erf(c + p.a.z),
+            gelu_erf(e + p.a.w));
     }
 };
 
@@ -132,10 +154,11 @@ struct EpiCrossK {  // A = encoder output (4 consecutive positions), B = [Wk of 
     T* kt;               // cross K cache
     const int* slot_of;  // batch entry -> slot
     int d, H, S;
-    __device__ void operator()(int m, int n, int, float a, float b, float c, float e) const {
+    __device__ EpiPre pre(int m, int, int) const { EpiPre p{}; p.s = slot_of[m / N_CTX]; return p; }
+    __device__ void operator()(int m, int n, int, float a, float b, float c, float e, const EpiPre& p) const {
         const int bseg = m / N_CTX, t = m - bseg * N_CTX;
         const int l = n / d, f = n - l * d, h = f >> 6, jj = f & 63;
-        const long long base = (((long long)l * S + slot_of[bseg]) * H + h) * 64 + jj;
+        const long long base = (((long long)l * S + p.s) * H + h) * 64 + jj;
         st4(kt + base * TC + t, a, b, c, e);
     }
 };
@@ -146,12 +169,17 @@ struct EpiCrossV {  // A = [Wv of every layer], B = encoder output
     T* v;             // cross V cache
     const int* slot_of;
     int d, H, S;
-    __device__ void operator()(int n, int m, int, float a, float b, float c, float e) const {
+    __device__ EpiPre pre(int n, int m, int) const {
+        EpiPre p{};
+        p.a = ld4(bv + n);
+        p.s = slot_of[m / N_CTX];
+        return p;
+    }
+    __device__ void operator()(int n, int m, int, float a, float b, float c, float e, const EpiPre& p) const {
         const int bseg = m / N_CTX, t = m - bseg * N_CTX;
         const int l = n / d, f = n - l * d, h = f >> 6, jj = f & 63;
-        const long long row = (((long long)l * S + slot_of[bseg]) * H + h) * TC + t;
-        const float* bb = bv + n;
-        st4(v + row * 64 + jj, a + bb[0], b + bb[1], c + bb[2], e + bb[3]);
+        const long long row = (((long long)l * S + p.s) * H + h) * TC + t;
+        st4(v + row * 64 + jj, a + p.a.x, b + p.a.y, c + p.a.z, e + p.a.w);
     }
 };
 
@@ -168,25 +196,33 @@ struct EpiDecQKV {
     const int* list;
     const int* pos;
     int d, H;
-    __device__ void operator()(int i, int r, int, float a, float b, float c, float e) const {
+    __device__ EpiPre pre(int i, int r, int) const {
+        EpiPre p{};
         if (i < d) {
-            const float* bb = bq + i;
-            st4(q + (long long)r * d + i, (a + bb[0]) * 0.125f, (b + bb[1]) * 0.125f,
-                (c + bb[2]) * 0.125f, (e + bb[3]) * 0.125f);
+            p.a = ld4(bq + i);
+        } else {
+            p.s = pos[list[r]];
+            if (i >= 2 * d) p.a = ld4(bv + (i - 2 * d));
+        }
+        return p;
+    }
+    __device__ void operator()(int i, int r, int, float a, float b, float c, float e, const EpiPre& p) const {
+        if (i < d) {
+            st4(q + (long long)r * d + i, (a + p.a.x) * 0.125f, (b + p.a.y) * 0.125f, (c + p.a.z) * 0.125f,
+                (e + p.a.w) * 0.125f);
             return;
         }
-        const int s = list[r], p = pos[s];
+        const int s = list[r], ps = p.s;
         if (i < 2 * d) {
             const int f = i - d, h = f >> 6, jj = f & 63;
-            T* base = kt + (((long long)s * H + h) * 64 + jj) * TS + p;
+            T* base = kt + (((long long)s * H + h) * 64 + jj) * TS + ps;
             stf(base, a);
             stf(base + TS, b);
             stf(base + 2 * TS, c);
             stf(base + 3 * TS, e);
         } else {
             const int f = i - 2 * d, h = f >> 6, jj = f & 63;
-            const float* bb = bv + f;
-            st4(v + (((long long)s * H + h) * TS + p) * 64 + jj, a + bb[0], b + bb[1], c + bb[2], e + bb[3]);
+            st4(v + (((long long)s * H + h) * TS + ps) * 64 + jj, a + p.a.x, b + p.a.y, c + p.a.z, e + p.a.w);
         }
     }
 };
@@ -196,17 +232,18 @@ struct EpiQ {  // cross-attention queries, scaled by 1/8
     const float* bias;
     T* q;
     int d;
-    __device__ void operator()(int i, int r, int, float a, float b, float c, float e) const {
-        const float* bb = bias + i;
-        st4(q + (long long)r * d + i, (a + bb[0]) * 0.125f, (b + bb[1]) * 0.125f, (c + bb[2]) * 0.125f,
-            (e + bb[3]) * 0.125f);
+    __device__ EpiPre pre(int i, int, int) const { EpiPre p{}; p.a = ld4(bias + i); return p; }
+    __device__ void operator()(int i, int r, int, float a, float b, float c, float e, const EpiPre& p) const {
+        st4(q + (long long)r * d + i, (a + p.a.x) * 0.125f, (b + p.a.y) * 0.125f, (c + p.a.z) * 0.125f,
+            (e + p.a.w) * 0.125f);
     }
 };
 
 struct EpiLogits {  // out[r][i..i+3] (fp32), rows beyond n_vocab dropped
     float* out;
     int V;
-    __device__ void operator()(int i, int r, int, float a, float b, float c, float e) const {
+    __device__ EpiPre pre(int, int, int) const { return EpiPre{}; }
+    __device__ void operator()(int i, int r, int, float a, float b, float c, float e, const EpiPre&) const {
         float* p = out + (long long)r * V + i;
         if (i + 3 < V) {
             p[0] = a; p[1] = b; p[2] = c; p[3] = e;

@@ -3,14 +3,16 @@
 //
 // The result never goes to memory as a plain matrix: an epilogue functor
 // receives each lane's output as four consecutive i for one j,
-//     epi(i0, j, z, v0, v1, v2, v3)   (rows i0..i0+3 of batch z, column j),
+//     p = epi.pre(i0, j, z); epi(i0, j, z, v0, v1, v2, v3, p)
+// (rows i0..i0+3 of batch z, column j; pre() issues the loads first),
 // and stores it in whatever layout the consumer wants (bias, GELU, residual
 // add, per-head or transposed cache layouts). Call sites pick which operand
 // is A so that the four consecutive i are the contiguous output dimension.
 //
 // gemm_bf16: bf16 inputs, v_mfma_f32_16x16x32_bf16 with fp32 accumulation,
-//   256x256x64 workgroup tile, 4 waves of 128x128, LDS double buffer with an
-//   XOR swizzle on 16-byte chunks, next K tile prefetched into registers.
+//   256x256 workgroup tile, 4 waves of 128x128, K tiles of 32 streamed into a
+//   4-stage LDS ring with direct global->LDS loads (three tiles in flight, no
+//   staging registers), 16-byte chunks XOR-swizzled against bank conflicts.
 //   Requires K % 64 == 0, MA % 4 == 0, 16-byte aligned rows (lda, ldb % 8 == 0).
 // gemm_simt: fp32 (or bf16 storage) SIMT kernel for the fp32 model and the
 //   front end: 64x64x16 tile, 4x4 outputs per thread, any K, any lda.
@@ -28,28 +30,40 @@ typedef float mfma_f32x4 __attribute__((ext_vector_type(4)));
 namespace gb {
 constexpr int BM = 256;   // A rows per workgroup
 constexpr int BN = 256;   // B rows per workgroup
-constexpr int BK = 64;
+constexpr int BK = 32;    // K per LDS stage
+constexpr int NS = 4;     // LDS stages
 constexpr int THREADS = 256;
-constexpr int TILE_BYTES = BM * BK * 2;  // one operand tile (32 KiB)
+constexpr int TILE_BYTES = BM * BK * 2;        // one operand tile of a stage (16 KiB)
+constexpr int STAGE_BYTES = 2 * TILE_BYTES;    // A and B tiles (32 KiB)
+constexpr int LDS_BYTES = NS * STAGE_BYTES;    // 128 KiB
 }  // namespace gb
+
+// Byte offset of 16-byte chunk c (0..3) of row r in a [rows][32] bf16 LDS tile:
+// position c ^ ((r >> 1) & 3), so the 8 rows read together by a ds_read_b128
+// group hit distinct banks.
+__device__ inline int swz32(int r, int c) { return r * 64 + ((c ^ ((r >> 1) & 3)) << 4); }
+
+// s_waitcnt immediate that waits until at most n vector-memory ops are outstanding.
+#define WMI_VMCNT(n) ((((n) & 0xF)) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
 
 // Byte offset of 16-byte chunk c (0..7) of row r inside a [rows][64] bf16 LDS tile.
 __device__ inline int swz(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
 
-// Eight 16-byte staging registers (named, so they never land in scratch).
-struct Stage8 {
-    u32x4 v0, v1, v2, v3, v4, v5, v6, v7;
-};
-// Loads 16-byte chunks of rows r0, r0 + 32, ..., r0 + 224 (clamped to nrows - 1).
-__device__ __forceinline__ void gload8(Stage8& g, const bf16* p, int r0, int nrows, int ld, int k0) {
-#define WMI_L(S) g.v##S = *reinterpret_cast<const u32x4*>(p + (long long)min(r0 + 32 * S, nrows - 1) * ld + k0)
-    WMI_L(0); WMI_L(1); WMI_L(2); WMI_L(3); WMI_L(4); WMI_L(5); WMI_L(6); WMI_L(7);
-#undef WMI_L
+// A and B fragments of one 32-wide K tile for this wave (rows wa.., wb..).
+__device__ __forceinline__ void load_frags(mfma_bf16x8 (&fa)[8], mfma_bf16x8 (&fb)[8], const unsigned char* stage,
+                                           int wa, int wb, int fr, int fc) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) fa[i] = *reinterpret_cast<const mfma_bf16x8*>(stage + swz32(wa + i * 16 + fr, fc));
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        fb[j] = *reinterpret_cast<const mfma_bf16x8*>(stage + gb::TILE_BYTES + swz32(wb + j * 16 + fr, fc));
 }
-__device__ __forceinline__ void lstore8(const Stage8& g, unsigned char* dst, int lr, int lc) {
-#define WMI_S(S) *reinterpret_cast<u32x4*>(dst + swz(lr + 32 * S, lc)) = g.v##S
-    WMI_S(0); WMI_S(1); WMI_S(2); WMI_S(3); WMI_S(4); WMI_S(5); WMI_S(6); WMI_S(7);
-#undef WMI_S
+__device__ __forceinline__ void mfma_8x8(mfma_f32x4 (&acc)[8][8], const mfma_bf16x8 (&fa)[8],
+                                         const mfma_bf16x8 (&fb)[8]) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
 }
 
 template <class Epi>
@@ -66,13 +80,23 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
     const int a0 = ta * gb::BM, b0 = tb * gb::BN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wa = (wave & 1) * 128, wb = (wave >> 1) * 128;
+    const int fr = lane & 15, fc = lane >> 4;  // fragment row, 8-element k group
 
-    // Global -> register staging: thread copies 16-byte chunk (tid & 7) of
-    // rows (tid >> 3) + 32 * s, s = 0..7 (rows past the end re-read the last row).
-    const int lc = tid & 7, lr = tid >> 3;
-    const bf16* Ab = A + lc * 8;
-    const bf16* Bb = B + lc * 8;
-    Stage8 stg;
+    // Direct loads: one wave instruction fills 1 KiB of LDS (16 rows x 64 B),
+    // lane i landing at byte 16 i. Wave w fills rows 64 w .. 64 w + 63 of both
+    // operand tiles with 4 + 4 instructions; lane i loads row 16 s + i / 4 and
+    // the logical chunk stored at its physical position i % 4.
+    const int dr = lane >> 2;
+    const int dc = (lane & 3) ^ ((dr >> 1) & 3);
+    const bf16* ga[4];
+    const bf16* gp[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const int r = wave * 64 + s * 16 + dr;
+        ga[s] = A + (long long)min(a0 + r, MA - 1) * lda + dc * 8;
+        gp[s] = B + (long long)min(b0 + r, MB - 1) * ldb + dc * 8;
+    }
+    const int ldsw = wave * 64 * 64;  // byte offset of this wave's rows in a tile
 
     mfma_f32x4 acc[8][8];
 #pragma unroll
@@ -80,54 +104,51 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[i][j] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
 
-#define WMI_GLOAD(P, ROW0, NROWS, LD, K0) gload8(stg, (P), (ROW0) + lr, (NROWS), (LD), (K0))
-#define WMI_LSTORE(DST) lstore8(stg, (DST), lr, lc)
+#define WMI_ISSUE(KT)                                                                                  \
+    do {                                                                                               \
+        const int st_ = ((KT) % gb::NS) * gb::STAGE_BYTES + ldsw;                                      \
+        const int k_ = (KT) * gb::BK;                                                                  \
+        _Pragma("unroll") for (int s = 0; s < 4; ++s)                                                 \
+            __builtin_amdgcn_global_load_lds(ga[s] + k_, lds + st_ + s * 1024, 16, 0, 0);              \
+        _Pragma("unroll") for (int s = 0; s < 4; ++s)                                                 \
+            __builtin_amdgcn_global_load_lds(gp[s] + k_, lds + st_ + gb::TILE_BYTES + s * 1024, 16, 0, 0); \
+    } while (0)
 
     const int nk = K / gb::BK;
-    WMI_GLOAD(Ab, a0, MA, lda, 0);
-    WMI_LSTORE(lds);
-    WMI_GLOAD(Bb, b0, MB, ldb, 0);
-    WMI_LSTORE(lds + gb::TILE_BYTES);
-    __syncthreads();
-    const int fr = lane & 15, fc = lane >> 4;  // fragment row, 8-element k group
+    WMI_ISSUE(0);
+    if (nk > 1) WMI_ISSUE(1);
+    if (nk > 2) WMI_ISSUE(2);
     for (int kt = 0; kt < nk; ++kt) {
-        const bool more = kt + 1 < nk;
-        const unsigned char* ta_ = lds + (kt & 1) * 2 * gb::TILE_BYTES;
-        const unsigned char* tb_ = ta_ + gb::TILE_BYTES;
-        unsigned char* na_ = lds + ((kt + 1) & 1) * 2 * gb::TILE_BYTES;
-        if (more) WMI_GLOAD(Ab, a0, MA, lda, (kt + 1) * gb::BK);
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            mfma_bf16x8 fa[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                fa[i] = *reinterpret_cast<const mfma_bf16x8*>(ta_ + swz(wa + i * 16 + fr, ks * 4 + fc));
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const mfma_bf16x8 fb = *reinterpret_cast<const mfma_bf16x8*>(tb_ + swz(wb + j * 16 + fr, ks * 4 + fc));
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb, acc[i][j], 0, 0, 0);
-            }
-            if (ks == 0 && more) {
-                WMI_LSTORE(na_);
-                WMI_GLOAD(Bb, b0, MB, ldb, (kt + 1) * gb::BK);
-            }
-        }
-        if (more) WMI_LSTORE(na_ + gb::TILE_BYTES);
-        __syncthreads();
+        // tile kt has landed once only the 8-load groups of later tiles are pending
+        const int later = min(nk - 1 - kt, gb::NS - 2);
+        if (later >= 2) __builtin_amdgcn_s_waitcnt(WMI_VMCNT(16));
+        else if (later == 1) __builtin_amdgcn_s_waitcnt(WMI_VMCNT(8));
+        else __builtin_amdgcn_s_waitcnt(WMI_VMCNT(0));
+        // every wave's part of tile kt is in LDS, and every wave is done with tile kt - 1
+        __builtin_amdgcn_s_barrier();
+        if (kt + gb::NS - 1 < nk) WMI_ISSUE(kt + gb::NS - 1);
+        mfma_bf16x8 fa[8], fb[8];
+        load_frags(fa, fb, lds + (kt % gb::NS) * gb::STAGE_BYTES, wa, wb, fr, fc);
+        __builtin_amdgcn_sched_barrier(0);  // every fragment read is issued ahead of the MFMAs
+        mfma_8x8(acc, fa, fb);
     }
-#undef WMI_GLOAD
-#undef WMI_LSTORE
-    // Lane holds C[i = base + 4*(lane>>4) + r][j = base + (lane & 15)].
+#undef WMI_ISSUE
+    // Lane holds C[i = base + 4*(lane>>4) + r][j = base + (lane & 15)]; the
+    // epilogue's loads for 8 fragments are issued before their stores.
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const int jj = b0 + wb + j * 16 + fr;
-        if (jj >= MB) continue;
+        const bool jok = jj < MB;
+        EpiPre pre[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int ii = a0 + wa + i * 16 + fc * 4;
-            if (ii < MA) epi(ii, jj, z, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            if (jok && ii < MA) pre[i] = epi.pre(ii, jj, z);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int ii = a0 + wa + i * 16 + fc * 4;
+            if (jok && ii < MA) epi(ii, jj, z, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], pre[i]);
         }
     }
 }
@@ -135,17 +156,17 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
 template <class Epi>
 inline void gemm_bf16(const bf16* A, int lda, long long sA, const bf16* B, int ldb, long long sB,
                       int MA, int MB, int K, int batch, const Epi& epi, hipStream_t st) {
-    if (K % gb::BK || MA % 4 || lda % 8 || ldb % 8 || MA <= 0 || MB <= 0 || batch <= 0)
+    if (K % 64 || MA % 4 || lda % 8 || ldb % 8 || MA <= 0 || MB <= 0 || batch <= 0)
         throw ArgError(-1, "gemm_bf16: unsupported shape");
     const int tilesA = (MA + gb::BM - 1) / gb::BM, tilesB = (MB + gb::BN - 1) / gb::BN;
     static bool attr_set = false;  // one per epilogue instantiation
     if (!attr_set) {
         WMI_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<Epi>),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, 4 * gb::TILE_BYTES));
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, gb::LDS_BYTES));
         attr_set = true;
     }
     dim3 grid(tilesA * tilesB, 1, batch);
-    hipLaunchKernelGGL(gemm_bf16_kernel<Epi>, grid, dim3(gb::THREADS), 4 * gb::TILE_BYTES, st, A, lda,
+    hipLaunchKernelGGL(gemm_bf16_kernel<Epi>, grid, dim3(gb::THREADS), gb::LDS_BYTES, st, A, lda,
                        sA, B, ldb, sB, MA, MB, K, tilesA, epi);
 }
 
@@ -188,10 +209,16 @@ __global__ __launch_bounds__(256) void gemm_simt_kernel(const TA* __restrict__ A
     }
     const int ii = a0 + ag * 4;
     if (ii >= MA) return;
+    EpiPre pre[4];
 #pragma unroll
     for (int y = 0; y < 4; ++y) {
         const int jj = b0 + bgp * 4 + y;
-        if (jj < MB) epi(ii, jj, z, acc[0][y], acc[1][y], acc[2][y], acc[3][y]);
+        if (jj < MB) pre[y] = epi.pre(ii, jj, z);
+    }
+#pragma unroll
+    for (int y = 0; y < 4; ++y) {
+        const int jj = b0 + bgp * 4 + y;
+        if (jj < MB) epi(ii, jj, z, acc[0][y], acc[1][y], acc[2][y], acc[3][y], pre[y]);
     }
 }
 

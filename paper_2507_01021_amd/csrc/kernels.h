@@ -695,6 +695,14 @@ __global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict
     }
     __syncthreads();
     if (wave > 0) return;
+    EpiPre pre[RT][NT];
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int u = 0; u < NT; ++u) {
+            const int i = i0 + t * 16 + fc * 4, r = u * 16 + fr;
+            if (i < MA && r < n) pre[t][u] = epi.pre(i, r, blockIdx.y);
+        }
 #pragma unroll
     for (int t = 0; t < RT; ++t)
 #pragma unroll
@@ -706,7 +714,7 @@ __global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict
                 v[e] = ((acc[t][u][e] + red[0][idx][lane]) + red[1][idx][lane]) + red[2][idx][lane];
             }
             const int i = i0 + t * 16 + fc * 4, r = u * 16 + fr;
-            if (i < MA && r < n) epi(i, r, blockIdx.y, v[0], v[1], v[2], v[3]);
+            if (i < MA && r < n) epi(i, r, blockIdx.y, v[0], v[1], v[2], v[3], pre[t][u]);
         }
 }
 
@@ -714,7 +722,8 @@ __global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict
 struct EpiPartial {
     float* part;
     int N, n;
-    __device__ void operator()(int i, int r, int ks, float a, float b, float c, float e) const {
+    __device__ EpiPre pre(int, int, int) const { return EpiPre{}; }
+    __device__ void operator()(int i, int r, int ks, float a, float b, float c, float e, const EpiPre&) const {
         st4(part + ((long long)ks * n + r) * N + i, a, b, c, e);
     }
 };
