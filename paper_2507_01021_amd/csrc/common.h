@@ -48,6 +48,23 @@ template <> struct St<bf16> {
 template <class T> __device__ inline float ldf(const T* p) { return St<T>::ld(p); }
 template <class T> __device__ inline void stf(T* p, float v) { St<T>::st(p, v); }
 
+// Fragment-major layout of a matrix with K columns (K % 32 == 0), used for
+// the bf16 decoder's projection weights and for the activations they
+// multiply: the 16-row x 32-column block (row tile r / 16, k-step k / 32)
+// is 1 KiB contiguous and holds, at byte 16 * l, what lane l of a 16x16x32
+// MFMA operand needs (row l % 16, columns 8 * (l / 16) .. + 7). One
+// operand fragment is therefore one fully contiguous 1 KiB load. Row tiles
+// are stored one after another, each with all K / 32 k-steps.
+__host__ __device__ inline long long frag_off(long long r, int k, int K) {
+    return (((r >> 4) * (K >> 5) + (k >> 5)) * 64 + ((k >> 3) & 3) * 16 + (r & 15)) * 8 + (k & 7);
+}
+// Decoder matrices: fragment-major when stored as bf16, row-major as fp32.
+template <class T>
+__host__ __device__ inline long long dec_off(long long r, int k, int K) {
+    if constexpr (sizeof(T) == 2) return frag_off(r, k, K);
+    else return r * K + k;
+}
+
 // Native vectors (plain loads/stores; HIP's uint4 struct copies as memcpy).
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));

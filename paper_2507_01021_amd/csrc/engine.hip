@@ -16,6 +16,8 @@
 //   1500 cached encoder positions (chunked + combine), output projection +
 //   residual, LN, fc1 + GELU, fc2 + residual -> final LN -> logits against
 //   the token embedding -> argmax, next input, position advance.
+//   In bf16 the projection weights and the activations they multiply are
+//   fragment-major (frag_off).
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
@@ -291,24 +293,22 @@ class EngineT final : public Engine {
             const DecLayerW<T>& L = dec_[l];
             const long long sl = (long long)l * S_ * H_ * 64;
             proj(L.Wqkv, 3 * d, dz_, n, d, 1,
-                 EpiDecQKV<T>{L.bq, L.bv, dq_, kts_ + sl * TS, vs_ + sl * TS, list_, pos_, d, H_});
-            DecAttnArgs sa{dq_, kts_ + sl * TS, vs_ + sl * TS, datt_, list_, pos_, TS, H_, d};
+                 EpiDecQKV<T>{L.bq, L.bv, dq_, kts_ + sl * TS, vs_ + sl * TS, list_, pos_, rowlen_, d, H_});
+            DecAttnArgs sa{dq_, kts_ + sl * TS, vs_ + sl * TS, datt_, list_, rowlen_, TS, H_, d};
             prof_begin(WHISPER_K_SELF_ATTN);
             hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, st_, sa);
             prof_end(WHISPER_K_SELF_ATTN);
-            proj(L.Wo, d, datt_, n, d, ks1, EpiPartial{gpart_, d, n});
-            resid_ln(ks1, n, L.bo, L.ln2g, L.ln2b);
+            proj_resid(L.Wo, datt_, n, d, ks1, L.bo, L.ln2g, L.ln2b);
             proj(L.Wcq, d, dz_, n, d, 1, EpiQ<T>{L.cbq, dq_, d});
             DecAttnArgs ca{dq_, ktc_ + sl * TC, vc_ + sl * TC, datt_, list_, nullptr, TC, H_, d};
             prof_begin(WHISPER_K_CROSS_ATTN);
             hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, st_, ca);
             prof_end(WHISPER_K_CROSS_ATTN);
-            proj(L.Wco, d, datt_, n, d, ks1, EpiPartial{gpart_, d, n});
-            resid_ln(ks1, n, L.cbo, L.ln3g, L.ln3b);
-            proj(L.W1, 4 * d, dz_, n, d, 1, EpiGelu<T>{L.b1, dh_, 4 * d});
-            proj(L.W2, d, dh_, n, 4 * d, ks4, EpiPartial{gpart_, d, n});
+            proj_resid(L.Wco, datt_, n, d, ks1, L.cbo, L.ln3g, L.ln3b);
+            proj(L.W1, 4 * d, dz_, n, d, 1, EpiGelu<T, true>{L.b1, dh_, 4 * d});
             const bool last = l + 1 == Ld_;
-            resid_ln(ks4, n, L.b2, last ? lnfg_ : dec_[l + 1].ln1g, last ? lnfb_ : dec_[l + 1].ln1b);
+            proj_resid(L.W2, dh_, n, 4 * d, ks4, L.b2, last ? lnfg_ : dec_[l + 1].ln1g,
+                       last ? lnfb_ : dec_[l + 1].ln1b);
         }
         proj(tok_emb_, V_, dz_, n, d, 1, EpiLogits{logits_, V_});
         hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, st_, logits_, V_, best_);
@@ -437,7 +437,7 @@ class EngineT final : public Engine {
     T *ypad_, *h1_, *zb_, *qh_, *kh_, *vt_, *ob_, *hb_;
     int last_nb_ = 0;
     // decoder state and workspace
-    int *seq_, *gen_, *pos_, *npr_, *list_, *forced_, *outtok_;
+    int *seq_, *gen_, *pos_, *npr_, *list_, *forced_, *outtok_, *rowlen_;
     T *kts_, *vs_, *ktc_, *vc_, *dz_, *dq_, *datt_, *dh_;
     float *dx_, *logits_, *gpart_;
     unsigned long long* best_;
@@ -532,11 +532,11 @@ class EngineT final : public Engine {
     // decoder: x += split-K partials + bias, then z = LN(x)
     void resid_ln(int KS, int n, const float* bias, const float* g, const float* b) {
         if (KS == 4) {
-            WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 4>), dim3(n), dim3(64), 0, st_, gpart_, n,
-                                                bias, dx_, dz_, g, b));
+            WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 4>), dim3(n), dim3(resid_ln_threads<E>()), 0,
+                                                st_, gpart_, n, bias, dx_, dz_, g, b));
         } else {
-            WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 1>), dim3(n), dim3(64), 0, st_, gpart_, n,
-                                                bias, dx_, dz_, g, b));
+            WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 1>), dim3(n), dim3(resid_ln_threads<E>()), 0,
+                                                st_, gpart_, n, bias, dx_, dz_, g, b));
         }
     }
     // split factor of a decode projection with reduction length K
@@ -554,6 +554,11 @@ class EngineT final : public Engine {
     void proj(const T* W, int MA, const T* X, int n, int K, int KS, const Epi& epi) {
         if constexpr (std::is_same<T, bf16>::value) skinny_bf16(W, MA, X, n, K, KS, epi, st_);
         else gemm_simt(W, K, K / KS, X, K, K / KS, MA, n, K / KS, KS, epi, st_);
+    }
+    // residual projection: x += W X + bias (split-K partials), then z = LN(x)
+    void proj_resid(const T* W, const T* X, int n, int K, int KS, const float* bias, const float* g, const float* b) {
+        proj(W, d_, X, n, K, KS, EpiPartial{gpart_, d_, n});
+        resid_ln(KS, n, bias, g, b);
     }
 
     void encode_pass(const SegmentDesc* segs, int nb, const int* slots) {
@@ -655,6 +660,29 @@ class EngineT final : public Engine {
             }
             return q;
         };
+        // Decoder projection matrices with K columns (rows of the named tensors
+        // stacked) in the decoder layout: bf16 fragment-major with the rows
+        // padded with zeros to a multiple of 32, fp32 row-major.
+        auto dec_mat = [&](const std::vector<std::string>& names, int K) -> T* {
+            if constexpr (!std::is_same<T, bf16>::value) {
+                return cat(names);
+            } else {
+                size_t rows = 0;
+                for (auto& nme : names) rows += count(nme) / K;
+                std::vector<T> h((rows + 31) / 32 * 32 * K);
+                memset(h.data(), 0, h.size() * sizeof(T));
+                size_t r0 = 0;
+                for (auto& nme : names) {
+                    const T* src = raw(nme);
+                    const size_t nr = count(nme) / K;
+                    for (size_t r = 0; r < nr; ++r)
+                        for (int k = 0; k < K; k += 8)
+                            memcpy(&h[frag_off(r0 + r, k, K)], src + r * K + k, 8 * sizeof(T));
+                    r0 += nr;
+                }
+                return upload_new(h);
+            }
+        };
         const int d = d_;
         {  // conv kernels to [out][tap][in] (input channels of conv1 padded to CP)
             std::vector<T> w1((size_t)d * 3 * CP);
@@ -688,7 +716,7 @@ class EngineT final : public Engine {
         }
         lnpg_ = vecf("enc.ln_post.g");
         lnpb_ = vecf("enc.ln_post.b");
-        tok_emb_ = mat("dec.tok_emb");
+        tok_emb_ = dec_mat({"dec.tok_emb"}, d);
         pos_emb_ = mat("dec.pos_emb");
         std::vector<std::string> ck, cv;
         std::vector<float> bcv;
@@ -696,15 +724,15 @@ class EngineT final : public Engine {
             const std::string p = "dec." + std::to_string(i);
             DecLayerW<T> L;
             L.ln1g = vecf(p + ".attn_ln.g"); L.ln1b = vecf(p + ".attn_ln.b");
-            L.Wqkv = cat({p + ".attn.q.w", p + ".attn.k.w", p + ".attn.v.w"});
+            L.Wqkv = dec_mat({p + ".attn.q.w", p + ".attn.k.w", p + ".attn.v.w"}, d);
             L.bq = vecf(p + ".attn.q.b"); L.bv = vecf(p + ".attn.v.b");
-            L.Wo = mat(p + ".attn.o.w"); L.bo = vecf(p + ".attn.o.b");
+            L.Wo = dec_mat({p + ".attn.o.w"}, d); L.bo = vecf(p + ".attn.o.b");
             L.ln2g = vecf(p + ".cross_ln.g"); L.ln2b = vecf(p + ".cross_ln.b");
-            L.Wcq = mat(p + ".cross.q.w"); L.cbq = vecf(p + ".cross.q.b");
-            L.Wco = mat(p + ".cross.o.w"); L.cbo = vecf(p + ".cross.o.b");
+            L.Wcq = dec_mat({p + ".cross.q.w"}, d); L.cbq = vecf(p + ".cross.q.b");
+            L.Wco = dec_mat({p + ".cross.o.w"}, d); L.cbo = vecf(p + ".cross.o.b");
             L.ln3g = vecf(p + ".mlp_ln.g"); L.ln3b = vecf(p + ".mlp_ln.b");
-            L.W1 = mat(p + ".mlp.fc1.w"); L.b1 = vecf(p + ".mlp.fc1.b");
-            L.W2 = mat(p + ".mlp.fc2.w"); L.b2 = vecf(p + ".mlp.fc2.b");
+            L.W1 = dec_mat({p + ".mlp.fc1.w"}, d); L.b1 = vecf(p + ".mlp.fc1.b");
+            L.W2 = dec_mat({p + ".mlp.fc2.w"}, 4 * d); L.b2 = vecf(p + ".mlp.fc2.b");
             dec_.push_back(L);
             ck.push_back(p + ".cross.k.w");
             cv.push_back(p + ".cross.v.w");
@@ -748,17 +776,20 @@ class EngineT final : public Engine {
         list_ = dalloc<int>(S);
         forced_ = dalloc<int>(S);
         outtok_ = dalloc<int>(S);
+        rowlen_ = dalloc<int>(S);
         kts_ = dalloc<T>(Ld * S * H * 64 * TS);
         vs_ = dalloc<T>(Ld * S * H * TS * 64);
         ktc_ = dalloc<T>(Ld * S * H * 64 * TC);
         vc_ = dalloc<T>(Ld * S * H * TC * 64);
+        // activations multiplied by projections: whole 16-row tiles (fragment-major in bf16)
+        const size_t S16 = (S + 15) / 16 * 16;
         dx_ = dalloc<float>(S * d);
-        dz_ = dalloc<T>(S * d);
+        dz_ = dalloc<T>(S16 * d);
         dq_ = dalloc<T>(S * d);
-        datt_ = dalloc<T>(S * d);
-        dh_ = dalloc<T>(S * 4 * d);
+        datt_ = dalloc<T>(S16 * d);
+        dh_ = dalloc<T>(S16 * 4 * d);
         logits_ = dalloc<float>(S * (size_t)V_);
-        gpart_ = dalloc<float>(4 * S * d);
+        gpart_ = dalloc<float>(4 * S * d);  // split-K partials [4][S][d]
         best_ = dalloc<unsigned long long>(S);
     }
 };

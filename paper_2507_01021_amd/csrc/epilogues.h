@@ -137,15 +137,16 @@ struct EpiResid {  // x[j][i..i+3] += v + bias
     }
 };
 
-template <class T>
-struct EpiGelu {  // out[j][i..i+3] = gelu(v + bias)
+// out[j][i..i+3] = gelu(v + bias); DEC: out is a decoder activation (dec_off), else row-major.
+template <class T, bool DEC = false>
+struct EpiGelu {
     const float* bias;
     T* out;
     int ld;
     __device__ EpiPre pre(int i, int, int) const { EpiPre p{}; p.a = ld4(bias + i); return p; }
     __device__ void operator()(int i, int j, int, float a, float b, float c, float e, const EpiPre& p) const {
-        st4(out + (long long)j * ld + i, gelu_erf(a + p.a.x), gelu_erf(b + p.a.y), gelu_erf(c + p.a.z),
-            gelu_erf(e + p.a.w));
+        st4(out + (DEC ? dec_off<T>(j, i, ld) : (long long)j * ld + i), gelu_erf(a + p.a.x), gelu_erf(b + p.a.y),
+            gelu_erf(c + p.a.z), gelu_erf(e + p.a.w));
     }
 };
 
@@ -185,7 +186,8 @@ struct EpiCrossV {  // A = [Wv of every layer], B = encoder output
 
 // Decoder: A = [Wq; Wk; Wv] of one layer, B = normalised rows (row r -> slot list[r]).
 // Queries go to q (scaled by 1/8); this position's key and value are appended
-// to the slot's self-attention cache.
+// to the slot's self-attention cache, and rowlen[r] = position + 1 (the
+// number of cached positions the row attends to).
 template <class T>
 struct EpiDecQKV {
     const float* bq;
@@ -195,6 +197,7 @@ struct EpiDecQKV {
     T* v;   // self V cache of this layer: [S][H][TS][64]
     const int* list;
     const int* pos;
+    int* rowlen;
     int d, H;
     __device__ EpiPre pre(int i, int r, int) const {
         EpiPre p{};
@@ -213,6 +216,7 @@ struct EpiDecQKV {
             return;
         }
         const int s = list[r], ps = p.s;
+        if (i == d) rowlen[r] = ps + 1;
         if (i < 2 * d) {
             const int f = i - d, h = f >> 6, jj = f & 63;
             T* base = kt + (((long long)s * H + h) * 64 + jj) * TS + ps;

@@ -80,9 +80,30 @@ __global__ __launch_bounds__(1024) void mel_norm_kernel(float* __restrict__ logm
 // (two passes over registers), eps 1e-5, gain and bias. E is a compile-time
 // constant so every load of a row is issued before the first use.
 
-template <int E, class T>
+// Layer norm of row `row` held in registers (element lane + 64 e) with
+// gain/bias already loaded; DEC: y is a decoder activation (dec_off layout),
+// else row-major.
+template <int E, bool DEC, class T>
+__device__ __forceinline__ void ln_row_apply(const float (&v)[E], int lane, int d, const float (&gg)[E],
+                                             const float (&bb)[E], T* __restrict__ y, int row) {
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) s += v[e];
+    const float mean = wave_sum(s) / d;
+    float q = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) { const float c = v[e] - mean; q += c * c; }
+    const float rstd = rsqrtf(wave_sum(q) / d + 1e-5f);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int c = lane + 64 * e;
+        stf(y + (DEC ? dec_off<T>(row, c, d) : (long long)row * d + c), (v[e] - mean) * rstd * gg[e] + bb[e]);
+    }
+}
+
+template <int E, bool DEC, class T>
 __device__ __forceinline__ void ln_row_store(const float (&v)[E], int lane, int d, const float* __restrict__ g,
-                                             const float* __restrict__ b, T* __restrict__ yr) {
+                                             const float* __restrict__ b, T* __restrict__ y, int row) {
     float s = 0.f;
 #pragma unroll
     for (int e = 0; e < E; ++e) s += v[e];
@@ -95,7 +116,10 @@ __device__ __forceinline__ void ln_row_store(const float (&v)[E], int lane, int 
 #pragma unroll
     for (int e = 0; e < E; ++e) { gg[e] = g[lane + 64 * e]; bb[e] = b[lane + 64 * e]; }
 #pragma unroll
-    for (int e = 0; e < E; ++e) stf(yr + lane + 64 * e, (v[e] - mean) * rstd * gg[e] + bb[e]);
+    for (int e = 0; e < E; ++e) {
+        const int c = lane + 64 * e;
+        stf(y + (DEC ? dec_off<T>(row, c, d) : (long long)row * d + c), (v[e] - mean) * rstd * gg[e] + bb[e]);
+    }
 }
 
 template <class T, int E>
@@ -109,11 +133,12 @@ __global__ __launch_bounds__(256) void layer_norm_kernel(const float* __restrict
     float v[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) v[e] = xr[lane + 64 * e];
-    ln_row_store<E>(v, lane, d, g, b, y + (long long)row * d);
+    ln_row_store<E, false>(v, lane, d, g, b, y, row);
 }
 
 // Decoder input: x = token embedding + position embedding (fp32), then the
-// first layer's layer norm.
+// first layer's layer norm. The token embedding (shared with the output
+// head) and z use the decoder layout (dec_off); x and pos_emb are row-major.
 template <class T, int E>
 __global__ __launch_bounds__(64) void embed_ln_kernel(const T* __restrict__ tok_emb, const T* __restrict__ pos_emb,
                                                       const int* __restrict__ list, const int* __restrict__ pos,
@@ -127,41 +152,62 @@ __global__ __launch_bounds__(64) void embed_ln_kernel(const T* __restrict__ tok_
 #pragma unroll
     for (int e = 0; e < E; ++e) {
         const int c = lane + 64 * e;
-        v[e] = ldf(tok_emb + (long long)tok * d + c) + ldf(pos_emb + (long long)p * d + c);
+        v[e] = ldf(tok_emb + dec_off<T>(tok, c, d)) + ldf(pos_emb + (long long)p * d + c);
     }
 #pragma unroll
     for (int e = 0; e < E; ++e) x[(long long)r * d + lane + 64 * e] = v[e];
-    ln_row_store<E>(v, lane, d, g, b, z + (long long)r * d);
+    ln_row_store<E, true>(v, lane, d, g, b, z, r);
 }
 
 // Residual update from split-K partial sums, then the next layer norm:
-// x[r] += sum_ks part[ks][r] + bias (partials added in ks order), z[r] = LN(x[r]).
+// x[r] += sum_ks part[ks][r] + bias (partials added in ks order), z[r] = LN(x[r])
+// (z in the decoder layout). One workgroup per row, thread t owns columns
+// 4t..4t+3, so every load of the row is a single 16-byte access issued up
+// front; mean and variance are reduced over the workgroup in a fixed order.
+template <int E>
+constexpr int resid_ln_threads() { return (16 * E + 63) / 64 * 64; }
+
 template <class T, int E, int KS>
-__global__ __launch_bounds__(64) void resid_ln_kernel(const float* __restrict__ part, int n,
-                                                      const float* __restrict__ bias, float* __restrict__ x,
-                                                      T* __restrict__ z, const float* __restrict__ g,
-                                                      const float* __restrict__ b) {
-    constexpr int d = 64 * E;
-    const int r = blockIdx.x, lane = threadIdx.x;
-    float v[E], bs[E], pk[KS][E];
+__global__ __launch_bounds__(resid_ln_threads<E>()) void resid_ln_kernel(const float* __restrict__ part, int n,
+                                                                      const float* __restrict__ bias,
+                                                                      float* __restrict__ x, T* __restrict__ z,
+                                                                      const float* __restrict__ g,
+                                                                      const float* __restrict__ b) {
+    constexpr int d = 64 * E, NW = resid_ln_threads<E>() / 64;
+    __shared__ float red[2][NW];
+    const int r = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const bool own = t < 16 * E;
+    const int c = 4 * min(t, 16 * E - 1);
+    const float4 xv = ld4(x + (long long)r * d + c), bs = ld4(bias + c), gg = ld4(g + c), bb = ld4(b + c);
+    float4 p[KS];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        v[e] = x[(long long)r * d + lane + 64 * e];
-        bs[e] = bias[lane + 64 * e];
-    }
+    for (int k = 0; k < KS; ++k) p[k] = ld4(part + ((long long)k * n + r) * d + c);
+    float4 acc = p[0];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+    for (int k = 1; k < KS; ++k) { acc.x += p[k].x; acc.y += p[k].y; acc.z += p[k].z; acc.w += p[k].w; }
+    const float v0 = xv.x + (acc.x + bs.x), v1 = xv.y + (acc.y + bs.y), v2 = xv.z + (acc.z + bs.z),
+                v3 = xv.w + (acc.w + bs.w);
+    if (own) st4(x + (long long)r * d + c, v0, v1, v2, v3);
+    float s = own ? (v0 + v1) + (v2 + v3) : 0.f;
+    s = wave_sum(s);
+    if (lane == 0) red[0][w] = s;
+    __syncthreads();
+    float tot = red[0][0];
 #pragma unroll
-        for (int e = 0; e < E; ++e) pk[ks][e] = part[((long long)ks * n + r) * d + lane + 64 * e];
+    for (int i = 1; i < NW; ++i) tot += red[0][i];
+    const float mean = tot / d;
+    const float e0 = v0 - mean, e1 = v1 - mean, e2 = v2 - mean, e3 = v3 - mean;
+    float q = own ? (e0 * e0 + e1 * e1) + (e2 * e2 + e3 * e3) : 0.f;
+    q = wave_sum(q);
+    if (lane == 0) red[1][w] = q;
+    __syncthreads();
+    float qt = red[1][0];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        float acc = pk[0][e];
-#pragma unroll
-        for (int ks = 1; ks < KS; ++ks) acc += pk[ks][e];
-        v[e] += acc + bs[e];
-        x[(long long)r * d + lane + 64 * e] = v[e];
-    }
-    ln_row_store<E>(v, lane, d, g, b, z + (long long)r * d);
+    for (int i = 1; i < NW; ++i) qt += red[1][i];
+    const float rstd = rsqrtf(qt / d + 1e-5f);
+    if (own)
+        st4(z + dec_off<T>(r, c, d), e0 * rstd * gg.x + bb.x, e1 * rstd * gg.y + bb.y, e2 * rstd * gg.z + bb.z,
+            e3 * rstd * gg.w + bb.w);
 }
 
 // Dispatch on the row width d = 64 * E.
@@ -412,22 +458,46 @@ __device__ inline void load_vec<float>(const float* p, float* out, int n) {
 }
 
 struct DecAttnArgs {
-    const void* q;      // [n][d], scaled by 1/8
+    const void* q;      // [n][d] row-major, scaled by 1/8
     const void* kt;     // cache K^T of this layer: [S][H][64][TP]
     const void* v;      // cache V of this layer:   [S][H][TP][64]
-    void* out;          // [n][d]
+    void* out;          // [n][d], decoder layout (dec_off)
     const int* list;    // row -> slot
-    const int* pos;     // slot -> position (self-attention)
+    const int* rowlen;  // row -> cached positions incl. this one (self-attention)
     int TP, H, d;
 };
 
+// Eight consecutive cache elements held as loaded (bf16: one 16-byte load).
+template <class T> struct Vec8;
+template <> struct Vec8<bf16> {
+    u32x4 v;
+    __device__ void load(const bf16* p) { v = *reinterpret_cast<const u32x4*>(p); }
+    __device__ float operator[](int i) const {
+        const unsigned w = v[i >> 1];
+        return __uint_as_float((i & 1) ? (w & 0xffff0000u) : (w << 16));
+    }
+};
+template <> struct Vec8<float> {
+    float4 a, b;
+    __device__ void load(const float* p) { a = ld4(p); b = ld4(p + 4); }
+    __device__ float operator[](int i) const {
+        const float4& h = i < 4 ? a : b;
+        const int j = i & 3;
+        return j == 0 ? h.x : j == 1 ? h.y : j == 2 ? h.z : h.w;
+    }
+};
+
 // Self-attention of one decode position over the slot's cached positions
-// 0..pos (causal by construction). Workgroup = 4 waves per (row, head):
+// 0..len-1 (causal by construction). Workgroup = 4 waves per (row, head).
+// The row's slot, length and query are loaded together, then every K and V
+// load of the workgroup is issued before the first use (addresses past the
+// length are clamped to the last valid 8 positions / row, so nothing beyond
+// the slot's positions is fetched from memory):
 //   scores: wave w sums dims 16w..16w+15 for all positions (lane owns 8
-//     consecutive positions, 16 loads in flight), partials added in LDS;
+//     consecutive positions), partials added in LDS in wave order;
 //   softmax: every wave holds all scores (fp32, wavefront reductions);
 //   P V: wave w takes positions 128w..128w+127, 8 lanes per 128-byte V row,
-//     partial outputs added in LDS.
+//     partial outputs added in LDS in wave order.
 template <class T>
 __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     __shared__ float qs[64];
@@ -435,27 +505,32 @@ __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     __shared__ float op[4][64];
     const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int slot = a.list[r];
-    const int len = a.pos[slot] + 1;
-    const T* q = reinterpret_cast<const T*>(a.q) + (long long)r * a.d + h * 64;
-    if (tid < 64) qs[tid] = ldf(q + tid);
-    __syncthreads();
+    const int len = a.rowlen[r];
+    float qv = 0.f;
+    if (tid < 64) qv = ldf(reinterpret_cast<const T*>(a.q) + (long long)r * a.d + h * 64 + tid);
     const long long head = (long long)slot * a.H + h;
     const T* kt = reinterpret_cast<const T*>(a.kt) + head * 64 * a.TP;
     const T* vv = reinterpret_cast<const T*>(a.v) + head * a.TP * 64;
     const int p0 = lane * 8;
+    const int pk = min(p0, (len - 1) & ~7);
+    Vec8<T> kv[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) kv[j].load(kt + (long long)(16 * w + j) * a.TP + pk);
+    const int dg = lane & 7, pg = lane >> 3;
+    const int lo = 128 * w, hi = min(len, lo + 128);
+    Vec8<T> vr[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) vr[u].load(vv + (long long)min(lo + pg + 8 * u, len - 1) * 64 + dg * 8);
+    if (tid < 64) qs[tid] = qv;
+    __syncthreads();
     float s[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) s[i] = 0.f;
-    if (p0 < len) {
-        float kv[16][8];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) load_vec<T>(kt + (long long)(16 * w + j) * a.TP + p0, kv[j], 8);
+    for (int j = 0; j < 16; ++j) {
+        const float qj = qs[16 * w + j];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const float qj = qs[16 * w + j];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) s[i] = fmaf(qj, kv[j][i], s[i]);
-        }
+        for (int i = 0; i < 8; ++i) s[i] = fmaf(qj, kv[j][i], s[i]);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) sp[w][p0 + i] = s[i];
@@ -481,27 +556,16 @@ __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
         for (int i = 0; i < 8; ++i) sp[0][p0 + i] = s[i];
     }
     __syncthreads();
-    const int dg = lane & 7, pg = lane >> 3;
     float o[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[i] = 0.f;
-    const int lo = 128 * w, hi = min(len, lo + 128);
-    if (lo < hi) {
 #pragma unroll
-        for (int b0 = 0; b0 < 128; b0 += 64) {
-            float vr[8][8];
-            float pw[8];
+    for (int u = 0; u < 16; ++u) {
+        const int pp = lo + pg + 8 * u;
+        if (pp < hi) {
+            const float pw = sp[0][pp];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int pp = lo + b0 + pg + 8 * u;
-                const int pc = min(pp, hi - 1);
-                load_vec<T>(vv + (long long)pc * 64 + dg * 8, vr[u], 8);
-                pw[u] = pp < hi ? sp[0][pc] : 0.f;
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-#pragma unroll
-                for (int i = 0; i < 8; ++i) o[i] = fmaf(pw[u], vr[u][i], o[i]);
+            for (int i = 0; i < 8; ++i) o[i] = fmaf(pw, vr[u][i], o[i]);
         }
     }
 #pragma unroll
@@ -517,7 +581,7 @@ __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     __syncthreads();
     if (tid < 64) {
         const float v = ((op[0][tid] + op[1][tid]) + op[2][tid]) + op[3][tid];
-        stf(reinterpret_cast<T*>(a.out) + (long long)r * a.d + h * 64 + tid, v / lsum);
+        stf(reinterpret_cast<T*>(a.out) + dec_off<T>(r, h * 64 + tid, a.d), v / lsum);
     }
 }
 
@@ -620,7 +684,7 @@ __global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {
             L += wgt * ml[c][1];
             acc += wgt * op[c][tid];
         }
-        stf(reinterpret_cast<T*>(a.out) + (long long)r * a.d + h * 64 + tid, acc / L);
+        stf(reinterpret_cast<T*>(a.out) + dec_off<T>(r, h * 64 + tid, a.d), acc / L);
     }
 }
 
@@ -628,93 +692,106 @@ __global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {
 //
 // C[i][r] = sum_k W[i][k] X[r][k] for a few rows r (active decode slots,
 // n <= 16 * NT) and many weight rows i: each weight byte is read once.
-// Grid (row tiles, KS): workgroup (tile, ks) covers 16 * RT weight rows and
-// K columns [ks * K, (ks + 1) * K) of rows of length ldw / ldx. Its 4 waves
+// W and X are fragment-major (frag_off), so every load below reads 1 KiB
+// contiguous. Grid (row tiles, KS): workgroup (tile, ks) covers 16 * RT
+// weight rows and reduction columns [ks * Kc, (ks + 1) * Kc). Its 4 waves
 // take interleaved 32-wide k-steps, U steps' loads issued before their
 // MFMAs; the wave partial sums are added in LDS in a fixed order, so a row's
-// result never depends on which other rows are present. The epilogue gets
-// z = ks (split-K partials go to EpiPartial).
-template <int RT, int NT, int U, class Epi>
-__global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict__ W, int ldw, int MA,
-                                                          const bf16* __restrict__ X, int ldx, int n, int K, Epi epi) {
-    __shared__ float red[3][RT * NT * 4][64];
+// result never depends on which other rows are present (row tiles past n
+// re-read the last valid tile and are dropped).
+template <int RT, int NT, int U>
+__device__ __forceinline__ void skinny_core(const bf16* __restrict__ W, const bf16* __restrict__ X, int nks_tot, int n,
+                                            int Kc, float* red, float (&v)[RT][NT][4]) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int fr = lane & 15, fc = lane >> 4;
-    const int i0 = blockIdx.x * 16 * RT;
-    const int kbase = blockIdx.y * K;
+    const int s_base = blockIdx.y * (Kc >> 5);
     const bf16* wp[RT];
 #pragma unroll
-    for (int t = 0; t < RT; ++t) wp[t] = W + (long long)min(i0 + t * 16 + fr, MA - 1) * ldw + kbase + fc * 8;
+    for (int t = 0; t < RT; ++t) wp[t] = W + (((long long)(blockIdx.x * RT + t) * nks_tot + s_base) * 64 + lane) * 8;
+    const int ulast = (n - 1) >> 4;
     const bf16* xp[NT];
 #pragma unroll
-    for (int u = 0; u < NT; ++u) xp[u] = X + (long long)min(u * 16 + fr, n - 1) * ldx + kbase + fc * 8;
+    for (int u = 0; u < NT; ++u) xp[u] = X + (((long long)min(u, ulast) * nks_tot + s_base) * 64 + lane) * 8;
     mfma_f32x4 acc[RT][NT];
 #pragma unroll
     for (int t = 0; t < RT; ++t)
 #pragma unroll
         for (int u = 0; u < NT; ++u) acc[t][u] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-    const int nks = K >> 5;
-    int s = wave;
-    for (; s + 4 * (U - 1) < nks; s += 4 * U) {
+    const int nks = Kc >> 5;
+    // Batches of U k-steps (s, s + 4, ...): all loads of a batch are issued
+    // before its MFMAs; steps past the end re-read the last step and are skipped.
+    for (int s0 = wave; s0 < nks; s0 += 4 * U) {
         mfma_bf16x8 a[U][RT], b[U][NT];
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            const int k = (s + 4 * q) * 32;
+            const int off = min(s0 + 4 * q, nks - 1) * 512;
 #pragma unroll
-            for (int t = 0; t < RT; ++t) a[q][t] = *reinterpret_cast<const mfma_bf16x8*>(wp[t] + k);
+            for (int t = 0; t < RT; ++t) a[q][t] = *reinterpret_cast<const mfma_bf16x8*>(wp[t] + off);
 #pragma unroll
-            for (int u = 0; u < NT; ++u) b[q][u] = *reinterpret_cast<const mfma_bf16x8*>(xp[u] + k);
+            for (int u = 0; u < NT; ++u) b[q][u] = *reinterpret_cast<const mfma_bf16x8*>(xp[u] + off);
         }
 #pragma unroll
-        for (int q = 0; q < U; ++q)
+        for (int q = 0; q < U; ++q) {
+            if (s0 + 4 * q < nks) {
 #pragma unroll
-            for (int t = 0; t < RT; ++t)
+                for (int t = 0; t < RT; ++t)
 #pragma unroll
-                for (int u = 0; u < NT; ++u)
-                    acc[t][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q][t], b[q][u], acc[t][u], 0, 0, 0);
+                    for (int u = 0; u < NT; ++u)
+                        acc[t][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q][t], b[q][u], acc[t][u], 0, 0, 0);
+            }
+        }
     }
-    for (; s < nks; s += 4) {
-        const int k = s * 32;
-        mfma_bf16x8 a[RT], b[NT];
-#pragma unroll
-        for (int t = 0; t < RT; ++t) a[t] = *reinterpret_cast<const mfma_bf16x8*>(wp[t] + k);
-#pragma unroll
-        for (int u = 0; u < NT; ++u) b[u] = *reinterpret_cast<const mfma_bf16x8*>(xp[u] + k);
-#pragma unroll
-        for (int t = 0; t < RT; ++t)
-#pragma unroll
-            for (int u = 0; u < NT; ++u) acc[t][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[t], b[u], acc[t][u], 0, 0, 0);
-    }
+    constexpr int F = RT * NT * 4;
     if (wave > 0) {
 #pragma unroll
         for (int t = 0; t < RT; ++t)
 #pragma unroll
             for (int u = 0; u < NT; ++u)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) red[wave - 1][(t * NT + u) * 4 + e][lane] = acc[t][u][e];
+                for (int e = 0; e < 4; ++e) red[((wave - 1) * F + (t * NT + u) * 4 + e) * 64 + lane] = acc[t][u][e];
     }
     __syncthreads();
-    if (wave > 0) return;
+    if (wave == 0) {
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+            for (int u = 0; u < NT; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int idx = (t * NT + u) * 4 + e;
+                    v[t][u][e] = ((acc[t][u][e] + red[idx * 64 + lane]) + red[(F + idx) * 64 + lane]) +
+                                 red[(2 * F + idx) * 64 + lane];
+                }
+    }
+}
+
+// Plain epilogue variant: wave 0 hands rows i..i+3 of column r to epi (its
+// loads, pre(), are issued before the main loop). z = ks.
+template <int RT, int NT, int U, class Epi>
+__global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict__ W, const bf16* __restrict__ X,
+                                                          int nks_tot, int MA, int n, int Kc, Epi epi) {
+    __shared__ float red[3 * RT * NT * 4 * 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int fr = lane & 15, fc = lane >> 4;
+    const int i0 = blockIdx.x * 16 * RT;
     EpiPre pre[RT][NT];
+    if (wave == 0) {
 #pragma unroll
-    for (int t = 0; t < RT; ++t)
+        for (int t = 0; t < RT; ++t)
 #pragma unroll
-        for (int u = 0; u < NT; ++u) {
-            const int i = i0 + t * 16 + fc * 4, r = u * 16 + fr;
-            if (i < MA && r < n) pre[t][u] = epi.pre(i, r, blockIdx.y);
-        }
-#pragma unroll
-    for (int t = 0; t < RT; ++t)
-#pragma unroll
-        for (int u = 0; u < NT; ++u) {
-            float v[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int idx = (t * NT + u) * 4 + e;
-                v[e] = ((acc[t][u][e] + red[0][idx][lane]) + red[1][idx][lane]) + red[2][idx][lane];
+            for (int u = 0; u < NT; ++u) {
+                const int i = i0 + t * 16 + fc * 4, r = u * 16 + fr;
+                if (i < MA && r < n) pre[t][u] = epi.pre(i, r, blockIdx.y);
             }
+    }
+    float v[RT][NT][4];
+    skinny_core<RT, NT, U>(W, X, nks_tot, n, Kc, red, v);
+    if (wave > 0) return;
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int u = 0; u < NT; ++u) {
             const int i = i0 + t * 16 + fc * 4, r = u * 16 + fr;
-            if (i < MA && r < n) epi(i, r, blockIdx.y, v[0], v[1], v[2], v[3], pre[t][u]);
+            if (i < MA && r < n) epi(i, r, blockIdx.y, v[t][u][0], v[t][u][1], v[t][u][2], v[t][u][3], pre[t][u]);
         }
 }
 
@@ -728,23 +805,50 @@ struct EpiPartial {
     }
 };
 
-// W: [MA][KS * K] weight rows, X: [n][KS * K]; KS workgroups split K.
+// U = k-steps per wave and batch for nks k-steps over 4 waves: all of a
+// wave's steps in one batch, up to 10 (4 with 8 row tiles, for registers).
+constexpr int skinny_u(int nks, int NT) {
+    return (nks + 3) / 4 <= 1 ? 1
+         : (nks + 3) / 4 <= 2 ? 2
+         : (nks + 3) / 4 <= 3 ? 3
+         : ((nks + 3) / 4 <= 4 || NT >= 8) ? 4
+         : (nks + 3) / 4 <= 6 ? 6 : 10;
+}
+
+#define WMI_SKINNY_U(Kc, NT, LAUNCH)                                                  \
+    do {                                                                             \
+        const int u_ = skinny_u((Kc) / 32, NT);                                       \
+        if (u_ == 1) { constexpr int U = 1; LAUNCH; }                                 \
+        else if (u_ == 2) { constexpr int U = 2; LAUNCH; }                            \
+        else if (u_ == 3) { constexpr int U = 3; LAUNCH; }                            \
+        else if (u_ == 4) { constexpr int U = 4; LAUNCH; }                            \
+        else if (u_ == 6) { constexpr int U = (NT) >= 8 ? 4 : 6; LAUNCH; }             \
+        else { constexpr int U = (NT) >= 8 ? 4 : 10; LAUNCH; }                        \
+    } while (0)
+
+#define WMI_SKINNY_NT(n, ...)                                         \
+    do {                                                             \
+        if ((n) <= 16) { constexpr int NT = 1; __VA_ARGS__; }          \
+        else if ((n) <= 32) { constexpr int NT = 2; __VA_ARGS__; }     \
+        else if ((n) <= 64) { constexpr int NT = 4; __VA_ARGS__; }     \
+        else { constexpr int NT = 8; __VA_ARGS__; }                    \
+    } while (0)
+
+// W: fragment-major [MA rounded up to 32][K], X: fragment-major [n rounded up
+// to 16][K]; KS workgroups split K.
 template <class Epi>
 inline void skinny_bf16(const bf16* W, int MA, const bf16* X, int n, int K, int KS, const Epi& epi, hipStream_t st) {
     if (KS < 1 || K % (32 * KS) || n <= 0 || n > 128 || MA <= 0) throw ArgError(-1, "skinny_bf16: unsupported shape");
-    const int Kc = K / KS;
-    const bool big = MA >= 16384;  // output head: 32 rows per workgroup
-#define WMI_SKINNY(RT, NT, U)                                                                              \
-    hipLaunchKernelGGL((skinny_bf16_kernel<RT, NT, U, Epi>), dim3((MA + 16 * RT - 1) / (16 * RT), KS),    \
-                       dim3(256), 0, st, W, K, MA, X, K, n, Kc, epi)
-    if (big) {
-        if (n <= 16) WMI_SKINNY(2, 1, 4); else if (n <= 32) WMI_SKINNY(2, 2, 4);
-        else if (n <= 64) WMI_SKINNY(2, 4, 2); else WMI_SKINNY(2, 8, 2);
+    const int Kc = K / KS, nks_tot = K / 32;
+    if (MA >= 16384) {  // output head: 32 rows per workgroup
+        const dim3 grid((MA + 31) / 32, KS);
+        WMI_SKINNY_NT(n, WMI_SKINNY_U(Kc, NT, hipLaunchKernelGGL((skinny_bf16_kernel<2, NT, U, Epi>), grid, dim3(256),
+                                                                0, st, W, X, nks_tot, MA, n, Kc, epi)));
     } else {
-        if (n <= 16) WMI_SKINNY(1, 1, 8); else if (n <= 32) WMI_SKINNY(1, 2, 8);
-        else if (n <= 64) WMI_SKINNY(1, 4, 4); else WMI_SKINNY(1, 8, 2);
+        const dim3 grid((MA + 15) / 16, KS);
+        WMI_SKINNY_NT(n, WMI_SKINNY_U(Kc, NT, hipLaunchKernelGGL((skinny_bf16_kernel<1, NT, U, Epi>), grid, dim3(256),
+                                                                0, st, W, X, nks_tot, MA, n, Kc, epi)));
     }
-#undef WMI_SKINNY
 }
 
 // ------------------------------------------------------------- greedy step
