@@ -467,37 +467,15 @@ struct DecAttnArgs {
     int TP, H, d;
 };
 
-// Eight consecutive cache elements held as loaded (bf16: one 16-byte load).
-template <class T> struct Vec8;
-template <> struct Vec8<bf16> {
-    u32x4 v;
-    __device__ void load(const bf16* p) { v = *reinterpret_cast<const u32x4*>(p); }
-    __device__ float operator[](int i) const {
-        const unsigned w = v[i >> 1];
-        return __uint_as_float((i & 1) ? (w & 0xffff0000u) : (w << 16));
-    }
-};
-template <> struct Vec8<float> {
-    float4 a, b;
-    __device__ void load(const float* p) { a = ld4(p); b = ld4(p + 4); }
-    __device__ float operator[](int i) const {
-        const float4& h = i < 4 ? a : b;
-        const int j = i & 3;
-        return j == 0 ? h.x : j == 1 ? h.y : j == 2 ? h.z : h.w;
-    }
-};
-
 // Self-attention of one decode position over the slot's cached positions
-// 0..len-1 (causal by construction). Workgroup = 4 waves per (row, head).
-// The row's slot, length and query are loaded together, then every K and V
-// load of the workgroup is issued before the first use (addresses past the
-// length are clamped to the last valid 8 positions / row, so nothing beyond
-// the slot's positions is fetched from memory):
+// 0..len-1 (causal by construction). Workgroup = 4 waves per (row, head):
 //   scores: wave w sums dims 16w..16w+15 for all positions (lane owns 8
-//     consecutive positions), partials added in LDS in wave order;
+//     consecutive positions, 16 loads in flight), partials added in LDS;
 //   softmax: every wave holds all scores (fp32, wavefront reductions);
 //   P V: wave w takes positions 128w..128w+127, 8 lanes per 128-byte V row,
-//     partial outputs added in LDS in wave order.
+//     partial outputs added in LDS.
+// (Issuing the V loads together with the K loads measured slower: the K and
+// V phases are kept apart.)
 template <class T>
 __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     __shared__ float qs[64];
@@ -506,31 +484,26 @@ __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int slot = a.list[r];
     const int len = a.rowlen[r];
-    float qv = 0.f;
-    if (tid < 64) qv = ldf(reinterpret_cast<const T*>(a.q) + (long long)r * a.d + h * 64 + tid);
+    const T* q = reinterpret_cast<const T*>(a.q) + (long long)r * a.d + h * 64;
+    if (tid < 64) qs[tid] = ldf(q + tid);
+    __syncthreads();
     const long long head = (long long)slot * a.H + h;
     const T* kt = reinterpret_cast<const T*>(a.kt) + head * 64 * a.TP;
     const T* vv = reinterpret_cast<const T*>(a.v) + head * a.TP * 64;
     const int p0 = lane * 8;
-    const int pk = min(p0, (len - 1) & ~7);
-    Vec8<T> kv[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) kv[j].load(kt + (long long)(16 * w + j) * a.TP + pk);
-    const int dg = lane & 7, pg = lane >> 3;
-    const int lo = 128 * w, hi = min(len, lo + 128);
-    Vec8<T> vr[16];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) vr[u].load(vv + (long long)min(lo + pg + 8 * u, len - 1) * 64 + dg * 8);
-    if (tid < 64) qs[tid] = qv;
-    __syncthreads();
     float s[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) s[i] = 0.f;
+    if (p0 < len) {
+        float kv[16][8];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        const float qj = qs[16 * w + j];
+        for (int j = 0; j < 16; ++j) load_vec<T>(kt + (long long)(16 * w + j) * a.TP + p0, kv[j], 8);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) s[i] = fmaf(qj, kv[j][i], s[i]);
+        for (int j = 0; j < 16; ++j) {
+            const float qj = qs[16 * w + j];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) s[i] = fmaf(qj, kv[j][i], s[i]);
+        }
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) sp[w][p0 + i] = s[i];
@@ -556,16 +529,27 @@ __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
         for (int i = 0; i < 8; ++i) sp[0][p0 + i] = s[i];
     }
     __syncthreads();
+    const int dg = lane & 7, pg = lane >> 3;
     float o[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[i] = 0.f;
+    const int lo = 128 * w, hi = min(len, lo + 128);
+    if (lo < hi) {
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-        const int pp = lo + pg + 8 * u;
-        if (pp < hi) {
-            const float pw = sp[0][pp];
+        for (int b0 = 0; b0 < 128; b0 += 64) {
+            float vr[8][8];
+            float pw[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) o[i] = fmaf(pw, vr[u][i], o[i]);
+            for (int u = 0; u < 8; ++u) {
+                const int pp = lo + b0 + pg + 8 * u;
+                const int pc = min(pp, hi - 1);
+                load_vec<T>(vv + (long long)pc * 64 + dg * 8, vr[u], 8);
+                pw[u] = pp < hi ? sp[0][pc] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int i = 0; i < 8; ++i) o[i] = fmaf(pw[u], vr[u][i], o[i]);
         }
     }
 #pragma unroll
