@@ -42,26 +42,43 @@ def encoder_flops(shape):
     return float(f)
 
 
-def decode_bytes(shape, schedule):
-    """Algorithmic HBM bytes of all decode steps: every weight once per step
-    (bf16), the output head, and for each active slot the cross K/V over 1500
-    positions plus self K/V over its positions so far, in every layer."""
+def decode_bytes(shape, st):
+    """Algorithmic HBM bytes of the decode steps counted in the library's work
+    counters `st`: every weight once per step (plus the output head), and for
+    each stepped slot the cross K/V over 1500 positions plus the self K/V over
+    its positions so far, in every layer."""
     d, L, esz = shape.d, shape.n_dec, 2 if shape.dtype == "bf16" else 4
     w = (14 * L * d * d + shape.n_vocab * d) * esz
-    total = 0.0
-    for positions in schedule:          # one entry per step: list of attended lengths
-        total += w + sum(2 * L * d * esz * (1500 + p) for p in positions)
-    return total
+    return (w * st["decode_steps"] + 2 * L * d * esz * 1500 * st["rows_decoded"]
+            + 2 * L * d * esz * st["positions_attended"])
 
 
-def fixed_schedule(segs):
-    """Decode steps of a batch whose segments all start together: step s
-    attends s + 1 positions for every slot still running."""
-    steps = []
-    n_steps = max(len(s.prompt) + s.max_new_tokens - 1 for s in segs)
-    for st in range(n_steps):
-        steps.append([st + 1 for s in segs if st < len(s.prompt) + s.max_new_tokens - 1])
-    return steps
+def copy_ceiling_gbps(torch, mib=1024):
+    """Measured device copy bandwidth (read + write bytes per second) of a
+    plain torch copy of `mib` MiB: a practical HBM ceiling next to the
+    published peak."""
+    x = torch.ones(mib * (1 << 20) // 4, dtype=torch.float32, device="cuda:0")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(5):
+        y.copy_(x)
+    b.record()
+    b.synchronize()
+    gbps = 5 * 2 * x.numel() * 4 / (a.elapsed_time(b) / 1e3) / 1e9
+    del x, y
+    return round(gbps, 1)
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def counter_traffic(workload):
@@ -128,6 +145,7 @@ def cpu_baseline(shape, W, segs):
     sample_s = t_fe + t_enc2 + 2 * t_ckv + 3 * t_step2 + t_head
     return {
         "value": audio / sum(per_seg), "unit": "audio-s/s", "cores": int(threads), "kind": "oracle",
+        "cpu": cpu_model(), "host_cpus": os.cpu_count(),
         "sample": (f"1 segment: front end, conv stem, 2 of {shape.n_enc} encoder layers, 2 of "
                    f"{shape.n_dec} cross-KV layers, 3 decode steps of a 2-layer decoder + output head; "
                    f"extrapolated per layer and per token to the workload ({sample_s:.1f} s of CPU work)"),
@@ -170,16 +188,19 @@ def main():
     for _ in range(a.warmup):
         ctx.transcribe(segs, device_audio=ptrs)
     torch.cuda.synchronize()
+    ctx.stats(reset=True)
     t0 = time.perf_counter()
     for _ in range(a.steps):
         res = ctx.transcribe(segs, device_audio=ptrs)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    st_timed = ctx.stats(reset=True)
     assert all(r["status"] == 0 and r["tokens"].size == s.max_new_tokens for r, s in zip(res, segs))
     # Per-kernel timing: the same steps again with HIP events around every
     # launch of the named kernels on the library's stream (decode steps then
     # run as individual launches instead of one captured graph per step).
-    kinds = (binding.K_CROSS_ATTN, binding.K_ENC_PASS, binding.K_DEC_STEP, binding.K_ENC_GEMM)
+    kinds = (binding.K_CROSS_ATTN, binding.K_ENC_PASS, binding.K_DEC_STEP, binding.K_ENC_GEMM,
+             binding.K_FRONT_END)
     for k in kinds:
         ctx.profile_enable(k, True)
     t1 = time.perf_counter()
@@ -188,6 +209,8 @@ def main():
     torch.cuda.synchronize()
     wall_timed = time.perf_counter() - t1
     prof = {k: ctx.profile_read(k) for k in kinds}
+    st = ctx.stats(reset=True)
+    copy_gbps = copy_ceiling_gbps(torch)
 
     if a.calib_copy_mib:
         x = torch.ones(a.calib_copy_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda:0")
@@ -198,31 +221,37 @@ def main():
 
     # dominant kernel: decode-step cross-attention (HBM-bound)
     ca_ms, ca_n = prof[binding.K_CROSS_ATTN]
-    sched = fixed_schedule(segs) if slots >= len(segs) else None
-    n_active_avg = (np.mean([len(p) for p in sched]) if sched else float(slots))
+    n_active_avg = st["rows_decoded"] / max(st["decode_steps"], 1)
     ca_bytes = n_active_avg * shape.d * 1500 * 2 * (2 if shape.dtype == "bf16" else 4)
     ca_avg_s = ca_ms / 1e3 / max(ca_n, 1)
     achieved = ca_bytes / ca_avg_s / 1e9
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
             "frac": round(achieved / (PEAK_HBM / 1e9), 4), "traffic": counter_traffic(a.workload),
             "kernel": "cross_attn_kernel<bf16> (decode-step cross-attention over the 1500 cached positions)",
-            "bytes_per_launch": ca_bytes, "avg_launch_us": round(ca_avg_s * 1e6, 2), "launches": ca_n}
+            "bytes_per_launch": ca_bytes, "avg_launch_us": round(ca_avg_s * 1e6, 2), "launches": ca_n,
+            "measured_copy_gbps": copy_gbps}
 
     enc_ms, enc_n = prof[binding.K_ENC_PASS]
     dec_ms, dec_n = prof[binding.K_DEC_STEP]
     fl = encoder_flops(shape) * len(segs) * a.steps
     peak_f = PEAK_BF16 if shape.dtype == "bf16" else PEAK_F32
+    fe_ms, fe_n = prof[binding.K_FRONT_END]
     enc = {"ms_per_pass": round(enc_ms / max(enc_n, 1), 3), "passes": enc_n,
-           "tflops": round(fl / (enc_ms / 1e3) / 1e12, 1), "mfma_frac": round(fl / (enc_ms / 1e3) / peak_f, 4)}
+           "tflops": round(fl / (enc_ms / 1e3) / 1e12, 1), "mfma_frac": round(fl / (enc_ms / 1e3) / peak_f, 4),
+           "front_end_ms_per_pass": round(fe_ms / max(fe_n, 1), 3)}
     g_ms, g_n = prof[binding.K_ENC_GEMM]
     fc1_flops = 2 * 1500 * shape.d * 4 * shape.d * len(segs) * shape.n_enc * a.steps
     enc["fc1_gemm_tflops"] = round(fc1_flops / (g_ms / 1e3) / 1e12, 1) if g_ms > 0 else None
     dec = {"ms_per_step": round(dec_ms / max(dec_n, 1), 3), "steps": dec_n,
-           "ms_per_call_eager_timed": round(wall_timed / a.steps * 1e3, 2)}
-    if sched:
-        db = decode_bytes(shape, sched) * a.steps
-        dec["gbps"] = round(db / (dec_ms / 1e3) / 1e9, 1)
-        dec["hbm_frac"] = round(db / (dec_ms / 1e3) / PEAK_HBM, 4)
+           "ms_per_call_eager_timed": round(wall_timed / a.steps * 1e3, 2),
+           "avg_active_slots": round(n_active_avg, 2)}
+    db = decode_bytes(shape, st)
+    dec["gbps"] = round(db / (dec_ms / 1e3) / 1e9, 1)
+    dec["hbm_frac"] = round(db / (dec_ms / 1e3) / PEAK_HBM, 4)
+    batcher = {"refill_batches_per_call": st_timed["refill_batches"] // a.steps,
+               "host_ms_per_refill": round(st_timed["batcher_host_ms"] / max(st_timed["refill_batches"], 1), 4),
+               "host_ms_per_call": round(st_timed["batcher_host_ms"] / a.steps, 3),
+               "engine_host_ms_per_call": round(st_timed["engine_host_ms"] / a.steps, 2)}
 
     value = audio_s * a.steps / wall
     out = {
@@ -233,7 +262,7 @@ def main():
         "config": {"workload": a.workload, "segments": len(segs), "slots": slots,
                    "new_tokens": [int(min(s.max_new_tokens for s in segs)), int(max(s.max_new_tokens for s in segs))],
                    "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1},
-        "roofline": roof, "encoder": enc, "decode": dec,
+        "roofline": roof, "encoder": enc, "decode": dec, "batcher": batcher,
     }
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, W, segs)

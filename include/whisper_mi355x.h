@@ -243,7 +243,8 @@ enum {
     WHISPER_K_ENC_ATTN = 3,    /* encoder attention */
     WHISPER_K_ENC_PASS = 4,    /* a whole encode pass (front end to cross-KV) */
     WHISPER_K_DEC_STEP = 5,    /* a whole decode step (embedding to argmax) */
-    WHISPER_K_COUNT = 6
+    WHISPER_K_FRONT_END = 6,   /* log-mel front end of an encode pass (audio to normalised mel) */
+    WHISPER_K_COUNT = 7
 };
 
 /* Starts (enable = 1) or stops (0) timing of `kernel`, clearing its totals. */
@@ -253,6 +254,28 @@ whisper_status whisper_profile_enable(whisper_ctx* ctx, int32_t kernel, int32_t 
  * (synchronises the stream). */
 whisper_status whisper_profile_read(whisper_ctx* ctx, int32_t kernel, double* total_ms,
                                     int64_t* launches);
+
+/*
+ * Work counters of a context since creation or the last reset, for
+ * throughput and roofline accounting (the decode-step byte count of the
+ * method's per-segment caches follows from rows_decoded and
+ * positions_attended). Counters cover whisper_batch_encode,
+ * whisper_batch_decode_step and whisper_batch_transcribe alike.
+ */
+typedef struct {
+    int64_t encode_passes;      /* encoder passes (each of up to max_encode_batch segments) */
+    int64_t segments_encoded;   /* segments through the front end and encoder */
+    int64_t decode_steps;       /* decode steps (one token for every listed slot) */
+    int64_t rows_decoded;       /* sum over steps of the number of slots stepped */
+    int64_t positions_attended; /* sum over steps and slots of self-attention lengths (position + 1) */
+    int64_t refill_batches;     /* transcribe: encode calls made by the batcher (slot refills) */
+    double batcher_host_ms;     /* transcribe: host time in the batcher's own logic (queue, slot
+                                   choice, retirement), engine calls excluded */
+    double engine_host_ms;      /* transcribe: host time inside engine calls (enqueue and waits) */
+} whisper_stats;
+
+/* Copies the counters to *out (not NULL); reset != 0 then zeroes them. */
+whisper_status whisper_stats_read(whisper_ctx* ctx, whisper_stats* out, int32_t reset);
 
 /*
  * Host-only check of the continuous batcher (no device work): runs the

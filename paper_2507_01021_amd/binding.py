@@ -16,13 +16,13 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwhisper_
 OK, E_INVAL, E_NOMEM, E_DEVICE, E_CAPACITY, E_STATE, E_BUFFER, E_FORMAT = 0, -1, -2, -3, -4, -5, -6, -7
 DTYPE_F32, DTYPE_BF16 = 0, 1
 T_MEL, T_ENC_OUT, T_CROSS_K, T_CROSS_V = 0, 1, 2, 3
-K_CROSS_ATTN, K_ENC_GEMM, K_SELF_ATTN, K_ENC_ATTN, K_ENC_PASS, K_DEC_STEP = 0, 1, 2, 3, 4, 5
+K_CROSS_ATTN, K_ENC_GEMM, K_SELF_ATTN, K_ENC_ATTN, K_ENC_PASS, K_DEC_STEP, K_FRONT_END = 0, 1, 2, 3, 4, 5, 6
 
 EXPORTS = (
     "whisper_params_from_blob", "whisper_ctx_create", "whisper_ctx_destroy", "whisper_last_error",
     "whisper_ctx_set_stream", "whisper_batch_encode", "whisper_batch_decode_step",
     "whisper_slot_tokens", "whisper_batch_transcribe", "whisper_debug_copy",
-    "whisper_profile_enable", "whisper_profile_read", "whisper_test_batcher",
+    "whisper_profile_enable", "whisper_profile_read", "whisper_stats_read", "whisper_test_batcher",
 )
 
 
@@ -45,6 +45,12 @@ class whisper_segment(C.Structure):
 class whisper_result(C.Structure):
     _fields_ = [("segment_id", C.c_int64), ("token_offset", C.c_int64), ("user_id", C.c_int32),
                 ("status", C.c_int32), ("n_tokens", C.c_int32), ("reserved", C.c_int32)]
+
+
+class whisper_stats(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in (
+        "encode_passes", "segments_encoded", "decode_steps", "rows_decoded", "positions_attended",
+        "refill_batches")] + [("batcher_host_ms", C.c_double), ("engine_host_ms", C.c_double)]
 
 
 _lib = None
@@ -74,6 +80,7 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "whisper_debug_copy": (i32, [vp, i32, i32, vp, C.c_size_t]),
         "whisper_profile_enable": (i32, [vp, i32, i32]),
         "whisper_profile_read": (i32, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64)]),
+        "whisper_stats_read": (i32, [vp, C.POINTER(whisper_stats), i32]),
         "whisper_test_batcher": (i32, [i32, C.POINTER(i64), pi32, C.POINTER(i64), pi32, i32, i32, i32,
                                       pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32]),
     }
@@ -220,6 +227,11 @@ class Context:
         ms, n = C.c_double(), C.c_int64()
         self._check(load().whisper_profile_read(self.h, kernel, C.byref(ms), C.byref(n)))
         return ms.value, n.value
+
+    def stats(self, reset: bool = False) -> dict:
+        st = whisper_stats()
+        self._check(load().whisper_stats_read(self.h, C.byref(st), 1 if reset else 0))
+        return {name: getattr(st, name) for name, _ in whisper_stats._fields_}
 
 
 def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_batch, refill_min,

@@ -3,6 +3,7 @@
 // batcher to the engine. Every check runs before any device work.
 #include <string.h>
 
+#include <chrono>
 #include <memory>
 #include <new>
 #include <set>
@@ -29,6 +30,7 @@ struct whisper_ctx {
     std::unique_ptr<wmi::Engine> eng;
     std::string err;
     std::vector<SlotState> slots;
+    whisper_stats stats{};
     bool broken = false;
 };
 
@@ -96,21 +98,48 @@ std::string check_params(const whisper_params& p, const whisper_params& blob) {
 }
 
 // Batch backend on a real context.
+// Engine calls of the batcher, with the work counters and the host time
+// spent inside them (the rest of the batcher's time is its own logic).
 struct EngineBackend : wmi::BatchBackend {
+    using clock = std::chrono::steady_clock;
     whisper_ctx* c;
     const whisper_segment* segs;
     std::vector<wmi::SegmentDesc> descs;
+    std::vector<int> steps;  // decode steps taken by each slot's current segment
+    double engine_ms = 0.0;
+    struct Timer {
+        double& acc;
+        clock::time_point t0 = clock::now();
+        ~Timer() { acc += std::chrono::duration<double, std::milli>(clock::now() - t0).count(); }
+    };
     void encode(const int* idx, int n, const int* slots) override {
+        Timer t{engine_ms};
         descs.resize(n);
         for (int k = 0; k < n; ++k) {
             const whisper_segment& s = segs[idx[k]];
             descs[k] = wmi::SegmentDesc{s.audio, s.n_samples, s.audio_on_device == 1, s.prompt, s.n_prompt};
+            steps[slots[k]] = 0;
         }
         c->eng->encode(descs.data(), n, slots, false);
+        c->stats.encode_passes += (n + c->p.max_encode_batch - 1) / c->p.max_encode_batch;
+        c->stats.segments_encoded += n;
+        c->stats.refill_batches += 1;
     }
-    void step(const int* slots, int n) override { c->eng->decode_step(slots, n, nullptr, nullptr, nullptr, false); }
-    void retire(int slot, int, int count, int32_t* dst) override { c->eng->read_tokens_async(slot, count, dst); }
-    void finish() override { c->eng->finish_reads(); }
+    void step(const int* slots, int n) override {
+        Timer t{engine_ms};
+        c->eng->decode_step(slots, n, nullptr, nullptr, nullptr, false);
+        c->stats.decode_steps += 1;
+        c->stats.rows_decoded += n;
+        for (int k = 0; k < n; ++k) c->stats.positions_attended += ++steps[slots[k]];
+    }
+    void retire(int slot, int, int count, int32_t* dst) override {
+        Timer t{engine_ms};
+        c->eng->read_tokens_async(slot, count, dst);
+    }
+    void finish() override {
+        Timer t{engine_ms};
+        c->eng->finish_reads();
+    }
 };
 
 // Batch backend of the host-only scheduler check.
@@ -213,6 +242,8 @@ whisper_status whisper_batch_encode(whisper_ctx* ctx, const whisper_segment* seg
             d[i] = wmi::SegmentDesc{segs[i].audio, segs[i].n_samples, segs[i].audio_on_device == 1, segs[i].prompt,
                                     segs[i].n_prompt};
         ctx->eng->encode(d.data(), n, slots, true);
+        ctx->stats.encode_passes += (n + ctx->p.max_encode_batch - 1) / ctx->p.max_encode_batch;
+        ctx->stats.segments_encoded += n;
         for (int i = 0; i < n; ++i) {
             SlotState& s = ctx->slots[slots[i]];
             s.active = true;
@@ -244,8 +275,11 @@ whisper_status whisper_batch_decode_step(whisper_ctx* ctx, const int32_t* slots,
     }
     return guarded(ctx, [&]() -> whisper_status {
         ctx->eng->decode_step(slots, n, forced, out_tokens, out_logits, true);
+        ctx->stats.decode_steps += 1;
+        ctx->stats.rows_decoded += n;
         for (int i = 0; i < n; ++i) {
             SlotState& s = ctx->slots[slots[i]];
+            ctx->stats.positions_attended += s.steps + 1;
             if (s.steps >= s.n_prompt - 1) s.generated++;
             s.steps++;
             if (s.generated == s.max_new) s.active = false;
@@ -294,8 +328,13 @@ whisper_status whisper_batch_transcribe(whisper_ctx* ctx, const whisper_segment*
         EngineBackend be;
         be.c = ctx;
         be.segs = segs;
+        be.steps.assign(ctx->p.max_slots, 0);
+        const auto t0 = EngineBackend::clock::now();
         wmi::run_continuous_batching(q, ctx->p.max_slots, ctx->p.max_encode_batch, ctx->p.refill_min, off, token_buf,
                                      be);
+        const double total = std::chrono::duration<double, std::milli>(EngineBackend::clock::now() - t0).count();
+        ctx->stats.engine_host_ms += be.engine_ms;
+        ctx->stats.batcher_host_ms += total - be.engine_ms;
         return WHISPER_OK;
     });
     for (auto& s : ctx->slots) s = SlotState();
@@ -333,6 +372,14 @@ whisper_status whisper_profile_read(whisper_ctx* ctx, int32_t kernel, double* to
         ctx->eng->profile_read(kernel, total_ms, launches);
         return WHISPER_OK;
     });
+}
+
+whisper_status whisper_stats_read(whisper_ctx* ctx, whisper_stats* out, int32_t reset) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (!out) return fail(ctx, WHISPER_E_INVAL, "out is NULL");
+    *out = ctx->stats;
+    if (reset) ctx->stats = whisper_stats{};
+    return WHISPER_OK;
 }
 
 whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const int32_t* user_id,

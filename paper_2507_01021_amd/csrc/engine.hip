@@ -593,11 +593,13 @@ class EngineT final : public Engine {
         last_nb_ = nb;
 
         prof_begin(WHISPER_K_ENC_PASS);
+        prof_begin(WHISPER_K_FRONT_END);
         hipLaunchKernelGGL(prep_audio_kernel, dim3((480400 + 255) / 256, nb), dim3(256), 0, st_, segsrc_, xpad_,
                            P_.pad_mode);
         gemm_simt(basis_, 400, 0, xpad_, 160, 480400, 404, 3000, 400, nb, EpiPower{power_}, st_);
         gemm_simt(melfb_, 201, 0, power_, 201, 0, nm_, nb * 3000, 201, 1, EpiLogMel{logmel_, nm_}, st_);
         hipLaunchKernelGGL(mel_norm_kernel<T>, dim3(nb), dim3(1024), 0, st_, logmel_, ypad_, nvalid_, nm_);
+        prof_end(WHISPER_K_FRONT_END);
         gemm(W1r_, 3 * CP, 0, ypad_, CP, 3002LL * CP, d, 3000, 3 * CP, nb, EpiConv1<T>{cb1_, h1_, d});
         gemm(W2r_, 3 * d, 0, h1_, 2 * d, 3002LL * d, d, N_CTX, 3 * d, nb, EpiConv2{cb2_, pe_, x_, d});
         for (int l = 0; l < Le_; ++l) {

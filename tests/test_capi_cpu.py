@@ -41,7 +41,8 @@ def test_struct_layouts_match_header(tmp_path):
     header's structs."""
     fields = {"whisper_params": [f for f, _ in binding.whisper_params._fields_],
               "whisper_segment": [f for f, _ in binding.whisper_segment._fields_],
-              "whisper_result": [f for f, _ in binding.whisper_result._fields_]}
+              "whisper_result": [f for f, _ in binding.whisper_result._fields_],
+              "whisper_stats": [f for f, _ in binding.whisper_stats._fields_]}
     lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HEADER}"', "int main(void) {"]
     for st, fs in fields.items():
         lines.append(f'printf("{st} %zu\\n", sizeof({st}));')
@@ -101,4 +102,6 @@ def test_null_context_calls_fail_cleanly(lib):
     assert lib.whisper_batch_encode(None, None, 1, None) == binding.E_INVAL
     assert lib.whisper_batch_decode_step(None, None, 1, None, None, None) == binding.E_INVAL
     assert lib.whisper_batch_transcribe(None, None, 1, None, 0, None) == binding.E_INVAL
+    st = binding.whisper_stats()
+    assert lib.whisper_stats_read(None, C.byref(st), 0) == binding.E_INVAL
     lib.whisper_ctx_destroy(None)

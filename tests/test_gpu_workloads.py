@@ -114,7 +114,17 @@ def test_continuous_batching_workload(name, sample):
     W = synth.make_weights(shape, 0)
     with binding.Context(synth.pack_blob(W), max_slots=slots, max_encode_batch=min(slots, 32)) as ctx:
         log(f"{name}: transcribe {len(segs)} segments with {slots} slots")
+        ctx.stats(reset=True)
         res = ctx.transcribe(segs)
+        st = ctx.stats()
+        # work counters are exact: every segment takes n_prompt - 1 + max_new steps,
+        # attending 1, 2, ... positions
+        steps = [len(s.prompt) - 1 + s.max_new_tokens for s in segs]
+        assert st["segments_encoded"] == len(segs)
+        assert st["rows_decoded"] == sum(steps)
+        assert st["positions_attended"] == sum(k * (k + 1) // 2 for k in steps)
+        assert max(steps) <= st["decode_steps"] <= sum(steps)
+        assert st["refill_batches"] >= -(-len(segs) // min(slots, 32))
         for s, r in zip(segs, res):
             assert (r["user_id"], r["segment_id"], r["status"]) == (s.user_id, s.segment_id, 0)
             assert r["tokens"].size == s.max_new_tokens
