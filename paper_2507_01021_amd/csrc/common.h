@@ -34,6 +34,19 @@ __host__ __device__ inline bf16 f2bf(float f) {
     return r;
 }
 
+// fp32 -> bf16 on the device with the hardware conversion (round to nearest
+// even, same result as f2bf): two values packed into one 32-bit word.
+__device__ inline uint32_t pack_bf16x2(float a, float b) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 hbf16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{a, b}), hbf16x2));
+}
+__device__ inline bf16 f2bf_dev(float f) {
+    bf16 r;
+    r.x = __builtin_bit_cast(uint16_t, (__bf16)f);
+    return r;
+}
+
 // Storage-type traits: load as fp32, store from fp32.
 template <class T> struct St;
 template <> struct St<float> {
@@ -42,7 +55,7 @@ template <> struct St<float> {
 };
 template <> struct St<bf16> {
     __device__ static inline float ld(const bf16* p) { return bf2f(*p); }
-    __device__ static inline void st(bf16* p, float v) { *p = f2bf(v); }
+    __device__ static inline void st(bf16* p, float v) { *p = f2bf_dev(v); }
 };
 
 template <class T> __device__ inline float ldf(const T* p) { return St<T>::ld(p); }
@@ -74,8 +87,7 @@ __device__ inline void st4(float* p, float a, float b, float c, float d) {
     *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
 }
 __device__ inline void st4(bf16* p, float a, float b, float c, float d) {
-    uint32_t lo = (uint32_t)f2bf(a).x | ((uint32_t)f2bf(b).x << 16);
-    uint32_t hi = (uint32_t)f2bf(c).x | ((uint32_t)f2bf(d).x << 16);
+    const uint32_t lo = pack_bf16x2(a, b), hi = pack_bf16x2(c, d);
     *reinterpret_cast<u32x2*>(p) = u32x2{lo, hi};
 }
 __device__ inline float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }

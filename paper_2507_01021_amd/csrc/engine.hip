@@ -17,12 +17,18 @@
 //   residual, LN, fc1 + GELU, fc2 + residual -> final LN -> logits against
 //   the token embedding -> argmax, next input, position advance.
 //   In bf16 the projection weights and the activations they multiply are
-//   fragment-major (frag_off).
+//   fragment-major (frag_off). With 32 or more slots in bf16 the rows are
+//   split in two halves (the first a whole number of 16-row tiles) that run
+//   the complete step on two streams, each as its own captured graph (the
+//   halves touch disjoint slots), so the two chains of small latency-bound
+//   kernels overlap. Steps with kernel timing on run unsplit, so each timed
+//   launch has the device to itself.
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
+#include <array>
 #include <map>
 #include <type_traits>
 #include <string>
@@ -206,8 +212,12 @@ class EngineT final : public Engine {
         EB_ = p.max_encode_batch;
         WMI_HIP(hipSetDevice(dev_));
         WMI_HIP(hipStreamCreateWithFlags(&own_stream_, hipStreamNonBlocking));
+        WMI_HIP(hipStreamCreateWithFlags(&st2_, hipStreamNonBlocking));
+        WMI_HIP(hipEventCreateWithFlags(&fork_ev_, hipEventDisableTiming));
+        WMI_HIP(hipEventCreateWithFlags(&join_ev_, hipEventDisableTiming));
         st_ = own_stream_;
         if (const char* g = getenv("WHISPER_STEP_GRAPHS")) graphs_ = g[0] != '0';
+        if (const char* g = getenv("WHISPER_STEP_SPLIT")) split_ = g[0] != '0';
         load_weights(blob, bytes);
         alloc_state();
         WMI_HIP(hipDeviceSynchronize());
@@ -219,13 +229,19 @@ class EngineT final : public Engine {
         for (auto& pr : prof_)
             for (auto& e : pr.used) { (void)hipEventDestroy(e.first); (void)hipEventDestroy(e.second); }
         for (auto e : event_pool_) (void)hipEventDestroy(e);
-        for (auto& g : step_graphs_) (void)hipGraphExecDestroy(g.second);
+        if (st2_) (void)hipStreamSynchronize(st2_);
+        for (auto& g : step_graphs_)
+            for (auto ge : g.second)
+                if (ge) (void)hipGraphExecDestroy(ge);
         for (auto& s : stage_) {
             if (s.ev) (void)hipEventDestroy(s.ev);
             if (s.host) (void)hipHostFree(s.host);
         }
         if (tokpin_) (void)hipHostFree(tokpin_);
         for (void* q : allocs_) (void)hipFree(q);
+        if (fork_ev_) (void)hipEventDestroy(fork_ev_);
+        if (join_ev_) (void)hipEventDestroy(join_ev_);
+        if (st2_) (void)hipStreamDestroy(st2_);
         if (own_stream_) (void)hipStreamDestroy(own_stream_);
     }
 
@@ -254,27 +270,36 @@ class EngineT final : public Engine {
         }
         if (forced) upload(1, forced_, forced, n * sizeof(int));
         // Plain steps (no teacher forcing, no per-step outputs, no kernel
-        // timing) replay a captured graph of the whole step; the graph only
-        // depends on n because the slot list lives in device memory.
+        // timing) replay captured graphs of the whole step; a graph only
+        // depends on the row count because the slot list lives in device memory.
         bool timed = false;
         for (auto& pr : prof_) timed = timed || pr.on;
+        const int h0 = timed ? n : split_rows(n);
+        const bool split = h0 < n;
+        prof_begin(WHISPER_K_DEC_STEP, st_);
+        if (split) {  // fork: the second half waits for everything enqueued so far
+            WMI_HIP(hipEventRecord(fork_ev_, st_));
+            WMI_HIP(hipStreamWaitEvent(st2_, fork_ev_, 0));
+        }
         if (graphs_ && !forced && !out_tok && !out_logits && !timed) {
             auto it = step_graphs_.find(n);
             if (it == step_graphs_.end()) {
-                hipGraph_t g = nullptr;
-                hipGraphExec_t ge = nullptr;
-                WMI_HIP(hipStreamBeginCapture(st_, hipStreamCaptureModeRelaxed));
-                launch_step(n, false);
-                WMI_HIP(hipStreamEndCapture(st_, &g));
-                const hipError_t e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
-                (void)hipGraphDestroy(g);
-                WMI_HIP(e);
+                std::array<hipGraphExec_t, 2> ge{nullptr, nullptr};
+                ge[0] = capture(st_, [&] { launch_rows(0, h0, false, st_, 0); });
+                if (split) ge[1] = capture(st2_, [&] { launch_rows(h0, n - h0, false, st2_, 1); });
                 it = step_graphs_.emplace(n, ge).first;
             }
-            WMI_HIP(hipGraphLaunch(it->second, st_));
+            WMI_HIP(hipGraphLaunch(it->second[0], st_));
+            if (split) WMI_HIP(hipGraphLaunch(it->second[1], st2_));
         } else {
-            launch_step(n, forced != nullptr);
+            launch_rows(0, h0, forced != nullptr, st_, 0);
+            if (split) launch_rows(h0, n - h0, forced != nullptr, st2_, 1);
         }
+        if (split) {  // join
+            WMI_HIP(hipEventRecord(join_ev_, st2_));
+            WMI_HIP(hipStreamWaitEvent(st_, join_ev_, 0));
+        }
+        prof_end(WHISPER_K_DEC_STEP, st_);
         WMI_HIP(hipGetLastError());
         if (out_tok) WMI_HIP(hipMemcpyAsync(out_tok, outtok_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
         if (out_logits)
@@ -282,39 +307,70 @@ class EngineT final : public Engine {
         if (sync_ || out_tok || out_logits || forced) WMI_HIP(hipStreamSynchronize(st_));
     }
 
-    // The kernels of one decode step for the first n entries of the slot list.
-    void launch_step(int n, bool forced) {
+    // Rows of the first half of a step of n rows: all of them below 32 rows
+    // (or in fp32), else a whole number of 16-row tiles near n / 2.
+    int split_rows(int n) const {
+        if (!split_ || !std::is_same<T, bf16>::value || n < 32) return n;
+        return 16 * std::max(1, (n + 16) / 32);
+    }
+
+    template <class F>
+    hipGraphExec_t capture(hipStream_t s, F&& launches) {
+        hipGraph_t g = nullptr;
+        hipGraphExec_t ge = nullptr;
+        WMI_HIP(hipStreamBeginCapture(s, hipStreamCaptureModeRelaxed));
+        launches();
+        WMI_HIP(hipStreamEndCapture(s, &g));
+        const hipError_t e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(g);
+        WMI_HIP(e);
+        return ge;
+    }
+
+    // The kernels of one decode step for rows r0 .. r0+n-1 of the slot list,
+    // on stream s, with split-K partial buffer `half` (0 or 1). r0 is a
+    // multiple of 16, so the fragment-major activations of these rows start
+    // at element r0 * K.
+    void launch_rows(int r0, int n, bool forced, hipStream_t s, int half) {
         const int d = d_;
         const int ks1 = split_k(d), ks4 = split_k(4 * d);
-        prof_begin(WHISPER_K_DEC_STEP);
-        WMI_SWITCH_E(d, hipLaunchKernelGGL((embed_ln_kernel<T, E>), dim3(n), dim3(64), 0, st_, tok_emb_, pos_emb_,
-                                           list_, pos_, seq_, dx_, dz_, dec_[0].ln1g, dec_[0].ln1b));
+        const int* list = list_ + r0;
+        T* dz = dz_ + (size_t)r0 * d;
+        T* dq = dq_ + (size_t)r0 * d;
+        T* datt = datt_ + (size_t)r0 * d;
+        T* dh = dh_ + (size_t)r0 * 4 * d;
+        float* dx = dx_ + (size_t)r0 * d;
+        int* rowlen = rowlen_ + r0;
+        float* pbuf = gpart_ + (size_t)half * 4 * S_ * d;
+        WMI_SWITCH_E(d, hipLaunchKernelGGL((embed_ln_kernel<T, E>), dim3(n), dim3(64), 0, s, tok_emb_, pos_emb_,
+                                           list, pos_, seq_, dx, dz, dec_[0].ln1g, dec_[0].ln1b));
         for (int l = 0; l < Ld_; ++l) {
             const DecLayerW<T>& L = dec_[l];
             const long long sl = (long long)l * S_ * H_ * 64;
-            proj(L.Wqkv, 3 * d, dz_, n, d, 1,
-                 EpiDecQKV<T>{L.bq, L.bv, dq_, kts_ + sl * TS, vs_ + sl * TS, list_, pos_, rowlen_, d, H_});
-            DecAttnArgs sa{dq_, kts_ + sl * TS, vs_ + sl * TS, datt_, list_, rowlen_, TS, H_, d};
-            prof_begin(WHISPER_K_SELF_ATTN);
-            hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, st_, sa);
-            prof_end(WHISPER_K_SELF_ATTN);
-            proj_resid(L.Wo, datt_, n, d, ks1, L.bo, L.ln2g, L.ln2b);
-            proj(L.Wcq, d, dz_, n, d, 1, EpiQ<T>{L.cbq, dq_, d});
-            DecAttnArgs ca{dq_, ktc_ + sl * TC, vc_ + sl * TC, datt_, list_, nullptr, TC, H_, d};
-            prof_begin(WHISPER_K_CROSS_ATTN);
-            hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, st_, ca);
-            prof_end(WHISPER_K_CROSS_ATTN);
-            proj_resid(L.Wco, datt_, n, d, ks1, L.cbo, L.ln3g, L.ln3b);
-            proj(L.W1, 4 * d, dz_, n, d, 1, EpiGelu<T, true>{L.b1, dh_, 4 * d});
+            proj(L.Wqkv, 3 * d, dz, n, d, 1,
+                 EpiDecQKV<T>{L.bq, L.bv, dq, kts_ + sl * TS, vs_ + sl * TS, list, pos_, rowlen, d, H_}, s);
+            DecAttnArgs sa{dq, kts_ + sl * TS, vs_ + sl * TS, datt, list, rowlen, TS, H_, d};
+            prof_begin(WHISPER_K_SELF_ATTN, s);
+            hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, s, sa);
+            prof_end(WHISPER_K_SELF_ATTN, s);
+            proj_resid(L.Wo, datt, n, d, ks1, L.bo, L.ln2g, L.ln2b, pbuf, dx, dz, s);
+            proj(L.Wcq, d, dz, n, d, 1, EpiQ<T>{L.cbq, dq, d}, s);
+            DecAttnArgs ca{dq, ktc_ + sl * TC, vc_ + sl * TC, datt, list, nullptr, TC, H_, d};
+            prof_begin(WHISPER_K_CROSS_ATTN, s);
+            hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, s, ca);
+            prof_end(WHISPER_K_CROSS_ATTN, s);
+            proj_resid(L.Wco, datt, n, d, ks1, L.cbo, L.ln3g, L.ln3b, pbuf, dx, dz, s);
+            proj(L.W1, 4 * d, dz, n, d, 1, EpiGelu<T, true>{L.b1, dh, 4 * d}, s);
             const bool last = l + 1 == Ld_;
-            proj_resid(L.W2, dh_, n, 4 * d, ks4, L.b2, last ? lnfg_ : dec_[l + 1].ln1g,
-                       last ? lnfb_ : dec_[l + 1].ln1b);
+            proj_resid(L.W2, dh, n, 4 * d, ks4, L.b2, last ? lnfg_ : dec_[l + 1].ln1g,
+                       last ? lnfb_ : dec_[l + 1].ln1b, pbuf, dx, dz, s);
         }
-        proj(tok_emb_, V_, dz_, n, d, 1, EpiLogits{logits_, V_});
-        hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, st_, logits_, V_, best_);
-        hipLaunchKernelGGL(argmax_step_kernel, dim3((n + 63) / 64), dim3(64), 0, st_, best_, n, list_, pos_, npr_,
-                           seq_, gen_, forced ? forced_ : nullptr, outtok_);
-        prof_end(WHISPER_K_DEC_STEP);
+        float* logits = logits_ + (size_t)r0 * V_;
+        unsigned long long* best = best_ + r0;
+        proj(tok_emb_, V_, dz, n, d, 1, EpiLogits{logits, V_}, s);
+        hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, s, logits, V_, best);
+        hipLaunchKernelGGL(argmax_step_kernel, dim3((n + 63) / 64), dim3(64), 0, s, best, n, list, pos_, npr_, seq_,
+                           gen_, forced ? forced_ + r0 : nullptr, outtok_ + r0);
     }
 
     void read_tokens(int slot, int count, int32_t* dst) override {
@@ -442,8 +498,10 @@ class EngineT final : public Engine {
     float *dx_, *logits_, *gpart_;
     unsigned long long* best_;
     std::vector<int> list_host_;
-    bool graphs_ = true;
-    std::map<int, hipGraphExec_t> step_graphs_;
+    bool graphs_ = true, split_ = true;
+    std::map<int, std::array<hipGraphExec_t, 2>> step_graphs_;  // per row count: first and second half
+    hipStream_t st2_ = nullptr;                                 // second half of a split step
+    hipEvent_t fork_ev_ = nullptr, join_ev_ = nullptr;
     // host staging
     Stage stage_[3];
     int32_t* tokpin_ = nullptr;
@@ -491,15 +549,15 @@ class EngineT final : public Engine {
         WMI_HIP(hipEventCreate(&e));
         return e;
     }
-    void prof_begin(int k) {
+    void prof_begin(int k, hipStream_t s) {
         if (!prof_[k].on) return;
         prof_[k].open = get_event();
-        WMI_HIP(hipEventRecord(prof_[k].open, st_));
+        WMI_HIP(hipEventRecord(prof_[k].open, s));
     }
-    void prof_end(int k) {
+    void prof_end(int k, hipStream_t s) {
         if (!prof_[k].on) return;
         hipEvent_t e = get_event();
-        WMI_HIP(hipEventRecord(e, st_));
+        WMI_HIP(hipEventRecord(e, s));
         prof_[k].used.push_back({prof_[k].open, e});
         if (prof_[k].used.size() >= 4096) {  // bound the number of live events
             WMI_HIP(hipStreamSynchronize(st_));
@@ -530,13 +588,14 @@ class EngineT final : public Engine {
                                             y, g, b, rows));
     }
     // decoder: x += split-K partials + bias, then z = LN(x)
-    void resid_ln(int KS, int n, const float* bias, const float* g, const float* b) {
+    void resid_ln(int KS, int n, const float* bias, const float* g, const float* b, float* part, float* dx, T* dz,
+                  hipStream_t s) {
         if (KS == 4) {
             WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 4>), dim3(n), dim3(resid_ln_threads<E>()), 0,
-                                                st_, gpart_, n, bias, dx_, dz_, g, b));
+                                                s, part, n, bias, dx, dz, g, b));
         } else {
             WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 1>), dim3(n), dim3(resid_ln_threads<E>()), 0,
-                                                st_, gpart_, n, bias, dx_, dz_, g, b));
+                                                s, part, n, bias, dx, dz, g, b));
         }
     }
     // split factor of a decode projection with reduction length K
@@ -551,14 +610,15 @@ class EngineT final : public Engine {
 
     // decode projection: rows = weight rows (MA), n activation rows of width K
     template <class Epi>
-    void proj(const T* W, int MA, const T* X, int n, int K, int KS, const Epi& epi) {
-        if constexpr (std::is_same<T, bf16>::value) skinny_bf16(W, MA, X, n, K, KS, epi, st_);
-        else gemm_simt(W, K, K / KS, X, K, K / KS, MA, n, K / KS, KS, epi, st_);
+    void proj(const T* W, int MA, const T* X, int n, int K, int KS, const Epi& epi, hipStream_t s) {
+        if constexpr (std::is_same<T, bf16>::value) skinny_bf16(W, MA, X, n, K, KS, epi, s);
+        else gemm_simt(W, K, K / KS, X, K, K / KS, MA, n, K / KS, KS, epi, s);
     }
     // residual projection: x += W X + bias (split-K partials), then z = LN(x)
-    void proj_resid(const T* W, const T* X, int n, int K, int KS, const float* bias, const float* g, const float* b) {
-        proj(W, d_, X, n, K, KS, EpiPartial{gpart_, d_, n});
-        resid_ln(KS, n, bias, g, b);
+    void proj_resid(const T* W, const T* X, int n, int K, int KS, const float* bias, const float* g, const float* b,
+                    float* part, float* dx, T* dz, hipStream_t s) {
+        proj(W, d_, X, n, K, KS, EpiPartial{part, d_, n}, s);
+        resid_ln(KS, n, bias, g, b, part, dx, dz, s);
     }
 
     void encode_pass(const SegmentDesc* segs, int nb, const int* slots) {
@@ -592,14 +652,14 @@ class EngineT final : public Engine {
         upload(2, nvalid_, small.data(), small.size() * sizeof(int));
         last_nb_ = nb;
 
-        prof_begin(WHISPER_K_ENC_PASS);
-        prof_begin(WHISPER_K_FRONT_END);
+        prof_begin(WHISPER_K_ENC_PASS, st_);
+        prof_begin(WHISPER_K_FRONT_END, st_);
         hipLaunchKernelGGL(prep_audio_kernel, dim3((480400 + 255) / 256, nb), dim3(256), 0, st_, segsrc_, xpad_,
                            P_.pad_mode);
         gemm_simt(basis_, 400, 0, xpad_, 160, 480400, 404, 3000, 400, nb, EpiPower{power_}, st_);
         gemm_simt(melfb_, 201, 0, power_, 201, 0, nm_, nb * 3000, 201, 1, EpiLogMel{logmel_, nm_}, st_);
         hipLaunchKernelGGL(mel_norm_kernel<T>, dim3(nb), dim3(1024), 0, st_, logmel_, ypad_, nvalid_, nm_);
-        prof_end(WHISPER_K_FRONT_END);
+        prof_end(WHISPER_K_FRONT_END, st_);
         gemm(W1r_, 3 * CP, 0, ypad_, CP, 3002LL * CP, d, 3000, 3 * CP, nb, EpiConv1<T>{cb1_, h1_, d});
         gemm(W2r_, 3 * d, 0, h1_, 2 * d, 3002LL * d, d, N_CTX, 3 * d, nb, EpiConv2{cb2_, pe_, x_, d});
         for (int l = 0; l < Le_; ++l) {
@@ -607,26 +667,26 @@ class EngineT final : public Engine {
             ln(x_, zb_, L.ln1g, L.ln1b, M);
             gemm(L.Wqk, d, 0, zb_, d, 0, 2 * d, M, d, 1, EpiQK<T>{L.bq, qh_, kh_, d, H_});
             gemm(zb_, d, 0, L.Wv, d, 0, M, d, d, 1, EpiVt<T>{L.bv, vt_, H_});
-            prof_begin(WHISPER_K_ENC_ATTN);
+            prof_begin(WHISPER_K_ENC_ATTN, st_);
             if constexpr (std::is_same<T, bf16>::value)
                 hipLaunchKernelGGL(enc_attn_bf16_kernel, dim3((N_CTX + ea::QB - 1) / ea::QB, nb * H_), dim3(256), 0,
                                    st_, qh_, kh_, vt_, ob_, H_, d);
             else
                 hipLaunchKernelGGL(enc_attn_f32_kernel, dim3((N_CTX + 63) / 64, nb * H_), dim3(64), 0, st_, qh_, kh_,
                                    vt_, ob_, H_, d);
-            prof_end(WHISPER_K_ENC_ATTN);
+            prof_end(WHISPER_K_ENC_ATTN, st_);
             gemm(L.Wo, d, 0, ob_, d, 0, d, M, d, 1, EpiResid{L.bo, x_, d});
             ln(x_, zb_, L.ln2g, L.ln2b, M);
-            prof_begin(WHISPER_K_ENC_GEMM);
+            prof_begin(WHISPER_K_ENC_GEMM, st_);
             gemm(L.W1, d, 0, zb_, d, 0, 4 * d, M, d, 1, EpiGelu<T>{L.b1, hb_, 4 * d});
-            prof_end(WHISPER_K_ENC_GEMM);
+            prof_end(WHISPER_K_ENC_GEMM, st_);
             gemm(L.W2, 4 * d, 0, hb_, 4 * d, 0, d, M, 4 * d, 1, EpiResid{L.b2, x_, d});
         }
         ln(x_, zb_, lnpg_, lnpb_, M);
         gemm(zb_, d, 0, WcK_, d, 0, M, Ld_ * d, d, 1, EpiCrossK<T>{ktc_, slot_of_, d, H_, S_});
         gemm(WcV_, d, 0, zb_, d, 0, Ld_ * d, M, d, 1, EpiCrossV<T>{bcV_, vc_, slot_of_, d, H_, S_});
         hipLaunchKernelGGL(seat_kernel, dim3(nb), dim3(256), 0, st_, slot_of_, seat_np_, seat_prompts_, seq_, pos_, npr_);
-        prof_end(WHISPER_K_ENC_PASS);
+        prof_end(WHISPER_K_ENC_PASS, st_);
     }
 
     // -------------------------------------------------------------- setup
@@ -791,7 +851,7 @@ class EngineT final : public Engine {
         datt_ = dalloc<T>(S16 * d);
         dh_ = dalloc<T>(S16 * 4 * d);
         logits_ = dalloc<float>(S * (size_t)V_);
-        gpart_ = dalloc<float>(4 * S * d);  // split-K partials [4][S][d]
+        gpart_ = dalloc<float>(2 * 4 * S * d);  // split-K partials [half][4][rows][d]
         best_ = dalloc<unsigned long long>(S);
     }
 };

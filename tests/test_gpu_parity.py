@@ -140,3 +140,26 @@ def test_pad_mode_feature_domain_mel():
             want = oracle.log_mel_segment(s.audio, shape.n_mels, 1)
             assert np.abs(mel - want).max() < 2e-5
             assert np.all(mel[:, s.audio.size // 160:] == 0)
+
+
+def test_base_split_step_equals_unsplit(monkeypatch):
+    """With 32 or more slots a decode step runs as two halves on two streams;
+    every segment's tokens (and the logits of a teacher-forced step) equal
+    those of the same batch stepped unsplit (bit-exact)."""
+    shape = synth.BASE
+    W = synth.make_weights(shape, 0)
+    blob = synth.pack_blob(W)
+    segs = synth.uniform_batch(shape, 40, 8, seed=3)
+    out = {}
+    for split in ("1", "0"):
+        monkeypatch.setenv("WHISPER_STEP_SPLIT", split)
+        with binding.Context(blob, max_slots=40) as ctx:
+            log(f"split={split}: transcribe 40 segments")
+            res = ctx.transcribe(segs)
+            ctx.encode(segs, list(range(40)))
+            _, lg = ctx.decode_step(list(range(40)), logits=True)
+            out[split] = ([r["tokens"] for r in res], lg)
+            drain(ctx, list(range(40)))
+    for a, b in zip(out["1"][0], out["0"][0]):
+        assert np.array_equal(a, b)
+    assert np.array_equal(out["1"][1], out["0"][1])
