@@ -32,7 +32,7 @@ constexpr int BM = 256;   // A rows per workgroup
 constexpr int BN = 256;   // B rows per workgroup
 constexpr int BK = 32;    // K per LDS stage
 constexpr int NS = 4;     // LDS stages
-constexpr int THREADS = 256;
+constexpr int THREADS = 512;  // 8 waves
 constexpr int TILE_BYTES = BM * BK * 2;        // one operand tile of a stage (16 KiB)
 constexpr int STAGE_BYTES = 2 * TILE_BYTES;    // A and B tiles (32 KiB)
 constexpr int LDS_BYTES = NS * STAGE_BYTES;    // 128 KiB
@@ -49,25 +49,13 @@ __device__ inline int swz32(int r, int c) { return r * 64 + ((c ^ ((r >> 1) & 3)
 // Byte offset of 16-byte chunk c (0..7) of row r inside a [rows][64] bf16 LDS tile.
 __device__ inline int swz(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
 
-// A and B fragments of one 32-wide K tile for this wave (rows wa.., wb..).
-__device__ __forceinline__ void load_frags(mfma_bf16x8 (&fa)[8], mfma_bf16x8 (&fb)[8], const unsigned char* stage,
-                                           int wa, int wb, int fr, int fc) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) fa[i] = *reinterpret_cast<const mfma_bf16x8*>(stage + swz32(wa + i * 16 + fr, fc));
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-        fb[j] = *reinterpret_cast<const mfma_bf16x8*>(stage + gb::TILE_BYTES + swz32(wb + j * 16 + fr, fc));
-}
-__device__ __forceinline__ void mfma_8x8(mfma_f32x4 (&acc)[8][8], const mfma_bf16x8 (&fa)[8],
-                                         const mfma_bf16x8 (&fb)[8]) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-}
-
+// C = A B^T for A [MA][K], B [MB][K] (bf16, row-major, batched over z):
+// a 256 x 256 workgroup tile, 8 waves (2 per SIMD) of 128 x 64 each on
+// 16x16x32 MFMAs, so one wave's MFMAs run while the other waits on its LDS
+// reads or the stage barrier. Operands go global -> LDS directly through a
+// 4-stage ring of 32-wide K tiles.
 template <class Epi>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
+__global__ __launch_bounds__(512, 1) void gemm_bf16_kernel(
     const bf16* __restrict__ A, int lda, long long sA, const bf16* __restrict__ B, int ldb,
     long long sB, int MA, int MB, int K, int tilesA, Epi epi) {
     extern __shared__ __align__(16) unsigned char lds[];
@@ -79,64 +67,70 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
     const int tb = blockIdx.x / tilesA;
     const int a0 = ta * gb::BM, b0 = tb * gb::BN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wa = (wave & 1) * 128, wb = (wave >> 1) * 128;
-    const int fr = lane & 15, fc = lane >> 4;  // fragment row, 8-element k group
+    const int wa = (wave & 1) * 128, wb = (wave >> 1) * 64;
+    const int fr = lane & 15, fc = lane >> 4;
 
-    // Direct loads: one wave instruction fills 1 KiB of LDS (16 rows x 64 B),
-    // lane i landing at byte 16 i. Wave w fills rows 64 w .. 64 w + 63 of both
-    // operand tiles with 4 + 4 instructions; lane i loads row 16 s + i / 4 and
-    // the logical chunk stored at its physical position i % 4.
+    // Direct loads: wave w fills rows 32 w .. 32 w + 31 of both operand tiles
+    // with 2 + 2 instructions of 16 rows x 64 B; lane i loads row 16 s + i / 4
+    // and the logical chunk stored at its physical position i % 4.
     const int dr = lane >> 2;
     const int dc = (lane & 3) ^ ((dr >> 1) & 3);
-    const bf16* ga[4];
-    const bf16* gp[4];
+    const bf16* ga[2];
+    const bf16* gp[2];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        const int r = wave * 64 + s * 16 + dr;
+    for (int s = 0; s < 2; ++s) {
+        const int r = wave * 32 + s * 16 + dr;
         ga[s] = A + (long long)min(a0 + r, MA - 1) * lda + dc * 8;
         gp[s] = B + (long long)min(b0 + r, MB - 1) * ldb + dc * 8;
     }
-    const int ldsw = wave * 64 * 64;  // byte offset of this wave's rows in a tile
+    const int ldsw = wave * 32 * 64;
 
-    mfma_f32x4 acc[8][8];
+    mfma_f32x4 acc[8][4];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
 
-#define WMI_ISSUE(KT)                                                                                  \
+#define WMI_ISSUE8(KT)                                                                                 \
     do {                                                                                               \
         const int st_ = ((KT) % gb::NS) * gb::STAGE_BYTES + ldsw;                                      \
         const int k_ = (KT) * gb::BK;                                                                  \
-        _Pragma("unroll") for (int s = 0; s < 4; ++s)                                                 \
+        _Pragma("unroll") for (int s = 0; s < 2; ++s)                                                 \
             __builtin_amdgcn_global_load_lds(ga[s] + k_, lds + st_ + s * 1024, 16, 0, 0);              \
-        _Pragma("unroll") for (int s = 0; s < 4; ++s)                                                 \
+        _Pragma("unroll") for (int s = 0; s < 2; ++s)                                                 \
             __builtin_amdgcn_global_load_lds(gp[s] + k_, lds + st_ + gb::TILE_BYTES + s * 1024, 16, 0, 0); \
     } while (0)
 
     const int nk = K / gb::BK;
-    WMI_ISSUE(0);
-    if (nk > 1) WMI_ISSUE(1);
-    if (nk > 2) WMI_ISSUE(2);
+    WMI_ISSUE8(0);
+    if (nk > 1) WMI_ISSUE8(1);
+    if (nk > 2) WMI_ISSUE8(2);
     for (int kt = 0; kt < nk; ++kt) {
-        // tile kt has landed once only the 8-load groups of later tiles are pending
+        // tile kt has landed once only the 4-load groups of later tiles are pending
         const int later = min(nk - 1 - kt, gb::NS - 2);
-        if (later >= 2) __builtin_amdgcn_s_waitcnt(WMI_VMCNT(16));
-        else if (later == 1) __builtin_amdgcn_s_waitcnt(WMI_VMCNT(8));
+        if (later >= 2) __builtin_amdgcn_s_waitcnt(WMI_VMCNT(8));
+        else if (later == 1) __builtin_amdgcn_s_waitcnt(WMI_VMCNT(4));
         else __builtin_amdgcn_s_waitcnt(WMI_VMCNT(0));
         // every wave's part of tile kt is in LDS, and every wave is done with tile kt - 1
         __builtin_amdgcn_s_barrier();
-        if (kt + gb::NS - 1 < nk) WMI_ISSUE(kt + gb::NS - 1);
-        mfma_bf16x8 fa[8], fb[8];
-        load_frags(fa, fb, lds + (kt % gb::NS) * gb::STAGE_BYTES, wa, wb, fr, fc);
-        __builtin_amdgcn_sched_barrier(0);  // every fragment read is issued ahead of the MFMAs
-        mfma_8x8(acc, fa, fb);
-    }
-#undef WMI_ISSUE
-    // Lane holds C[i = base + 4*(lane>>4) + r][j = base + (lane & 15)]; the
-    // epilogue's loads for 8 fragments are issued before their stores.
+        if (kt + gb::NS - 1 < nk) WMI_ISSUE8(kt + gb::NS - 1);
+        const unsigned char* stage = lds + (kt % gb::NS) * gb::STAGE_BYTES;
+        mfma_bf16x8 fa[8], fb[4];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+        for (int i = 0; i < 8; ++i) fa[i] = *reinterpret_cast<const mfma_bf16x8*>(stage + swz32(wa + i * 16 + fr, fc));
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            fb[j] = *reinterpret_cast<const mfma_bf16x8*>(stage + gb::TILE_BYTES + swz32(wb + j * 16 + fr, fc));
+        __builtin_amdgcn_sched_barrier(0);  // every fragment read is issued ahead of the MFMAs
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+#undef WMI_ISSUE8
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
         const int jj = b0 + wb + j * 16 + fr;
         const bool jok = jj < MB;
         EpiPre pre[8];
@@ -166,7 +160,7 @@ inline void gemm_bf16(const bf16* A, int lda, long long sA, const bf16* B, int l
         attr_set = true;
     }
     dim3 grid(tilesA * tilesB, 1, batch);
-    hipLaunchKernelGGL(gemm_bf16_kernel<Epi>, grid, dim3(gb::THREADS), gb::LDS_BYTES, st, A, lda,
+    hipLaunchKernelGGL((gemm_bf16_kernel<Epi>), grid, dim3(gb::THREADS), gb::LDS_BYTES, st, A, lda,
                        sA, B, ldb, sB, MA, MB, K, tilesA, epi);
 }
 
