@@ -334,7 +334,7 @@ __global__ __launch_bounds__(256, 2) void enc_attn_bf16_kernel(const bf16* __res
             mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
             mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
             const float mnew = fmaxf(mrun[u], mx * LOG2E);
-            const float alpha = exp2f(mrun[u] - mnew);
+            const float alpha = exp2_softmax(mrun[u] - mnew);
             mrun[u] = mnew;
             float ls = 0.f;
             float pv[4][4];
@@ -342,7 +342,7 @@ __global__ __launch_bounds__(256, 2) void enc_attn_bf16_kernel(const bf16* __res
             for (int a = 0; a < 4; ++a)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    pv[a][r] = exp2f(fmaf(sc[a][u][r], LOG2E, -mnew));
+                    pv[a][r] = exp2_softmax(fmaf(sc[a][u][r], LOG2E, -mnew));
                     ls += pv[a][r];
                 }
             ls += __shfl_xor(ls, 16, 64);
@@ -425,7 +425,7 @@ __global__ __launch_bounds__(64) void enc_attn_f32_kernel(const float* __restric
             for (int j = 0; j < 64; ++j) s = fmaf(qv[j], ks[kk][j], s);
             s *= LOG2E;
             const float mnew = fmaxf(m, s);
-            const float alpha = exp2f(m - mnew), p = exp2f(s - mnew);
+            const float alpha = exp2_softmax(m - mnew), p = exp2_softmax(s - mnew);
             l = l * alpha + p;
 #pragma unroll
             for (int j = 0; j < 64; ++j) o[j] = fmaf(p, vs[j][kk], o[j] * alpha);
@@ -519,7 +519,7 @@ __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     float lsum = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        s[i] = (p0 + i < len) ? exp2f(s[i] - mx) : 0.f;
+        s[i] = (p0 + i < len) ? exp2_softmax(s[i] - mx) : 0.f;
         lsum += s[i];
     }
     lsum = wave_sum(lsum);
@@ -618,7 +618,7 @@ __global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {
     float lsum = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const float p = (p0 + i < N_CTX) ? exp2f(s[i] - mx) : 0.f;
+        const float p = (p0 + i < N_CTX) ? exp2_softmax(s[i] - mx) : 0.f;
         ps[w][lane * 4 + i] = p;
         lsum += p;
     }
@@ -664,7 +664,7 @@ __global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {
         float L = 0.f, acc = 0.f;
 #pragma unroll
         for (int c = 0; c < CW; ++c) {
-            const float wgt = exp2f(ml[c][0] - M);
+            const float wgt = exp2_softmax(ml[c][0] - M);
             L += wgt * ml[c][1];
             acc += wgt * op[c][tid];
         }
