@@ -96,7 +96,9 @@ typedef struct {
  *   prompt          host array of n_prompt token ids in [0, n_vocab)
  *   n_prompt        >= 1; n_prompt + max_new_tokens <= n_text_ctx
  *   max_new_tokens  >= 1: exactly this many tokens are generated
- *   arrival_us      queue priority key (whisper_batch_transcribe only)
+ *   arrival_us      queue priority key (whisper_batch_transcribe / _serve); with
+ *                   real-time admission also the time, in microseconds after
+ *                   the call starts, from which the segment may be served
  */
 typedef struct {
     const float* audio;
@@ -115,6 +117,8 @@ typedef struct {
 typedef struct {
     int64_t segment_id;
     int64_t token_offset;  /* first token in token_buf */
+    int64_t finish_us;     /* when the device had computed the segment's last token,
+                              in microseconds after the call started */
     int32_t user_id;
     int32_t status;        /* WHISPER_OK, or the error that stopped the batch */
     int32_t n_tokens;      /* = max_new_tokens when status is WHISPER_OK */
@@ -221,6 +225,20 @@ whisper_status whisper_batch_transcribe(whisper_ctx* ctx, const whisper_segment*
                                         int32_t n, int32_t* token_buf, int64_t token_buf_cap,
                                         whisper_result* results);
 
+/*
+ * whisper_batch_transcribe with optional real-time admission (the serving
+ * form of Section 2.2's central queue): with realtime != 0 a segment joins
+ * the queue only once arrival_us microseconds have passed since the call
+ * started; while nothing is runnable the call waits for the next arrival,
+ * and every encode pass and decode step completes before the next decision.
+ * realtime = 0 is exactly whisper_batch_transcribe. Tokens do not depend on
+ * admission times (segments are independent); results[i].finish_us records
+ * when each segment's last token was computed.
+ */
+whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs, int32_t n,
+                                   int32_t* token_buf, int64_t token_buf_cap,
+                                   whisper_result* results, int32_t realtime);
+
 /* Tensors readable with whisper_debug_copy (test use: per-stage parity). */
 enum {
     WHISPER_T_MEL = 0,     /* fp32 [n_mels][3000] normalised log-mel of entry `index`
@@ -288,13 +306,18 @@ whisper_status whisper_stats_read(whisper_ctx* ctx, whisper_stats* out, int32_t 
  * and, if events is not NULL, the schedule: one int32 triple per engine call
  * (kind 0 = encode, slot, input index) or (kind 1 = decode step, number of
  * active slots, 0), at most events_cap triples, count in *n_events.
+ * realtime != 0 runs real-time admission on a simulated clock that starts at
+ * 0 and advances by encode_us per encoded segment and step_us per decode
+ * step, and jumps to the next arrival when idle; finish_us is that clock
+ * after the segment's last step.
  */
 whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const int32_t* user_id,
                                     const int64_t* segment_id, const int32_t* max_new_tokens,
                                     int32_t slots, int32_t encode_batch, int32_t refill_min,
                                     int32_t* token_buf, int64_t token_buf_cap,
                                     whisper_result* results, int32_t* events,
-                                    int32_t events_cap, int32_t* n_events);
+                                    int32_t events_cap, int32_t* n_events, int32_t realtime,
+                                    int64_t encode_us, int64_t step_us);
 
 #ifdef __cplusplus
 }

@@ -21,7 +21,7 @@ K_CROSS_ATTN, K_ENC_GEMM, K_SELF_ATTN, K_ENC_ATTN, K_ENC_PASS, K_DEC_STEP, K_FRO
 EXPORTS = (
     "whisper_params_from_blob", "whisper_ctx_create", "whisper_ctx_destroy", "whisper_last_error",
     "whisper_ctx_set_stream", "whisper_batch_encode", "whisper_batch_decode_step",
-    "whisper_slot_tokens", "whisper_batch_transcribe", "whisper_debug_copy",
+    "whisper_slot_tokens", "whisper_batch_transcribe", "whisper_batch_serve", "whisper_debug_copy",
     "whisper_profile_enable", "whisper_profile_read", "whisper_stats_read", "whisper_test_batcher",
 )
 
@@ -43,8 +43,8 @@ class whisper_segment(C.Structure):
 
 
 class whisper_result(C.Structure):
-    _fields_ = [("segment_id", C.c_int64), ("token_offset", C.c_int64), ("user_id", C.c_int32),
-                ("status", C.c_int32), ("n_tokens", C.c_int32), ("reserved", C.c_int32)]
+    _fields_ = [("segment_id", C.c_int64), ("token_offset", C.c_int64), ("finish_us", C.c_int64),
+                ("user_id", C.c_int32), ("status", C.c_int32), ("n_tokens", C.c_int32), ("reserved", C.c_int32)]
 
 
 class whisper_stats(C.Structure):
@@ -77,12 +77,14 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "whisper_slot_tokens": (i32, [vp, i32, pi32, i32, pi32]),
         "whisper_batch_transcribe": (i32, [vp, C.POINTER(whisper_segment), i32, pi32, i64,
                                           C.POINTER(whisper_result)]),
+        "whisper_batch_serve": (i32, [vp, C.POINTER(whisper_segment), i32, pi32, i64,
+                                     C.POINTER(whisper_result), i32]),
         "whisper_debug_copy": (i32, [vp, i32, i32, vp, C.c_size_t]),
         "whisper_profile_enable": (i32, [vp, i32, i32]),
         "whisper_profile_read": (i32, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64)]),
         "whisper_stats_read": (i32, [vp, C.POINTER(whisper_stats), i32]),
         "whisper_test_batcher": (i32, [i32, C.POINTER(i64), pi32, C.POINTER(i64), pi32, i32, i32, i32,
-                                      pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32]),
+                                      pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32, i32, i64, i64]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -201,18 +203,23 @@ class Context:
         self._check(load().whisper_slot_tokens(self.h, slot, _ptr(buf, C.c_int32), cap, C.byref(n)))
         return buf[: min(n.value, cap)].copy()
 
-    def transcribe(self, segs, device_audio=None):
+    def transcribe(self, segs, device_audio=None, realtime: bool = False):
+        """whisper_batch_transcribe, or whisper_batch_serve with real-time
+        admission (segments served from their arrival_us) when realtime."""
         sa = _SegArray(segs, device_audio)
         total = sum(int(s.max_new_tokens) for s in segs)
         buf = np.zeros(max(1, total), dtype=np.int32)
         res = (whisper_result * max(1, len(segs)))()
-        self._check(load().whisper_batch_transcribe(self.h, sa.arr, len(segs), _ptr(buf, C.c_int32),
-                                                    buf.size, res))
+        if realtime:
+            st = load().whisper_batch_serve(self.h, sa.arr, len(segs), _ptr(buf, C.c_int32), buf.size, res, 1)
+        else:
+            st = load().whisper_batch_transcribe(self.h, sa.arr, len(segs), _ptr(buf, C.c_int32), buf.size, res)
+        self._check(st)
         out = []
         for i in range(len(segs)):
             r = res[i]
             out.append({"user_id": r.user_id, "segment_id": r.segment_id, "status": r.status,
-                        "tokens": buf[r.token_offset: r.token_offset + r.n_tokens].copy()})
+                        "finish_us": r.finish_us, "tokens": buf[r.token_offset: r.token_offset + r.n_tokens].copy()})
         return out
 
     def debug_copy(self, tensor: int, index: int, shape):
@@ -235,8 +242,9 @@ class Context:
 
 
 def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_batch, refill_min,
-                 events_cap=100000):
-    """Runs the library's scheduler on the host with its fake engine."""
+                 events_cap=100000, realtime=False, encode_us=0, step_us=0):
+    """Runs the library's scheduler on the host with its fake engine (and,
+    with realtime, real-time admission on the fake engine's simulated clock)."""
     lib = load()
     n = len(arrival_us)
     a = np.ascontiguousarray(arrival_us, dtype=np.int64)
@@ -251,8 +259,11 @@ def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_
     st = lib.whisper_test_batcher(n, _ptr(a, C.c_int64), _ptr(u, C.c_int32), _ptr(s, C.c_int64),
                                   _ptr(m, C.c_int32), slots, encode_batch, refill_min,
                                   _ptr(buf, C.c_int32), buf.size, res, _ptr(ev, C.c_int32),
-                                  events_cap, C.byref(ne))
+                                  events_cap, C.byref(ne), 1 if realtime else 0, encode_us, step_us)
     _check(st)
     results = [(res[i].segment_id, res[i].token_offset, res[i].user_id, res[i].status, res[i].n_tokens)
                for i in range(n)]
+    if realtime:
+        return buf[:total], results, ev[: 3 * min(ne.value, events_cap)].reshape(-1, 3), \
+            [res[i].finish_us for i in range(n)]
     return buf[:total], results, ev[: 3 * min(ne.value, events_cap)].reshape(-1, 3)

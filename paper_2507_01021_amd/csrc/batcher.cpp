@@ -9,7 +9,8 @@
 namespace wmi {
 
 void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots, int encode_batch, int refill_min,
-                             const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be) {
+                             const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be,
+                             bool realtime) {
     if (n_slots < 1 || encode_batch < 1 || refill_min < 1) throw std::invalid_argument("batcher: bad parameters");
     const int n = (int)segs.size();
     std::vector<int> order(n);
@@ -18,13 +19,24 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
         return std::make_tuple(segs[a].arrival_us, segs[a].user_id, segs[a].segment_id, a) <
                std::make_tuple(segs[b].arrival_us, segs[b].user_id, segs[b].segment_id, b);
     });
-    std::deque<int> queue(order.begin(), order.end());
+    // Not yet arrived (real-time admission) in priority order, which starts
+    // with arrival time: admitting a prefix keeps the queue in priority order.
+    std::deque<int> pending(order.begin(), order.end());
+    std::deque<int> queue;
+    auto admit = [&]() {
+        const int64_t now = realtime ? be.now_us() : 0;
+        while (!pending.empty() && (!realtime || segs[pending.front()].arrival_us <= now)) {
+            queue.push_back(pending.front());
+            pending.pop_front();
+        }
+    };
     std::set<int> free_slots;
     for (int s = 0; s < n_slots; ++s) free_slots.insert(s);
     std::vector<int> seg_of(n_slots, -1), steps_left(n_slots, 0);
     int active = 0;
     std::vector<int> idx, slots, list;
     for (;;) {
+        admit();
         const int nfree = n_slots - active;
         if (!queue.empty() && nfree > 0 && (nfree >= refill_min || active < refill_min)) {
             while (!queue.empty() && !free_slots.empty()) {
@@ -44,7 +56,11 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
                 active += (int)idx.size();
             }
         }
-        if (active == 0) break;  // nothing active means nothing queued either
+        if (active == 0) {
+            if (pending.empty()) break;  // nothing active, queued or still to arrive
+            be.wait_until(segs[pending.front()].arrival_us);
+            continue;
+        }
         list.clear();
         for (int s = 0; s < n_slots; ++s)
             if (seg_of[s] >= 0) list.push_back(s);

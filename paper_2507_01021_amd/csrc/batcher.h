@@ -11,6 +11,11 @@
 // n_prompt + max_new_tokens - 1 steps and its tokens are copied to the
 // caller's buffer at the segment's input-order offset. Results do not depend
 // on the policy's parameters, because each segment is an independent unit.
+//
+// Real-time admission (optional): a segment joins the queue only once the
+// backend's clock has reached its arrival_us; with nothing to run, the
+// batcher waits for the next arrival. Without it every segment is queued at
+// the start (arrival_us is then only the priority key).
 #pragma once
 
 #include <stdint.h>
@@ -34,14 +39,19 @@ class BatchBackend {
     virtual void encode(const int* idx, int n, const int* slots) = 0;
     // One decode step over the listed slots (ascending).
     virtual void step(const int* slots, int n) = 0;
-    // Slot finished segment idx: deliver its `count` tokens to dst (may be
-    // deferred until finish()).
+    // Slot finished segment idx with the step just run: deliver its `count`
+    // tokens to dst (may be deferred until finish()) and note its finish time.
     virtual void retire(int slot, int idx, int count, int32_t* dst) = 0;
     virtual void finish() = 0;
+    // Real-time admission only: microseconds since the run started (work
+    // already submitted has completed), and waiting until that clock reaches t.
+    virtual int64_t now_us() { return 0; }
+    virtual void wait_until(int64_t) {}
 };
 
 // Runs the whole queue; offsets[i] is segment i's first token in token_buf.
 void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots, int encode_batch, int refill_min,
-                             const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be);
+                             const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be,
+                             bool realtime = false);
 
 }  // namespace wmi

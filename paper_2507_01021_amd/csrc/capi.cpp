@@ -5,6 +5,7 @@
 
 #include <chrono>
 #include <memory>
+#include <thread>
 #include <new>
 #include <set>
 #include <string>
@@ -104,8 +105,12 @@ struct EngineBackend : wmi::BatchBackend {
     using clock = std::chrono::steady_clock;
     whisper_ctx* c;
     const whisper_segment* segs;
+    bool realtime = false;
+    clock::time_point t0 = clock::now();
     std::vector<wmi::SegmentDesc> descs;
-    std::vector<int> steps;  // decode steps taken by each slot's current segment
+    std::vector<int> steps;    // decode steps taken by each slot's current segment
+    std::vector<int> mark_of;  // completion mark of each retired segment
+    int step_mark = -1;        // mark after the latest step, once a segment retired with it
     double engine_ms = 0.0;
     struct Timer {
         double& acc;
@@ -120,25 +125,35 @@ struct EngineBackend : wmi::BatchBackend {
             descs[k] = wmi::SegmentDesc{s.audio, s.n_samples, s.audio_on_device == 1, s.prompt, s.n_prompt};
             steps[slots[k]] = 0;
         }
-        c->eng->encode(descs.data(), n, slots, false);
+        c->eng->encode(descs.data(), n, slots, realtime);
         c->stats.encode_passes += (n + c->p.max_encode_batch - 1) / c->p.max_encode_batch;
         c->stats.segments_encoded += n;
         c->stats.refill_batches += 1;
     }
     void step(const int* slots, int n) override {
         Timer t{engine_ms};
-        c->eng->decode_step(slots, n, nullptr, nullptr, nullptr, false);
+        c->eng->decode_step(slots, n, nullptr, nullptr, nullptr, realtime);
+        step_mark = -1;
         c->stats.decode_steps += 1;
         c->stats.rows_decoded += n;
         for (int k = 0; k < n; ++k) c->stats.positions_attended += ++steps[slots[k]];
     }
-    void retire(int slot, int, int count, int32_t* dst) override {
+    void retire(int slot, int idx, int count, int32_t* dst) override {
         Timer t{engine_ms};
+        if (step_mark < 0) step_mark = c->eng->mark();
+        mark_of[idx] = step_mark;
         c->eng->read_tokens_async(slot, count, dst);
     }
     void finish() override {
         Timer t{engine_ms};
         c->eng->finish_reads();
+    }
+    int64_t now_us() override {
+        return std::chrono::duration_cast<std::chrono::microseconds>(clock::now() - t0).count();
+    }
+    void wait_until(int64_t t) override {
+        const int64_t dt = t - now_us();
+        if (dt > 0) std::this_thread::sleep_for(std::chrono::microseconds(dt));
     }
 };
 
@@ -146,15 +161,24 @@ struct EngineBackend : wmi::BatchBackend {
 struct FakeBackend : wmi::BatchBackend {
     const int64_t* seg_ids;
     std::vector<int32_t>* events;
+    std::vector<int64_t>* finish_at;
+    int64_t clock_us = 0, encode_us = 0, step_us = 0;
     void encode(const int* idx, int n, const int* slots) override {
         for (int k = 0; k < n; ++k) events->insert(events->end(), {0, slots[k], idx[k]});
+        clock_us += encode_us * n;
     }
-    void step(const int*, int n) override { events->insert(events->end(), {1, n, 0}); }
+    void step(const int*, int n) override {
+        events->insert(events->end(), {1, n, 0});
+        clock_us += step_us;
+    }
     void retire(int, int idx, int count, int32_t* dst) override {
         for (int j = 0; j < count; ++j)
             dst[j] = (int32_t)((uint64_t)(seg_ids[idx] * 7919 + (int64_t)j * 104729) % 50000);
+        (*finish_at)[idx] = clock_us;
     }
     void finish() override {}
+    int64_t now_us() override { return clock_us; }
+    void wait_until(int64_t t) override { clock_us = t > clock_us ? t : clock_us; }
 };
 
 std::vector<int64_t> offsets_of(const std::vector<wmi::QueuedSegment>& q, int64_t* total) {
@@ -302,8 +326,8 @@ whisper_status whisper_slot_tokens(whisper_ctx* ctx, int32_t slot, int32_t* dst,
     });
 }
 
-whisper_status whisper_batch_transcribe(whisper_ctx* ctx, const whisper_segment* segs, int32_t n, int32_t* token_buf,
-                                        int64_t token_buf_cap, whisper_result* results) {
+whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs, int32_t n, int32_t* token_buf,
+                                   int64_t token_buf_cap, whisper_result* results, int32_t realtime) {
     if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
     if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
     if (n < 0) return fail(ctx, WHISPER_E_INVAL, "n must be >= 0");
@@ -315,6 +339,8 @@ whisper_status whisper_batch_transcribe(whisper_ctx* ctx, const whisper_segment*
     for (int i = 0; i < n; ++i) {
         const std::string bad = check_segment(ctx->p, segs[i], i);
         if (!bad.empty()) return fail(ctx, WHISPER_E_INVAL, bad);
+        if (realtime && segs[i].arrival_us < 0)
+            return fail(ctx, WHISPER_E_INVAL, "segment " + std::to_string(i) + ": arrival_us must be >= 0");
         q[i] = wmi::QueuedSegment{segs[i].arrival_us, segs[i].user_id, segs[i].segment_id, segs[i].n_prompt,
                                   segs[i].max_new_tokens};
     }
@@ -323,24 +349,37 @@ whisper_status whisper_batch_transcribe(whisper_ctx* ctx, const whisper_segment*
     if (!token_buf || token_buf_cap < total)
         return fail(ctx, WHISPER_E_BUFFER, "token_buf needs " + std::to_string(total) + " entries");
     for (int i = 0; i < n; ++i)
-        results[i] = whisper_result{segs[i].segment_id, off[i], segs[i].user_id, WHISPER_OK, segs[i].max_new_tokens, 0};
+        results[i] = whisper_result{segs[i].segment_id, off[i], 0, segs[i].user_id, WHISPER_OK,
+                                    segs[i].max_new_tokens, 0};
     const whisper_status r = guarded(ctx, [&]() -> whisper_status {
         EngineBackend be;
         be.c = ctx;
         be.segs = segs;
+        be.realtime = realtime != 0;
         be.steps.assign(ctx->p.max_slots, 0);
-        const auto t0 = EngineBackend::clock::now();
+        be.mark_of.assign(n, -1);
+        ctx->eng->mark_reset();
+        be.t0 = EngineBackend::clock::now();
         wmi::run_continuous_batching(q, ctx->p.max_slots, ctx->p.max_encode_batch, ctx->p.refill_min, off, token_buf,
-                                     be);
-        const double total = std::chrono::duration<double, std::milli>(EngineBackend::clock::now() - t0).count();
+                                     be, be.realtime);
+        const double total_ms =
+            std::chrono::duration<double, std::milli>(EngineBackend::clock::now() - be.t0).count();
         ctx->stats.engine_host_ms += be.engine_ms;
-        ctx->stats.batcher_host_ms += total - be.engine_ms;
+        ctx->stats.batcher_host_ms += total_ms - be.engine_ms;
+        const std::vector<double> t = ctx->eng->mark_times_us();
+        for (int i = 0; i < n; ++i)
+            if (be.mark_of[i] >= 0) results[i].finish_us = (int64_t)t[be.mark_of[i]];
         return WHISPER_OK;
     });
     for (auto& s : ctx->slots) s = SlotState();
     if (r != WHISPER_OK)
         for (int i = 0; i < n; ++i) { results[i].status = r; results[i].n_tokens = 0; }
     return r;
+}
+
+whisper_status whisper_batch_transcribe(whisper_ctx* ctx, const whisper_segment* segs, int32_t n, int32_t* token_buf,
+                                        int64_t token_buf_cap, whisper_result* results) {
+    return whisper_batch_serve(ctx, segs, n, token_buf, token_buf_cap, results, 0);
 }
 
 whisper_status whisper_debug_copy(whisper_ctx* ctx, int32_t tensor, int32_t index, void* dst, size_t bytes) {
@@ -386,11 +425,13 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
                                     const int64_t* segment_id, const int32_t* max_new_tokens, int32_t slots,
                                     int32_t encode_batch, int32_t refill_min, int32_t* token_buf,
                                     int64_t token_buf_cap, whisper_result* results, int32_t* events,
-                                    int32_t events_cap, int32_t* n_events) {
+                                    int32_t events_cap, int32_t* n_events, int32_t realtime, int64_t encode_us,
+                                    int64_t step_us) {
     if (n < 0 || (n > 0 && (!arrival_us || !user_id || !segment_id || !max_new_tokens || !results)))
         return fail(nullptr, WHISPER_E_INVAL, "bad arguments");
     if (slots < 1 || encode_batch < 1 || refill_min < 1)
         return fail(nullptr, WHISPER_E_INVAL, "slots, encode_batch and refill_min must be >= 1");
+    if (encode_us < 0 || step_us < 0) return fail(nullptr, WHISPER_E_INVAL, "clock steps must be >= 0");
     std::vector<wmi::QueuedSegment> q(n);
     for (int i = 0; i < n; ++i) {
         if (max_new_tokens[i] < 1) return fail(nullptr, WHISPER_E_INVAL, "max_new_tokens must be >= 1");
@@ -401,16 +442,20 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
     if ((total > 0 && !token_buf) || token_buf_cap < total)
         return fail(nullptr, WHISPER_E_BUFFER, "token_buf needs " + std::to_string(total) + " entries");
     std::vector<int32_t> ev;
+    std::vector<int64_t> fin(n, 0);
     FakeBackend be;
     be.seg_ids = segment_id;
     be.events = &ev;
+    be.finish_at = &fin;
+    be.encode_us = encode_us;
+    be.step_us = step_us;
     try {
-        wmi::run_continuous_batching(q, slots, encode_batch, refill_min, off, token_buf, be);
+        wmi::run_continuous_batching(q, slots, encode_batch, refill_min, off, token_buf, be, realtime != 0);
     } catch (const std::exception& e) {
         return fail(nullptr, WHISPER_E_INVAL, e.what());
     }
     for (int i = 0; i < n; ++i)
-        results[i] = whisper_result{segment_id[i], off[i], user_id[i], WHISPER_OK, max_new_tokens[i], 0};
+        results[i] = whisper_result{segment_id[i], off[i], fin[i], user_id[i], WHISPER_OK, max_new_tokens[i], 0};
     if (n_events) *n_events = (int32_t)(ev.size() / 3);
     if (events) {
         const size_t k = ev.size() < (size_t)events_cap * 3 ? ev.size() : (size_t)events_cap * 3;

@@ -8,6 +8,7 @@
 #include <stdint.h>
 
 #include <memory>
+#include <vector>
 
 #include "../../include/whisper_mi355x.h"
 
@@ -42,6 +43,13 @@ class Engine {
     virtual void debug_copy(int tensor, int index, void* dst, size_t bytes) = 0;
     virtual void profile_enable(int kernel, bool on) = 0;
     virtual void profile_read(int kernel, double* ms, int64_t* launches) = 0;
+    // Completion-time marks: mark_reset() starts the clock on the stream,
+    // mark() records a point after the work queued so far and returns its
+    // index, mark_times_us() waits for the stream and returns every mark's
+    // time in microseconds since the reset.
+    virtual void mark_reset() = 0;
+    virtual int mark() = 0;
+    virtual std::vector<double> mark_times_us() = 0;
 };
 
 // Throws ArgError (code = whisper_status) or DeviceError.

@@ -229,6 +229,8 @@ class EngineT final : public Engine {
         for (auto& pr : prof_)
             for (auto& e : pr.used) { (void)hipEventDestroy(e.first); (void)hipEventDestroy(e.second); }
         for (auto e : event_pool_) (void)hipEventDestroy(e);
+        for (auto e : marks_) (void)hipEventDestroy(e);
+        if (mark_start_) (void)hipEventDestroy(mark_start_);
         if (st2_) (void)hipStreamSynchronize(st2_);
         for (auto& g : step_graphs_)
             for (auto ge : g.second)
@@ -440,6 +442,30 @@ class EngineT final : public Engine {
         }
     }
 
+    // -------------------------------------------------------------- completion marks
+    void mark_reset() override {
+        for (auto e : marks_) event_pool_.push_back(e);
+        marks_.clear();
+        if (!mark_start_) mark_start_ = get_event();
+        WMI_HIP(hipEventRecord(mark_start_, st_));
+    }
+    int mark() override {
+        hipEvent_t e = get_event();
+        WMI_HIP(hipEventRecord(e, st_));
+        marks_.push_back(e);
+        return (int)marks_.size() - 1;
+    }
+    std::vector<double> mark_times_us() override {
+        WMI_HIP(hipStreamSynchronize(st_));
+        std::vector<double> t(marks_.size());
+        for (size_t i = 0; i < marks_.size(); ++i) {
+            float ms = 0.f;
+            WMI_HIP(hipEventElapsedTime(&ms, mark_start_, marks_[i]));
+            t[i] = 1e3 * ms;
+        }
+        return t;
+    }
+
     // -------------------------------------------------------------- profiling
     void profile_enable(int k, bool on) override {
         WMI_HIP(hipStreamSynchronize(st_));
@@ -509,6 +535,8 @@ class EngineT final : public Engine {
     std::vector<PendingRead> pending_;
     Prof prof_[WHISPER_K_COUNT];
     std::vector<hipEvent_t> event_pool_;
+    hipEvent_t mark_start_ = nullptr;
+    std::vector<hipEvent_t> marks_;
 
     template <class U>
     U* dalloc(size_t count) {

@@ -301,3 +301,26 @@ def workload(name: str, seed: int = 1):
 
 
 WORKLOADS = ("tiny-b2", "base-b16", "small-u8-b64", "large-v3-b32", "turbo-u64-q512")
+
+
+def recording(shape: ModelShape, rng: np.random.Generator, seconds: float, user_id: int, first_id: int,
+              arrival_us: int = 0, tokens_per_s: float = 3.3) -> list:
+    """One user's recording of `seconds` cut into VAD-style segments of 3-30 s
+    (lengths drawn uniformly, the last one taking the remainder), each with
+    the standard prompt and max(4, round(tokens_per_s * length)) tokens (at
+    most 224): dictation speed of about 2.5 words per second. Every segment
+    arrives with the recording."""
+    p = prompt_for(shape)
+    left = float(seconds)
+    lengths = []
+    while left > 30.0:
+        L = float(rng.uniform(3.0, min(30.0, left - 3.0)))
+        lengths.append(L)
+        left -= L
+    lengths.append(left)
+    segs = []
+    for k, L in enumerate(lengths):
+        n = int(round(L * SAMPLE_RATE))
+        nt = int(min(224, max(4, round(tokens_per_s * L))))
+        segs.append(Segment(synth_audio(rng, n), user_id, first_id + k, list(p), nt, int(arrival_us)))
+    return segs

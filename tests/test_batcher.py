@@ -103,3 +103,63 @@ def test_bad_arguments(lib):
         binding.test_batcher([0], [0], [0], [1], 0, 1, 1)
     toks, res, ev = binding.test_batcher([], [], [], [], 2, 1, 1)
     assert len(res) == 0 and len(ev) == 0
+
+
+def simulate_realtime(arrival, user, seg, new, slots, eb, R, enc_us, step_us):
+    """Brute force of real-time admission on the fake engine's clock: a
+    segment is queued once the clock has reached its arrival; encoding costs
+    enc_us per segment, a step step_us; an idle batcher jumps to the next
+    arrival. Returns the engine calls and every segment's finish time."""
+    n = len(arrival)
+    pending = sorted(range(n), key=lambda i: (arrival[i], user[i], seg[i], i))
+    queue, free = [], list(range(slots))
+    seg_of, left = [-1] * slots, [0] * slots
+    events, finish, clock = [], [0] * n, 0
+    while True:
+        while pending and arrival[pending[0]] <= clock:
+            queue.append(pending.pop(0))
+        active = slots - len(free)
+        if queue and free and (len(free) >= R or active < R):
+            while queue and free:
+                k = 0
+                while queue and free and k < eb:
+                    i = queue.pop(0)
+                    s = min(free)
+                    free.remove(s)
+                    seg_of[s], left[s] = i, new[i]
+                    events.append((0, s, i))
+                    k += 1
+                clock += enc_us * k
+        if slots - len(free) == 0:
+            if not pending:
+                break
+            clock = max(clock, arrival[pending[0]])
+            continue
+        lst = [s for s in range(slots) if seg_of[s] >= 0]
+        events.append((1, len(lst), 0))
+        clock += step_us
+        for s in lst:
+            left[s] -= 1
+            if left[s] == 0:
+                finish[seg_of[s]] = clock
+                seg_of[s] = -1
+                free.append(s)
+    return events, finish
+
+
+@pytest.mark.parametrize("n,users,slots,eb,R,enc,step", [(1, 1, 1, 1, 1, 100, 1000), (12, 3, 4, 2, 1, 50_000, 400_000),
+                                                         (40, 8, 8, 3, 4, 20_000, 150_000),
+                                                         (64, 8, 16, 16, 16, 5_000, 30_000),
+                                                         (30, 5, 40, 7, 16, 0, 1)])
+def test_realtime_admission_matches_bruteforce(lib, n, users, slots, eb, R, enc, step):
+    """Segments are served only once they have arrived; with nothing to run
+    the batcher waits for the next arrival (simulated clock)."""
+    a, u, s, m = workload(n, users, seed=n + 7)
+    toks, res, ev, fin = binding.test_batcher(a, u, s, m, slots, eb, R, realtime=True, encode_us=enc, step_us=step)
+    want_ev, want_fin = simulate_realtime(a, u, s, m, slots, eb, R, enc, step)
+    assert [tuple(e) for e in ev] == want_ev
+    assert fin == want_fin
+    assert all(f >= t for f, t in zip(fin, a))
+    off = np.concatenate([[0], np.cumsum(m)[:-1]])
+    for i in range(n):
+        assert list(toks[off[i]: off[i] + m[i]]) == fake_tokens(s[i], m[i])

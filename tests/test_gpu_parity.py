@@ -163,3 +163,22 @@ def test_base_split_step_equals_unsplit(monkeypatch):
     for a, b in zip(out["1"][0], out["0"][0]):
         assert np.array_equal(a, b)
     assert np.array_equal(out["1"][1], out["0"][1])
+
+
+def test_serve_realtime_admission_tokens_and_times(tiny):
+    """Real-time admission: segments arriving 0-150 ms apart get the same
+    tokens as the offline call, and none finishes before it arrived."""
+    shape, W, segs, ref, ctx = tiny
+    import copy
+    late = []
+    for k, s in enumerate(segs * 2):
+        t = copy.copy(s)
+        t.segment_id = k
+        t.arrival_us = 75_000 * k
+        late.append(t)
+    offline = ctx.transcribe(late)
+    served = ctx.transcribe(late, realtime=True)
+    for s, a, b in zip(late, offline, served):
+        assert np.array_equal(a["tokens"], b["tokens"])
+        assert b["finish_us"] >= s.arrival_us
+    assert all(r["finish_us"] > 0 for r in offline)
