@@ -210,13 +210,28 @@ def decoder_step(W, shape, token, cache, ckv_seg):
     return (_ln(W, "dec.ln", x) @ _w(W, "dec.tok_emb").T)[0]
 
 
-def greedy(W, shape, ckv_seg, prompt, n_new, forced=None, cached=True):
-    """Greedy decode of exactly n_new tokens after the prompt.
+def pick_token(logits, step, suppress=(), suppress_begin=()):
+    """The greedy choice at generated position `step` (0 = first token after
+    the prompt) with logit filters: ids in `suppress` can never be chosen,
+    ids in `suppress_begin` not at step 0; among the rest, the largest logit,
+    lowest id on ties."""
+    lg = np.array(logits, dtype=np.float64, copy=True)
+    if len(suppress):
+        lg[np.asarray(list(suppress), dtype=np.int64)] = -np.inf
+    if step == 0 and len(suppress_begin):
+        lg[np.asarray(list(suppress_begin), dtype=np.int64)] = -np.inf
+    return int(np.argmax(lg))                # first maximum = lowest id on ties
 
-    Token 1 is the argmax at the prompt's last position; token i+1 is the
-    argmax after feeding token i (or forced[i-1] when teacher forcing).
-    Returns (tokens [n_new] int64, logits [n_new, V] float64), the logits
-    being those each token was taken from."""
+
+def greedy(W, shape, ckv_seg, prompt, n_new, forced=None, cached=True, eot=None, suppress=(),
+           suppress_begin=()):
+    """Greedy decode of up to n_new tokens after the prompt.
+
+    Token 1 is the choice (pick_token) at the prompt's last position; token
+    i+1 the choice after feeding token i (or forced[i-1] when teacher
+    forcing). Decoding stops early when the choice is `eot` (end of text,
+    not returned). Returns (tokens int64, logits float64): one logits row
+    per choice made, i.e. one more row than tokens when stopped by eot."""
     prompt = [int(t) for t in prompt]
     if len(prompt) < 1 or len(prompt) + n_new > shape.n_text_ctx:
         raise ValueError("prompt length + n_new must fit the text context")
@@ -228,17 +243,21 @@ def greedy(W, shape, ckv_seg, prompt, n_new, forced=None, cached=True):
         nxt = prompt[-1]
         for i in range(n_new):
             lg = decoder_step(W, shape, nxt, cache, ckv_seg)
-            g = int(np.argmax(lg))           # first maximum = lowest id on ties
-            toks.append(g)
+            g = pick_token(lg, i, suppress, suppress_begin)
             logits.append(lg)
+            if eot is not None and g == eot:
+                break
+            toks.append(g)
             nxt = g if forced is None else int(forced[i])
     else:
         seq = list(prompt)
         for i in range(n_new):
             lg = decoder_logits_full(W, shape, seq, ckv_seg)[-1]
-            g = int(np.argmax(lg))
-            toks.append(g)
+            g = pick_token(lg, i, suppress, suppress_begin)
             logits.append(lg)
+            if eot is not None and g == eot:
+                break
+            toks.append(g)
             seq.append(g if forced is None else int(forced[i]))
     return np.array(toks, dtype=np.int64), np.stack(logits)
 

@@ -274,3 +274,62 @@ def test_prompt_length_validation(weights):
         M.greedy(weights, SMALL_SHAPE, None, [], 3)
     with pytest.raises(ValueError):
         M.greedy(weights, SMALL_SHAPE, None, PROMPT, 445)
+
+
+# ---------------------------------------------------------------- logit filters and end of text
+
+def test_pick_token_is_the_filtered_argmax():
+    """By definition: the choice is allowed, no allowed id has a larger
+    logit, and no allowed id with an equal logit is smaller (small integer
+    logits make ties common)."""
+    g = _rng(11)
+    for trial in range(200):
+        lg = g.integers(-3, 4, 40).astype(np.float64)
+        sup = set(g.choice(40, g.integers(0, 10), replace=False).tolist())
+        beg = set(g.choice(40, g.integers(0, 10), replace=False).tolist())
+        step = int(g.integers(0, 3))
+        banned = sup | (beg if step == 0 else set())
+        if len(banned) == 40:
+            continue
+        t = M.pick_token(lg, step, sup, beg)
+        assert t not in banned
+        allowed = [i for i in range(40) if i not in banned]
+        assert lg[t] == max(lg[i] for i in allowed)
+        assert t == min(i for i in allowed if lg[i] == lg[t])
+
+
+def _ref_run(weights, segments, n=6):
+    s = segments[0]
+    E = M.encoder(weights, SMALL_SHAPE, oracle.log_mel_segment(s.audio, SMALL_SHAPE.n_mels)[None])
+    ckv = M._seg_ckv(M.cross_kv(weights, SMALL_SHAPE, E), 0)
+    toks, lg = M.greedy(weights, SMALL_SHAPE, ckv, s.prompt, n)
+    return ckv, s.prompt, toks, lg
+
+
+def test_end_of_text_truncates_the_unconstrained_run(weights, segments):
+    ckv, prompt, toks, lg = _ref_run(weights, segments)
+    # the first position holding a token not seen before it (position 0 if none later)
+    k = next((i for i in range(1, len(toks)) if toks[i] not in toks[:i]), 0)
+    got, glg = M.greedy(weights, SMALL_SHAPE, ckv, prompt, len(toks), eot=int(toks[k]))
+    assert np.array_equal(got, toks[:k])
+    assert len(glg) == k + 1 and np.array_equal(glg, lg[:k + 1])   # one row per choice, the stop included
+
+
+def test_suppressing_the_choice_takes_the_runner_up(weights, segments):
+    ckv, prompt, toks, lg = _ref_run(weights, segments)
+    got, glg = M.greedy(weights, SMALL_SHAPE, ckv, prompt, 1, suppress={int(toks[0])})
+    order = np.argsort(-lg[0], kind="stable")
+    assert order[0] == toks[0] and got[0] == order[1]
+    got_b, _ = M.greedy(weights, SMALL_SHAPE, ckv, prompt, 1, suppress_begin={int(toks[0])})
+    assert got_b[0] == order[1]
+
+
+def test_begin_suppression_applies_to_the_first_choice_only(weights, segments):
+    """With the first choice begin-suppressed, the run takes the runner-up r
+    first and then continues exactly as the unfiltered run whose prompt ends
+    with r (the begin list no longer applies)."""
+    ckv, prompt, toks, lg = _ref_run(weights, segments)
+    r = int(np.argsort(-lg[0], kind="stable")[1])
+    got, _ = M.greedy(weights, SMALL_SHAPE, ckv, prompt, len(toks), suppress_begin={int(toks[0])})
+    rest, _ = M.greedy(weights, SMALL_SHAPE, ckv, list(prompt) + [r], len(toks) - 1)
+    assert got[0] == r and np.array_equal(got[1:], rest)
