@@ -239,6 +239,25 @@ whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs
                                    int32_t* token_buf, int64_t token_buf_cap,
                                    whisper_result* results, int32_t realtime);
 
+/*
+ * Decoding options of the context (real use of the listing's generate),
+ * for every later decode step; requires every slot idle.
+ *   eot             end-of-text token id, or -1 (default): with an id,
+ *                   whisper_batch_transcribe / _serve end a segment at its
+ *                   first end-of-text token: results[i].n_tokens counts the
+ *                   tokens before it (<= max_new_tokens) and the rest of its
+ *                   token_buf range is -1. whisper_batch_decode_step does not
+ *                   stop by itself (the caller sees the token).
+ *   suppress        n_suppress ids that are never chosen (logit filter)
+ *   suppress_first  n_first ids that are not chosen as a segment's first
+ *                   generated token (e.g. blank and end of text)
+ * The filters act on the choice only: out_logits stay unfiltered. Ids must
+ * be in [0, n_vocab) and must not cover every id. Defaults: no filters.
+ */
+whisper_status whisper_set_decoding(whisper_ctx* ctx, int32_t eot, const int32_t* suppress,
+                                    int32_t n_suppress, const int32_t* suppress_first,
+                                    int32_t n_first);
+
 /* Tensors readable with whisper_debug_copy (test use: per-stage parity). */
 enum {
     WHISPER_T_MEL = 0,     /* fp32 [n_mels][3000] normalised log-mel of entry `index`
@@ -309,7 +328,8 @@ whisper_status whisper_stats_read(whisper_ctx* ctx, whisper_stats* out, int32_t 
  * realtime != 0 runs real-time admission on a simulated clock that starts at
  * 0 and advances by encode_us per encoded segment and step_us per decode
  * step, and jumps to the next arrival when idle; finish_us is that clock
- * after the segment's last step.
+ * after the segment's last step. eot >= 0 stops a segment at its first fake
+ * token equal to eot (polled one step late, as the engine's backend does).
  */
 whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const int32_t* user_id,
                                     const int64_t* segment_id, const int32_t* max_new_tokens,
@@ -317,7 +337,7 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
                                     int32_t* token_buf, int64_t token_buf_cap,
                                     whisper_result* results, int32_t* events,
                                     int32_t events_cap, int32_t* n_events, int32_t realtime,
-                                    int64_t encode_us, int64_t step_us);
+                                    int64_t encode_us, int64_t step_us, int32_t eot);
 
 #ifdef __cplusplus
 }

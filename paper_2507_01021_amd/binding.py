@@ -22,7 +22,8 @@ EXPORTS = (
     "whisper_params_from_blob", "whisper_ctx_create", "whisper_ctx_destroy", "whisper_last_error",
     "whisper_ctx_set_stream", "whisper_batch_encode", "whisper_batch_decode_step",
     "whisper_slot_tokens", "whisper_batch_transcribe", "whisper_batch_serve", "whisper_debug_copy",
-    "whisper_profile_enable", "whisper_profile_read", "whisper_stats_read", "whisper_test_batcher",
+    "whisper_profile_enable", "whisper_profile_read", "whisper_stats_read", "whisper_set_decoding",
+    "whisper_test_batcher",
 )
 
 
@@ -83,8 +84,9 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "whisper_profile_enable": (i32, [vp, i32, i32]),
         "whisper_profile_read": (i32, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64)]),
         "whisper_stats_read": (i32, [vp, C.POINTER(whisper_stats), i32]),
+        "whisper_set_decoding": (i32, [vp, i32, pi32, i32, pi32, i32]),
         "whisper_test_batcher": (i32, [i32, C.POINTER(i64), pi32, C.POINTER(i64), pi32, i32, i32, i32,
-                                      pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32, i32, i64, i64]),
+                                      pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32, i32, i64, i64, i32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -235,6 +237,12 @@ class Context:
         self._check(load().whisper_profile_read(self.h, kernel, C.byref(ms), C.byref(n)))
         return ms.value, n.value
 
+    def set_decoding(self, eot: int = -1, suppress=(), suppress_first=()):
+        a = np.ascontiguousarray(list(suppress), dtype=np.int32)
+        b = np.ascontiguousarray(list(suppress_first), dtype=np.int32)
+        self._check(load().whisper_set_decoding(self.h, int(eot), _ptr(a, C.c_int32), a.size, _ptr(b, C.c_int32),
+                                                b.size))
+
     def stats(self, reset: bool = False) -> dict:
         st = whisper_stats()
         self._check(load().whisper_stats_read(self.h, C.byref(st), 1 if reset else 0))
@@ -242,7 +250,7 @@ class Context:
 
 
 def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_batch, refill_min,
-                 events_cap=100000, realtime=False, encode_us=0, step_us=0):
+                 events_cap=100000, realtime=False, encode_us=0, step_us=0, eot=-1):
     """Runs the library's scheduler on the host with its fake engine (and,
     with realtime, real-time admission on the fake engine's simulated clock)."""
     lib = load()
@@ -259,7 +267,7 @@ def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_
     st = lib.whisper_test_batcher(n, _ptr(a, C.c_int64), _ptr(u, C.c_int32), _ptr(s, C.c_int64),
                                   _ptr(m, C.c_int32), slots, encode_batch, refill_min,
                                   _ptr(buf, C.c_int32), buf.size, res, _ptr(ev, C.c_int32),
-                                  events_cap, C.byref(ne), 1 if realtime else 0, encode_us, step_us)
+                                  events_cap, C.byref(ne), 1 if realtime else 0, encode_us, step_us, eot)
     _check(st)
     results = [(res[i].segment_id, res[i].token_offset, res[i].user_id, res[i].status, res[i].n_tokens)
                for i in range(n)]

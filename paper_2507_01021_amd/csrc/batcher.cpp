@@ -33,8 +33,17 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
     std::set<int> free_slots;
     for (int s = 0; s < n_slots; ++s) free_slots.insert(s);
     std::vector<int> seg_of(n_slots, -1), steps_left(n_slots, 0);
+    std::vector<int64_t> first_step(n_slots, 0);  // index of the first step each slot's segment ran in
+    int64_t steps = 0;
     int active = 0;
-    std::vector<int> idx, slots, list;
+    std::vector<int> idx, slots, list, stopped;
+    auto retire = [&](int s) {
+        const int i = seg_of[s];
+        be.retire(s, i, segs[i].max_new_tokens, token_buf + offsets[i]);
+        seg_of[s] = -1;
+        free_slots.insert(s);
+        --active;
+    };
     for (;;) {
         admit();
         const int nfree = n_slots - active;
@@ -51,6 +60,7 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
                     slots.push_back(s);
                     seg_of[s] = i;
                     steps_left[s] = segs[i].n_prompt + segs[i].max_new_tokens - 1;
+                    first_step[s] = steps;
                 }
                 be.encode(idx.data(), (int)idx.size(), slots.data());
                 active += (int)idx.size();
@@ -65,15 +75,14 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
         for (int s = 0; s < n_slots; ++s)
             if (seg_of[s] >= 0) list.push_back(s);
         be.step(list.data(), (int)list.size());
-        for (int s : list) {
-            if (--steps_left[s] == 0) {
-                const int i = seg_of[s];
-                be.retire(s, i, segs[i].max_new_tokens, token_buf + offsets[i]);
-                seg_of[s] = -1;
-                free_slots.insert(s);
-                --active;
-            }
-        }
+        for (int s : list)
+            if (--steps_left[s] == 0) retire(s);
+        int64_t as_of = -1;
+        stopped.clear();
+        if (be.stops(stopped, as_of))
+            for (int s : stopped)  // only the segment that was in the slot at step as_of
+                if (seg_of[s] >= 0 && first_step[s] <= as_of) retire(s);
+        ++steps;
     }
     be.finish();
 }

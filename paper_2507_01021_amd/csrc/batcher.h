@@ -16,6 +16,12 @@
 // backend's clock has reached its arrival_us; with nothing to run, the
 // batcher waits for the next arrival. Without it every segment is queued at
 // the start (arrival_us is then only the priority key).
+//
+// End-of-text stop (optional): the backend may report slots whose segment
+// has produced its end-of-text token as of some earlier step; such a slot
+// retires at once (its tokens up to end of text are the result), freeing it
+// for the queue. A slot may run a step or two past its end of text before
+// this is known; those tokens are never delivered.
 #pragma once
 
 #include <stdint.h>
@@ -47,6 +53,10 @@ class BatchBackend {
     // already submitted has completed), and waiting until that clock reaches t.
     virtual int64_t now_us() { return 0; }
     virtual void wait_until(int64_t) {}
+    // End-of-text stop only, called after every step: slots known to have
+    // reached end of text as of step `as_of` (steps count from 0); false if
+    // nothing is known yet.
+    virtual bool stops(std::vector<int>& slots, int64_t& as_of) { return false; }
 };
 
 // Runs the whole queue; offsets[i] is segment i's first token in token_buf.

@@ -32,6 +32,7 @@ struct whisper_ctx {
     std::string err;
     std::vector<SlotState> slots;
     whisper_stats stats{};
+    int eot = -1;  // end-of-text token of whisper_batch_transcribe / _serve, -1: none
     bool broken = false;
 };
 
@@ -111,6 +112,9 @@ struct EngineBackend : wmi::BatchBackend {
     std::vector<int> steps;    // decode steps taken by each slot's current segment
     std::vector<int> mark_of;  // completion mark of each retired segment
     int step_mark = -1;        // mark after the latest step, once a segment retired with it
+    bool eot_stop = false;     // retire segments at their end-of-text token
+    std::vector<int32_t> stop_of;  // each retired segment's end-of-text position (-1: none)
+    int64_t n_steps = 0;
     double engine_ms = 0.0;
     struct Timer {
         double& acc;
@@ -133,6 +137,8 @@ struct EngineBackend : wmi::BatchBackend {
     void step(const int* slots, int n) override {
         Timer t{engine_ms};
         c->eng->decode_step(slots, n, nullptr, nullptr, nullptr, realtime);
+        if (eot_stop) c->eng->stop_snapshot();
+        ++n_steps;
         step_mark = -1;
         c->stats.decode_steps += 1;
         c->stats.rows_decoded += n;
@@ -143,6 +149,17 @@ struct EngineBackend : wmi::BatchBackend {
         if (step_mark < 0) step_mark = c->eng->mark();
         mark_of[idx] = step_mark;
         c->eng->read_tokens_async(slot, count, dst);
+        if (eot_stop) c->eng->read_stop_async(slot, &stop_of[idx]);
+    }
+    bool stops(std::vector<int>& out, int64_t& as_of) override {
+        if (!eot_stop) return false;
+        Timer t{engine_ms};
+        const int* p = c->eng->stop_poll();
+        if (!p) return false;
+        for (int s = 0; s < c->p.max_slots; ++s)
+            if (p[s] >= 0) out.push_back(s);
+        as_of = n_steps - 2;
+        return true;
     }
     void finish() override {
         Timer t{engine_ms};
@@ -162,19 +179,43 @@ struct FakeBackend : wmi::BatchBackend {
     const int64_t* seg_ids;
     std::vector<int32_t>* events;
     std::vector<int64_t>* finish_at;
+    std::vector<int32_t>* stop_of;
     int64_t clock_us = 0, encode_us = 0, step_us = 0;
+    int eot = -1;
+    // per slot: segment, tokens generated, end-of-text position; snapshots after each step
+    std::vector<int> seg, gen, stop_at;
+    std::vector<std::vector<int>> snaps;
+    static int32_t token(int64_t seg_id, int j) { return (int32_t)((uint64_t)(seg_id * 7919 + (int64_t)j * 104729) % 50000); }
     void encode(const int* idx, int n, const int* slots) override {
-        for (int k = 0; k < n; ++k) events->insert(events->end(), {0, slots[k], idx[k]});
+        for (int k = 0; k < n; ++k) {
+            events->insert(events->end(), {0, slots[k], idx[k]});
+            seg[slots[k]] = idx[k];
+            gen[slots[k]] = 0;
+            stop_at[slots[k]] = -1;
+        }
         clock_us += encode_us * n;
     }
-    void step(const int*, int n) override {
+    void step(const int* slots, int n) override {
         events->insert(events->end(), {1, n, 0});
         clock_us += step_us;
+        for (int k = 0; k < n; ++k) {
+            const int s = slots[k], g = gen[s]++;
+            if (eot >= 0 && stop_at[s] < 0 && token(seg_ids[seg[s]], g) == eot) stop_at[s] = g;
+        }
+        snaps.push_back(stop_at);
     }
-    void retire(int, int idx, int count, int32_t* dst) override {
-        for (int j = 0; j < count; ++j)
-            dst[j] = (int32_t)((uint64_t)(seg_ids[idx] * 7919 + (int64_t)j * 104729) % 50000);
+    void retire(int slot, int idx, int count, int32_t* dst) override {
+        for (int j = 0; j < count; ++j) dst[j] = token(seg_ids[idx], j);
         (*finish_at)[idx] = clock_us;
+        (*stop_of)[idx] = stop_at[slot];
+    }
+    bool stops(std::vector<int>& out, int64_t& as_of) override {
+        if (eot < 0 || snaps.size() < 2) return false;
+        const std::vector<int>& p = snaps[snaps.size() - 2];
+        for (size_t s = 0; s < p.size(); ++s)
+            if (p[s] >= 0) out.push_back((int)s);
+        as_of = (int64_t)snaps.size() - 2;
+        return true;
     }
     void finish() override {}
     int64_t now_us() override { return clock_us; }
@@ -326,6 +367,48 @@ whisper_status whisper_slot_tokens(whisper_ctx* ctx, int32_t slot, int32_t* dst,
     });
 }
 
+// End-of-text results: a segment that produced its end-of-text token keeps
+// the tokens before it (n_tokens); the rest of its token_buf range is -1.
+static void finish_stops(const std::vector<int32_t>& stop_of, whisper_result* results, int32_t* token_buf, int n) {
+    for (int i = 0; i < n; ++i) {
+        const int32_t k = stop_of[i];
+        if (k < 0 || k >= results[i].n_tokens) continue;
+        for (int32_t j = k; j < results[i].n_tokens; ++j) token_buf[results[i].token_offset + j] = -1;
+        results[i].n_tokens = k;
+    }
+}
+
+whisper_status whisper_set_decoding(whisper_ctx* ctx, int32_t eot, const int32_t* suppress, int32_t n_suppress,
+                                    const int32_t* suppress_first, int32_t n_first) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    const int V = ctx->p.n_vocab;
+    if (eot < -1 || eot >= V) return fail(ctx, WHISPER_E_INVAL, "eot must be -1 or a token id");
+    if (n_suppress < 0 || n_first < 0 || (n_suppress > 0 && !suppress) || (n_first > 0 && !suppress_first))
+        return fail(ctx, WHISPER_E_INVAL, "bad suppress list");
+    std::set<int> never, first;
+    for (int i = 0; i < n_suppress; ++i) {
+        if (suppress[i] < 0 || suppress[i] >= V) return fail(ctx, WHISPER_E_INVAL, "suppressed id out of range");
+        never.insert(suppress[i]);
+    }
+    for (int i = 0; i < n_first; ++i) {
+        if (suppress_first[i] < 0 || suppress_first[i] >= V)
+            return fail(ctx, WHISPER_E_INVAL, "suppressed id out of range");
+        first.insert(suppress_first[i]);
+    }
+    std::set<int> both = never;
+    both.insert(first.begin(), first.end());
+    if ((int)both.size() >= V) return fail(ctx, WHISPER_E_INVAL, "the filters would suppress every token");
+    for (auto& s : ctx->slots)
+        if (s.active) return fail(ctx, WHISPER_E_STATE, "decoding options change with every slot idle");
+    return guarded(ctx, [&]() -> whisper_status {
+        const std::vector<int> a(never.begin(), never.end()), b(first.begin(), first.end());
+        ctx->eng->set_decoding(eot, a.data(), (int)a.size(), b.data(), (int)b.size());
+        ctx->eot = eot;
+        return WHISPER_OK;
+    });
+}
+
 whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs, int32_t n, int32_t* token_buf,
                                    int64_t token_buf_cap, whisper_result* results, int32_t realtime) {
     if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
@@ -356,9 +439,12 @@ whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs
         be.c = ctx;
         be.segs = segs;
         be.realtime = realtime != 0;
+        be.eot_stop = ctx->eot >= 0;
         be.steps.assign(ctx->p.max_slots, 0);
         be.mark_of.assign(n, -1);
+        be.stop_of.assign(n, -1);
         ctx->eng->mark_reset();
+        ctx->eng->stop_reset();
         be.t0 = EngineBackend::clock::now();
         wmi::run_continuous_batching(q, ctx->p.max_slots, ctx->p.max_encode_batch, ctx->p.refill_min, off, token_buf,
                                      be, be.realtime);
@@ -369,6 +455,7 @@ whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs
         const std::vector<double> t = ctx->eng->mark_times_us();
         for (int i = 0; i < n; ++i)
             if (be.mark_of[i] >= 0) results[i].finish_us = (int64_t)t[be.mark_of[i]];
+        finish_stops(be.stop_of, results, token_buf, n);
         return WHISPER_OK;
     });
     for (auto& s : ctx->slots) s = SlotState();
@@ -426,7 +513,7 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
                                     int32_t encode_batch, int32_t refill_min, int32_t* token_buf,
                                     int64_t token_buf_cap, whisper_result* results, int32_t* events,
                                     int32_t events_cap, int32_t* n_events, int32_t realtime, int64_t encode_us,
-                                    int64_t step_us) {
+                                    int64_t step_us, int32_t eot) {
     if (n < 0 || (n > 0 && (!arrival_us || !user_id || !segment_id || !max_new_tokens || !results)))
         return fail(nullptr, WHISPER_E_INVAL, "bad arguments");
     if (slots < 1 || encode_batch < 1 || refill_min < 1)
@@ -443,12 +530,18 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
         return fail(nullptr, WHISPER_E_BUFFER, "token_buf needs " + std::to_string(total) + " entries");
     std::vector<int32_t> ev;
     std::vector<int64_t> fin(n, 0);
+    std::vector<int32_t> stop_of(n, -1);
     FakeBackend be;
     be.seg_ids = segment_id;
     be.events = &ev;
     be.finish_at = &fin;
+    be.stop_of = &stop_of;
     be.encode_us = encode_us;
     be.step_us = step_us;
+    be.eot = eot < 0 ? -1 : eot;
+    be.seg.assign(slots, -1);
+    be.gen.assign(slots, 0);
+    be.stop_at.assign(slots, -1);
     try {
         wmi::run_continuous_batching(q, slots, encode_batch, refill_min, off, token_buf, be, realtime != 0);
     } catch (const std::exception& e) {
@@ -456,6 +549,7 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
     }
     for (int i = 0; i < n; ++i)
         results[i] = whisper_result{segment_id[i], off[i], fin[i], user_id[i], WHISPER_OK, max_new_tokens[i], 0};
+    finish_stops(stop_of, results, token_buf, n);
     if (n_events) *n_events = (int32_t)(ev.size() / 3);
     if (events) {
         const size_t k = ev.size() < (size_t)events_cap * 3 ? ev.size() : (size_t)events_cap * 3;

@@ -38,6 +38,9 @@ class Engine {
     // Queues a copy of gen[slot][0..count) into host memory owned by the
     // engine; finish_reads() waits and delivers every queued copy to dst.
     virtual void read_tokens_async(int slot, int count, int32_t* dst) = 0;
+    // Queues a copy of the slot's end-of-text position (tokens generated
+    // before its first end-of-text token, -1 if none), delivered like tokens.
+    virtual void read_stop_async(int slot, int32_t* dst) = 0;
     virtual void finish_reads() = 0;
     virtual void sync() = 0;
     virtual void debug_copy(int tensor, int index, void* dst, size_t bytes) = 0;
@@ -48,6 +51,15 @@ class Engine {
     // index, mark_times_us() waits for the stream and returns every mark's
     // time in microseconds since the reset.
     virtual void mark_reset() = 0;
+    // Decoding options for the following steps: end-of-text token (-1: none)
+    // and logit filters (ids never chosen / not chosen first), ids < n_vocab.
+    virtual void set_decoding(int eot, const int* never, int n_never, const int* first, int n_first) = 0;
+    // End-of-text polling: stop_snapshot() queues a copy of every slot's
+    // end-of-text position; stop_poll() returns the snapshot before the
+    // latest (host memory, max_slots entries) or null; stop_reset() forgets them.
+    virtual void stop_snapshot() = 0;
+    virtual const int* stop_poll() = 0;
+    virtual void stop_reset() = 0;
     virtual int mark() = 0;
     virtual std::vector<double> mark_times_us() = 0;
 };

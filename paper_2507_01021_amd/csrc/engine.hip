@@ -240,6 +240,10 @@ class EngineT final : public Engine {
             if (s.host) (void)hipHostFree(s.host);
         }
         if (tokpin_) (void)hipHostFree(tokpin_);
+        for (int b = 0; b < 2; ++b) {
+            if (stop_pin_[b]) (void)hipHostFree(stop_pin_[b]);
+            if (stop_ev_[b]) (void)hipEventDestroy(stop_ev_[b]);
+        }
         for (void* q : allocs_) (void)hipFree(q);
         if (fork_ev_) (void)hipEventDestroy(fork_ev_);
         if (join_ev_) (void)hipEventDestroy(join_ev_);
@@ -370,9 +374,10 @@ class EngineT final : public Engine {
         float* logits = logits_ + (size_t)r0 * V_;
         unsigned long long* best = best_ + r0;
         proj(tok_emb_, V_, dz, n, d, 1, EpiLogits{logits, V_}, s);
-        hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, s, logits, V_, best);
+        const TokenFilter tf{use_never_ ? never_mask_ : nullptr, use_first_ ? first_mask_ : nullptr, list, pos_, npr_};
+        hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, s, logits, V_, best, tf);
         hipLaunchKernelGGL(argmax_step_kernel, dim3((n + 63) / 64), dim3(64), 0, s, best, n, list, pos_, npr_, seq_,
-                           gen_, forced ? forced_ + r0 : nullptr, outtok_ + r0);
+                           gen_, forced ? forced_ + r0 : nullptr, outtok_ + r0, eot_, stop_at_);
     }
 
     void read_tokens(int slot, int count, int32_t* dst) override {
@@ -383,6 +388,13 @@ class EngineT final : public Engine {
     }
 
     void read_tokens_async(int slot, int count, int32_t* dst) override {
+        queue_read(gen_ + (size_t)slot * 448, count, dst);
+    }
+    void read_stop_async(int slot, int32_t* dst) override { queue_read(stop_at_ + slot, 1, dst); }
+
+    // Queues a copy of count ints from device memory into the pinned area,
+    // delivered to dst by finish_reads().
+    void queue_read(const int* src, int count, int32_t* dst) {
         if (count <= 0) return;
         if (tokpin_used_ + count > tokpin_cap_) {
             finish_reads();
@@ -393,8 +405,7 @@ class EngineT final : public Engine {
                 WMI_HIP(hipHostMalloc(reinterpret_cast<void**>(&tokpin_), tokpin_cap_ * sizeof(int)));
             }
         }
-        WMI_HIP(hipMemcpyAsync(tokpin_ + tokpin_used_, gen_ + (size_t)slot * 448, count * sizeof(int),
-                               hipMemcpyDeviceToHost, st_));
+        WMI_HIP(hipMemcpyAsync(tokpin_ + tokpin_used_, src, count * sizeof(int), hipMemcpyDeviceToHost, st_));
         pending_.push_back({tokpin_used_, count, dst});
         tokpin_used_ += count;
     }
@@ -405,6 +416,46 @@ class EngineT final : public Engine {
         pending_.clear();
         tokpin_used_ = 0;
     }
+
+    // -------------------------------------------------------------- decoding options
+    void set_decoding(int eot, const int* never, int n_never, const int* first, int n_first) override {
+        WMI_HIP(hipStreamSynchronize(st_));
+        const size_t words = (size_t)V_ / 32 + 1;
+        std::vector<unsigned> a(words, 0u), b(words, 0u);
+        for (int i = 0; i < n_never; ++i) a[never[i] >> 5] |= 1u << (never[i] & 31);
+        for (int i = 0; i < n_first; ++i) b[first[i] >> 5] |= 1u << (first[i] & 31);
+        WMI_HIP(hipMemcpy(never_mask_, a.data(), words * 4, hipMemcpyHostToDevice));
+        WMI_HIP(hipMemcpy(first_mask_, b.data(), words * 4, hipMemcpyHostToDevice));
+        use_never_ = n_never > 0;
+        use_first_ = n_first > 0;
+        eot_ = eot;
+        // the options are launch arguments of the captured steps
+        for (auto& g : step_graphs_)
+            for (auto ge : g.second)
+                if (ge) WMI_HIP(hipGraphExecDestroy(ge));
+        step_graphs_.clear();
+    }
+
+    // Snapshot of every slot's stop_at after the work queued so far; poll
+    // returns the snapshot taken before the latest one (its copy has long
+    // completed when the caller keeps one step ahead), or null.
+    void stop_snapshot() override {
+        const int b = (int)(snapshots_ & 1);
+        if (!stop_pin_[b]) {
+            WMI_HIP(hipHostMalloc(reinterpret_cast<void**>(&stop_pin_[b]), (size_t)S_ * sizeof(int)));
+            WMI_HIP(hipEventCreateWithFlags(&stop_ev_[b], hipEventDisableTiming));
+        }
+        WMI_HIP(hipMemcpyAsync(stop_pin_[b], stop_at_, (size_t)S_ * sizeof(int), hipMemcpyDeviceToHost, st_));
+        WMI_HIP(hipEventRecord(stop_ev_[b], st_));
+        ++snapshots_;
+    }
+    const int* stop_poll() override {
+        if (snapshots_ < 2) return nullptr;
+        const int b = (int)((snapshots_ - 2) & 1);
+        WMI_HIP(hipEventSynchronize(stop_ev_[b]));
+        return stop_pin_[b];
+    }
+    void stop_reset() override { snapshots_ = 0; }
 
     // -------------------------------------------------------------- debug
     void debug_copy(int tensor, int index, void* dst, size_t bytes) override {
@@ -519,7 +570,14 @@ class EngineT final : public Engine {
     T *ypad_, *h1_, *zb_, *qh_, *kh_, *vt_, *ob_, *hb_;
     int last_nb_ = 0;
     // decoder state and workspace
-    int *seq_, *gen_, *pos_, *npr_, *list_, *forced_, *outtok_, *rowlen_;
+    int *seq_, *gen_, *pos_, *npr_, *list_, *forced_, *outtok_, *rowlen_, *stop_at_;
+    // decoding options: logit filter masks, end-of-text token (-1: none)
+    unsigned *never_mask_, *first_mask_;
+    bool use_never_ = false, use_first_ = false;
+    int eot_ = -1;
+    int* stop_pin_[2] = {nullptr, nullptr};
+    hipEvent_t stop_ev_[2] = {nullptr, nullptr};
+    int64_t snapshots_ = 0;
     T *kts_, *vs_, *ktc_, *vc_, *dz_, *dq_, *datt_, *dh_;
     float *dx_, *logits_, *gpart_;
     unsigned long long* best_;
@@ -713,7 +771,8 @@ class EngineT final : public Engine {
         ln(x_, zb_, lnpg_, lnpb_, M);
         gemm(zb_, d, 0, WcK_, d, 0, M, Ld_ * d, d, 1, EpiCrossK<T>{ktc_, slot_of_, d, H_, S_});
         gemm(WcV_, d, 0, zb_, d, 0, Ld_ * d, M, d, 1, EpiCrossV<T>{bcV_, vc_, slot_of_, d, H_, S_});
-        hipLaunchKernelGGL(seat_kernel, dim3(nb), dim3(256), 0, st_, slot_of_, seat_np_, seat_prompts_, seq_, pos_, npr_);
+        hipLaunchKernelGGL(seat_kernel, dim3(nb), dim3(256), 0, st_, slot_of_, seat_np_, seat_prompts_, seq_, pos_, npr_,
+                           stop_at_);
         prof_end(WHISPER_K_ENC_PASS, st_);
     }
 
@@ -867,6 +926,9 @@ class EngineT final : public Engine {
         forced_ = dalloc<int>(S);
         outtok_ = dalloc<int>(S);
         rowlen_ = dalloc<int>(S);
+        stop_at_ = dalloc<int>(S);
+        never_mask_ = dalloc<unsigned>((size_t)V_ / 32 + 1);
+        first_mask_ = dalloc<unsigned>((size_t)V_ / 32 + 1);
         kts_ = dalloc<T>(Ld * S * H * 64 * TS);
         vs_ = dalloc<T>(Ld * S * H * TS * 64);
         ktc_ = dalloc<T>(Ld * S * H * 64 * TC);

@@ -844,26 +844,56 @@ inline void skinny_bf16(const bf16* W, int MA, const bf16* X, int n, int K, int 
 // order of arrival; (2) one thread per row reads best[r], resets it, records
 // the token, feeds it (or the forced token) as the next input once the
 // prompt is consumed, and advances the slot's position.
+// Logit filters (optional): ids whose bit is set in `never` cannot be
+// chosen, ids set in `first` not as a row's first generated token (the row
+// is at its first generated token when its input is the prompt's last).
 constexpr int ARGMAX_CHUNKS = 16;
+
+struct TokenFilter {
+    const unsigned* never;  // [V / 32 + 1] bit mask, or null
+    const unsigned* first;  // [V / 32 + 1] bit mask, or null
+    const int* list;        // row -> slot
+    const int* pos;         // slot -> input position
+    const int* n_prompt;    // slot -> prompt length
+};
 
 __device__ inline unsigned long long amax_key(float v, int i) {
     return ((unsigned long long)f2ord(v) << 32) | (unsigned long long)(0xffffffffu - (unsigned)i);
 }
 
 __global__ __launch_bounds__(256) void argmax_partial_kernel(const float* __restrict__ logits, int V,
-                                                             unsigned long long* __restrict__ best) {
+                                                             unsigned long long* __restrict__ best, TokenFilter f) {
     const int r = blockIdx.y, t = threadIdx.x;
     const int per = (V + ARGMAX_CHUNKS - 1) / ARGMAX_CHUNKS;
     const int lo = blockIdx.x * per, hi = min(V, lo + per);
     const float* lg = logits + (long long)r * V;
+    const unsigned* never = f.never;
+    const unsigned* first = nullptr;
+    if (f.first) {
+        const int s = f.list[r];
+        if (f.pos[s] == f.n_prompt[s] - 1) first = f.first;
+    }
     unsigned long long k = 0;
     for (int i = lo + t; i < hi; i += 256 * 4) {
         float v[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[q] = (i + 256 * q < hi) ? lg[i + 256 * q] : -INFINITY;
+        if (never || first) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int j = i + 256 * q;
+                if (j < hi) {
+                    const unsigned bit = 1u << (j & 31);
+                    if ((never && (never[j >> 5] & bit)) || (first && (first[j >> 5] & bit))) v[q] = -INFINITY;
+                }
+            }
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            if (i + 256 * q < hi) { const unsigned long long c = amax_key(v[q], i + 256 * q); k = c > k ? c : k; }
+            if (i + 256 * q < hi && v[q] != -INFINITY) {
+                const unsigned long long c = amax_key(v[q], i + 256 * q);
+                k = c > k ? c : k;
+            }
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -880,9 +910,12 @@ __global__ __launch_bounds__(256) void argmax_partial_kernel(const float* __rest
     }
 }
 
+// eot >= 0: the first time a slot's generated token is eot, stop_at[slot]
+// becomes the number of tokens generated before it.
 __global__ void argmax_step_kernel(unsigned long long* __restrict__ best, int n, const int* __restrict__ list,
                                    int* __restrict__ pos, const int* __restrict__ n_prompt, int* __restrict__ seq,
-                                   int* __restrict__ gen, const int* __restrict__ forced, int* __restrict__ out_tok) {
+                                   int* __restrict__ gen, const int* __restrict__ forced, int* __restrict__ out_tok,
+                                   int eot, int* __restrict__ stop_at) {
     const int r = blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= n) return;
     const unsigned long long k = best[r];
@@ -890,7 +923,9 @@ __global__ void argmax_step_kernel(unsigned long long* __restrict__ best, int n,
     const int tok = (int)(0xffffffffu - (unsigned)(k & 0xffffffffull));
     const int s = list[r], p = pos[s], np = n_prompt[s];
     if (p >= np - 1) {
-        gen[s * 448 + (p - (np - 1))] = tok;
+        const int g = p - (np - 1);
+        if (eot >= 0 && tok == eot && stop_at[s] < 0) stop_at[s] = g;
+        gen[s * 448 + g] = tok;
         seq[s * 448 + p + 1] = forced ? forced[r] : tok;
         out_tok[r] = tok;
     } else {
@@ -899,13 +934,14 @@ __global__ void argmax_step_kernel(unsigned long long* __restrict__ best, int n,
     pos[s] = p + 1;
 }
 
-// Seat prompts: for entry e, slot slots[e] gets tokens prompts[e * 448 ...].
+// Seat prompts: for entry e, slot slots[e] gets tokens prompts[e * 448 ...]
+// (position 0, no end of text seen).
 __global__ void seat_kernel(const int* __restrict__ slots, const int* __restrict__ np_in,
                             const int* __restrict__ prompts, int* __restrict__ seq, int* __restrict__ pos,
-                            int* __restrict__ n_prompt) {
+                            int* __restrict__ n_prompt, int* __restrict__ stop_at) {
     const int e = blockIdx.x, s = slots[e];
     for (int i = threadIdx.x; i < 448; i += blockDim.x) seq[s * 448 + i] = i < np_in[e] ? prompts[e * 448 + i] : 0;
-    if (threadIdx.x == 0) { pos[s] = 0; n_prompt[s] = np_in[e]; }
+    if (threadIdx.x == 0) { pos[s] = 0; n_prompt[s] = np_in[e]; stop_at[s] = -1; }
 }
 
 }  // namespace wmi

@@ -163,3 +163,75 @@ def test_realtime_admission_matches_bruteforce(lib, n, users, slots, eb, R, enc,
     off = np.concatenate([[0], np.cumsum(m)[:-1]])
     for i in range(n):
         assert list(toks[off[i]: off[i] + m[i]]) == fake_tokens(s[i], m[i])
+
+
+def simulate_eot(arrival, user, seg, new, slots, eb, R, eot):
+    """Brute force of end-of-text stop with the fake engine: a slot's stop is
+    known one step after it happened (the snapshot before the latest); a
+    segment's result is its tokens before end of text."""
+    n = len(arrival)
+    queue = sorted(range(n), key=lambda i: (arrival[i], user[i], seg[i], i))
+    free = list(range(slots))
+    seg_of, left, first = [-1] * slots, [0] * slots, [0] * slots
+    gen, stop_at = [0] * slots, [-1] * slots
+    snaps, events, n_tok, steps = [], [], list(new), 0
+
+    def retire(s):
+        i = seg_of[s]
+        if 0 <= stop_at[s] < new[i]:
+            n_tok[i] = stop_at[s]
+        seg_of[s] = -1
+        free.append(s)
+
+    while True:
+        active = slots - len(free)
+        if queue and free and (len(free) >= R or active < R):
+            while queue and free:
+                k = 0
+                while queue and free and k < eb:
+                    i = queue.pop(0)
+                    s = min(free)
+                    free.remove(s)
+                    seg_of[s], left[s], first[s], gen[s], stop_at[s] = i, new[i], steps, 0, -1
+                    events.append((0, s, i))
+                    k += 1
+        if slots - len(free) == 0:
+            break
+        lst = [s for s in range(slots) if seg_of[s] >= 0]
+        events.append((1, len(lst), 0))
+        for s in lst:
+            g = gen[s]
+            gen[s] += 1
+            if stop_at[s] < 0 and fake_tokens(seg[seg_of[s]], g + 1)[g] == eot:
+                stop_at[s] = g
+        snaps.append(list(stop_at))
+        for s in lst:
+            left[s] -= 1
+            if left[s] == 0:
+                retire(s)
+        if len(snaps) >= 2:
+            p, as_of = snaps[-2], len(snaps) - 2
+            for s in range(slots):
+                if p[s] >= 0 and seg_of[s] >= 0 and first[s] <= as_of:
+                    retire(s)
+        steps += 1
+    return events, n_tok
+
+
+@pytest.mark.parametrize("n,users,slots,eb,R", [(12, 3, 4, 2, 1), (40, 8, 8, 3, 4), (64, 8, 16, 16, 16)])
+def test_end_of_text_stop_matches_bruteforce(lib, n, users, slots, eb, R):
+    a, u, s, m = workload(n, users, seed=n + 11)
+    long_ones = [i for i in range(n) if m[i] >= 4][:3]
+    for i in long_ones:
+        eot = fake_tokens(s[i], 3)[2]          # segment i stops after 2 tokens
+        toks, res, ev = binding.test_batcher(a, u, s, m, slots, eb, R, eot=eot)
+        want_ev, want_n = simulate_eot(a, u, s, m, slots, eb, R, eot)
+        assert [tuple(e) for e in ev] == want_ev
+        assert [r[4] for r in res] == want_n
+        assert want_n[i] == 2
+        off = np.concatenate([[0], np.cumsum(m)[:-1]])
+        for j in range(n):
+            got = list(toks[off[j]: off[j] + m[j]])
+            assert got[:want_n[j]] == fake_tokens(s[j], want_n[j])
+            assert got[want_n[j]:] == [-1] * (m[j] - want_n[j])
+            assert eot not in got[:want_n[j]]

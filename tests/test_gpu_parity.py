@@ -11,6 +11,7 @@ import sys
 import numpy as np
 import pytest
 
+from oracle import model as M
 from paper_2507_01021_amd import binding, synth
 
 from parity import TOL, check_tokens, drain, drive_teacher_forced, oracle_run, rel_row_err
@@ -182,3 +183,46 @@ def test_serve_realtime_admission_tokens_and_times(tiny):
         assert np.array_equal(a["tokens"], b["tokens"])
         assert b["finish_us"] >= s.arrival_us
     assert all(r["finish_us"] > 0 for r in offline)
+
+
+def _filtered_margin_ok(lg, step, suppress, first, tol):
+    """The filtered choice at this position is not a near tie."""
+    o = np.array(lg, np.float64)
+    o[list(suppress)] = -np.inf
+    if step == 0:
+        o[list(first)] = -np.inf
+    top = np.sort(o[np.isfinite(o)])[-2:]
+    return top[1] - top[0] > 2 * tol * np.abs(np.asarray(lg)).max()
+
+
+def test_tiny_end_of_text_and_logit_filters_match_oracle(tiny):
+    """End-of-text stop and the two logit filters in a whole transcribe
+    call: each segment's tokens and count equal the oracle's filtered greedy
+    run (compared up to the first near tie)."""
+    shape, W, segs, ref, ctx = tiny
+    suppress = {int(ref[0]["tokens"][0])}            # the first segment's unfiltered first choice
+    first = {int(ref[1]["tokens"][0])}               # and the second's, as a first token only
+    runs = [M.greedy(W, shape, r["ckv"], s.prompt, s.max_new_tokens, suppress=suppress, suppress_begin=first)
+            for s, r in zip(segs, ref)]
+    t1 = runs[1][0]
+    k = next((i for i in range(1, len(t1)) if t1[i] not in t1[:i]), len(t1) - 1)
+    eot = int(t1[k])                                 # the second segment ends after k tokens
+    want = [M.greedy(W, shape, r["ckv"], s.prompt, s.max_new_tokens, eot=eot, suppress=suppress,
+                     suppress_begin=first) for s, r in zip(segs, ref)]
+    ctx.set_decoding(eot=eot, suppress=sorted(suppress), suppress_first=sorted(first))
+    try:
+        res = ctx.transcribe(segs)
+    finally:
+        ctx.set_decoding()
+    for (wt, wl), r, s in zip(want, res, segs):
+        log(f"oracle {wt.tolist()} gpu {r['tokens'].tolist()}")
+        upto = 0
+        while upto < len(wl) and _filtered_margin_ok(wl[upto], upto, suppress, first, TOL["f32"]):
+            upto += 1
+        if upto == len(wl):                           # no near tie anywhere: everything must agree
+            assert r["tokens"].size == wt.size
+        n = min(upto, wt.size)
+        assert np.array_equal(r["tokens"][:n], wt[:n])
+        assert not np.isin(r["tokens"], list(suppress)).any()
+        if r["tokens"].size:
+            assert int(r["tokens"][0]) not in first
