@@ -74,6 +74,17 @@ enum { WHISPER_DTYPE_F32 = 0, WHISPER_DTYPE_BF16 = 1 };
  *                     when at least this many slots are free or fewer than
  *                     this many are active (0 selects 16); results never
  *                     depend on it
+ *   batch_policy      0: continuous batching, queue in arrival order;
+ *                     1: dynamic: queue ordered by arrival_us + step_cost_us x
+ *                     decode steps (shorter segments first, with aging), and
+ *                     refills formed for encoder efficiency: free slots are
+ *                     refilled once they can take min(queued, refill_min)
+ *                     segments and either refill_min are queued, every
+ *                     segment has arrived, or the oldest queued one has
+ *                     waited max_wait_ms; and whenever fewer than refill_min
+ *                     slots are active; results never depend on it
+ *   step_cost_us      dynamic policy: estimated decode step time (0 selects 2000)
+ *   max_wait_ms       dynamic policy: longest wait for a fuller refill
  */
 typedef struct {
     int32_t n_mels, n_audio_ctx, n_audio_state, n_audio_head, n_audio_layer;
@@ -83,7 +94,10 @@ typedef struct {
     int32_t max_encode_batch;
     int32_t pad_mode;
     int32_t refill_min;
-    int32_t reserved[5];
+    int32_t batch_policy;
+    int32_t step_cost_us;
+    int32_t max_wait_ms;
+    int32_t reserved[2];
 } whisper_params;
 
 /*
@@ -330,6 +344,8 @@ whisper_status whisper_stats_read(whisper_ctx* ctx, whisper_stats* out, int32_t 
  * step, and jumps to the next arrival when idle; finish_us is that clock
  * after the segment's last step. eot >= 0 stops a segment at its first fake
  * token equal to eot (polled one step late, as the engine's backend does).
+ * batch_policy, step_cost_us and max_wait_us select the queue policy as the
+ * context fields of those names do (max_wait in microseconds here).
  */
 whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const int32_t* user_id,
                                     const int64_t* segment_id, const int32_t* max_new_tokens,
@@ -337,7 +353,8 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
                                     int32_t* token_buf, int64_t token_buf_cap,
                                     whisper_result* results, int32_t* events,
                                     int32_t events_cap, int32_t* n_events, int32_t realtime,
-                                    int64_t encode_us, int64_t step_us, int32_t eot);
+                                    int64_t encode_us, int64_t step_us, int32_t eot,
+                                    int32_t batch_policy, int64_t step_cost_us, int64_t max_wait_us);
 
 #ifdef __cplusplus
 }

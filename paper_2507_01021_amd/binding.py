@@ -31,8 +31,8 @@ class whisper_params(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "n_mels", "n_audio_ctx", "n_audio_state", "n_audio_head", "n_audio_layer",
         "n_vocab", "n_text_ctx", "n_text_state", "n_text_head", "n_text_layer",
-        "dtype", "max_slots", "max_encode_batch", "pad_mode", "refill_min")] + [
-        ("reserved", C.c_int32 * 5)]
+        "dtype", "max_slots", "max_encode_batch", "pad_mode", "refill_min", "batch_policy",
+        "step_cost_us", "max_wait_ms")] + [("reserved", C.c_int32 * 2)]
 
 
 class whisper_segment(C.Structure):
@@ -86,7 +86,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "whisper_stats_read": (i32, [vp, C.POINTER(whisper_stats), i32]),
         "whisper_set_decoding": (i32, [vp, i32, pi32, i32, pi32, i32]),
         "whisper_test_batcher": (i32, [i32, C.POINTER(i64), pi32, C.POINTER(i64), pi32, i32, i32, i32,
-                                      pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32, i32, i64, i64, i32]),
+                                      pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32, i32, i64, i64, i32,
+                                      i32, i64, i64]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -149,11 +150,13 @@ class Context:
     """One engine context on a HIP device."""
 
     def __init__(self, blob: np.ndarray, max_slots: int = 32, max_encode_batch: int = 0,
-                 pad_mode: int = 0, refill_min: int = 0, device: int = 0):
+                 pad_mode: int = 0, refill_min: int = 0, device: int = 0, batch_policy: int = 0,
+                 step_cost_us: int = 0, max_wait_ms: int = 0):
         lib = load()
         p = params_from_blob(blob)
         p.max_slots, p.max_encode_batch, p.pad_mode, p.refill_min = (
             max_slots, max_encode_batch, pad_mode, refill_min)
+        p.batch_policy, p.step_cost_us, p.max_wait_ms = batch_policy, step_cost_us, max_wait_ms
         self.params = p
         h = C.c_void_p()
         _check(lib.whisper_ctx_create(C.byref(p), blob.ctypes.data, blob.nbytes, device, C.byref(h)))
@@ -250,7 +253,8 @@ class Context:
 
 
 def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_batch, refill_min,
-                 events_cap=100000, realtime=False, encode_us=0, step_us=0, eot=-1):
+                 events_cap=100000, realtime=False, encode_us=0, step_us=0, eot=-1, policy=0,
+                 step_cost_us=2000, max_wait_us=0):
     """Runs the library's scheduler on the host with its fake engine (and,
     with realtime, real-time admission on the fake engine's simulated clock)."""
     lib = load()
@@ -267,7 +271,8 @@ def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_
     st = lib.whisper_test_batcher(n, _ptr(a, C.c_int64), _ptr(u, C.c_int32), _ptr(s, C.c_int64),
                                   _ptr(m, C.c_int32), slots, encode_batch, refill_min,
                                   _ptr(buf, C.c_int32), buf.size, res, _ptr(ev, C.c_int32),
-                                  events_cap, C.byref(ne), 1 if realtime else 0, encode_us, step_us, eot)
+                                  events_cap, C.byref(ne), 1 if realtime else 0, encode_us, step_us, eot,
+                                  policy, step_cost_us, max_wait_us)
     _check(st)
     results = [(res[i].segment_id, res[i].token_offset, res[i].user_id, res[i].status, res[i].n_tokens)
                for i in range(n)]

@@ -1,5 +1,7 @@
 #include "batcher.h"
 
+#include <stdint.h>
+
 #include <algorithm>
 #include <deque>
 #include <set>
@@ -10,7 +12,7 @@ namespace wmi {
 
 void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots, int encode_batch, int refill_min,
                              const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be,
-                             bool realtime) {
+                             bool realtime, const BatchPolicy& policy) {
     if (n_slots < 1 || encode_batch < 1 || refill_min < 1) throw std::invalid_argument("batcher: bad parameters");
     const int n = (int)segs.size();
     std::vector<int> order(n);
@@ -19,17 +21,30 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
         return std::make_tuple(segs[a].arrival_us, segs[a].user_id, segs[a].segment_id, a) <
                std::make_tuple(segs[b].arrival_us, segs[b].user_id, segs[b].segment_id, b);
     });
-    // Not yet arrived (real-time admission) in priority order, which starts
-    // with arrival time: admitting a prefix keeps the queue in priority order.
+    // Not yet arrived (real-time admission), in arrival order.
     std::deque<int> pending(order.begin(), order.end());
-    std::deque<int> queue;
+    // Queued, in serving order: (key, user, segment id, input index).
+    auto key_of = [&](int i) {
+        int64_t k = segs[i].arrival_us;
+        if (policy.dynamic)
+            k += policy.step_cost_us * (int64_t)(segs[i].n_prompt + segs[i].max_new_tokens - 1);
+        return std::make_tuple(k, segs[i].user_id, segs[i].segment_id, i);
+    };
+    std::set<std::tuple<int64_t, int32_t, int64_t, int>> queue;
+    int64_t now = 0;
+    auto oldest_wait = [&]() {  // the longest wait among queued segments
+        int64_t first = INT64_MAX;
+        for (const auto& e : queue) first = std::min(first, segs[std::get<3>(e)].arrival_us);
+        return now - first;
+    };
     auto admit = [&]() {
-        const int64_t now = realtime ? be.now_us() : 0;
+        now = realtime ? be.now_us() : 0;
         while (!pending.empty() && (!realtime || segs[pending.front()].arrival_us <= now)) {
-            queue.push_back(pending.front());
+            queue.insert(key_of(pending.front()));
             pending.pop_front();
         }
     };
+
     std::set<int> free_slots;
     for (int s = 0; s < n_slots; ++s) free_slots.insert(s);
     std::vector<int> seg_of(n_slots, -1), steps_left(n_slots, 0);
@@ -47,13 +62,24 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
     for (;;) {
         admit();
         const int nfree = n_slots - active;
-        if (!queue.empty() && nfree > 0 && (nfree >= refill_min || active < refill_min)) {
+        bool go = !queue.empty() && nfree > 0;
+        if (go && policy.dynamic) {
+            // A pass of min(queued, refill_min) segments; while fewer than
+            // refill_min are queued, wait (bounded) for more to arrive.
+            const int q = (int)queue.size();
+            go = active < refill_min ||
+                 (nfree >= std::min(q, refill_min) &&
+                  (q >= refill_min || pending.empty() || oldest_wait() >= policy.max_wait_us));
+        } else if (go) {
+            go = nfree >= refill_min || active < refill_min;
+        }
+        if (go) {
             while (!queue.empty() && !free_slots.empty()) {
                 idx.clear();
                 slots.clear();
                 while (!queue.empty() && !free_slots.empty() && (int)idx.size() < encode_batch) {
-                    const int i = queue.front();
-                    queue.pop_front();
+                    const int i = std::get<3>(*queue.begin());
+                    queue.erase(queue.begin());
                     const int s = *free_slots.begin();
                     free_slots.erase(free_slots.begin());
                     idx.push_back(i);

@@ -17,6 +17,18 @@
 // batcher waits for the next arrival. Without it every segment is queued at
 // the start (arrival_us is then only the priority key).
 //
+// Dynamic policy (optional, Section 2.2's dynamic batching by segment length
+// and wait time): the queue is ordered by arrival_us + step_cost_us x the
+// segment's decode steps (n_prompt + max_new_tokens - 1), so a shorter
+// segment goes ahead of longer ones that arrived less than the difference in
+// their service times earlier (shortest-first with aging); and refills are
+// formed for encoder efficiency (an encoder pass costs a large fixed part
+// plus a part per segment): free slots are refilled once they can take
+// min(queued, refill_min) segments and either refill_min are queued, no
+// segment is still to arrive, or the oldest queued one has waited
+// max_wait_us; and, as in continuous batching, whenever fewer than
+// refill_min slots are active.
+//
 // End-of-text stop (optional): the backend may report slots whose segment
 // has produced its end-of-text token as of some earlier step; such a slot
 // retires at once (its tokens up to end of text are the result), freeing it
@@ -59,9 +71,15 @@ class BatchBackend {
     virtual bool stops(std::vector<int>& slots, int64_t& as_of) { return false; }
 };
 
+struct BatchPolicy {
+    bool dynamic = false;
+    int64_t step_cost_us = 2000;  // dynamic: estimated microseconds per decode step
+    int64_t max_wait_us = 0;      // dynamic + real time: longest wait for a fuller refill
+};
+
 // Runs the whole queue; offsets[i] is segment i's first token in token_buf.
 void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots, int encode_batch, int refill_min,
                              const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be,
-                             bool realtime = false);
+                             bool realtime = false, const BatchPolicy& policy = BatchPolicy());
 
 }  // namespace wmi

@@ -96,6 +96,8 @@ std::string check_params(const whisper_params& p, const whisper_params& blob) {
     if (p.max_encode_batch < 0 || p.max_encode_batch > p.max_slots) return "max_encode_batch must be in 0..max_slots";
     if (p.pad_mode != 0 && p.pad_mode != 1) return "pad_mode must be 0 or 1";
     if (p.refill_min < 0) return "refill_min must be >= 0";
+    if (p.batch_policy < 0 || p.batch_policy > 1) return "batch_policy must be 0 or 1";
+    if (p.step_cost_us < 0 || p.max_wait_ms < 0) return "step_cost_us and max_wait_ms must be >= 0";
     return "";
 }
 
@@ -257,6 +259,7 @@ whisper_status whisper_ctx_create(const whisper_params* params, const void* weig
     whisper_params p = *params;
     if (p.max_encode_batch == 0) p.max_encode_batch = p.max_slots < 32 ? p.max_slots : 32;
     if (p.refill_min == 0) p.refill_min = 16;
+    if (p.step_cost_us == 0) p.step_cost_us = 2000;
     std::unique_ptr<whisper_ctx> c(new (std::nothrow) whisper_ctx());
     if (!c) return fail(nullptr, WHISPER_E_NOMEM, "host allocation failed");
     c->p = p;
@@ -446,8 +449,12 @@ whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs
         ctx->eng->mark_reset();
         ctx->eng->stop_reset();
         be.t0 = EngineBackend::clock::now();
+        wmi::BatchPolicy pol;
+        pol.dynamic = ctx->p.batch_policy == 1;
+        pol.step_cost_us = ctx->p.step_cost_us;
+        pol.max_wait_us = 1000LL * ctx->p.max_wait_ms;
         wmi::run_continuous_batching(q, ctx->p.max_slots, ctx->p.max_encode_batch, ctx->p.refill_min, off, token_buf,
-                                     be, be.realtime);
+                                     be, be.realtime, pol);
         const double total_ms =
             std::chrono::duration<double, std::milli>(EngineBackend::clock::now() - be.t0).count();
         ctx->stats.engine_host_ms += be.engine_ms;
@@ -513,12 +520,15 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
                                     int32_t encode_batch, int32_t refill_min, int32_t* token_buf,
                                     int64_t token_buf_cap, whisper_result* results, int32_t* events,
                                     int32_t events_cap, int32_t* n_events, int32_t realtime, int64_t encode_us,
-                                    int64_t step_us, int32_t eot) {
+                                    int64_t step_us, int32_t eot, int32_t batch_policy, int64_t step_cost_us,
+                                    int64_t max_wait_us) {
     if (n < 0 || (n > 0 && (!arrival_us || !user_id || !segment_id || !max_new_tokens || !results)))
         return fail(nullptr, WHISPER_E_INVAL, "bad arguments");
     if (slots < 1 || encode_batch < 1 || refill_min < 1)
         return fail(nullptr, WHISPER_E_INVAL, "slots, encode_batch and refill_min must be >= 1");
     if (encode_us < 0 || step_us < 0) return fail(nullptr, WHISPER_E_INVAL, "clock steps must be >= 0");
+    if (batch_policy < 0 || batch_policy > 1 || step_cost_us < 0 || max_wait_us < 0)
+        return fail(nullptr, WHISPER_E_INVAL, "bad batch policy");
     std::vector<wmi::QueuedSegment> q(n);
     for (int i = 0; i < n; ++i) {
         if (max_new_tokens[i] < 1) return fail(nullptr, WHISPER_E_INVAL, "max_new_tokens must be >= 1");
@@ -543,7 +553,11 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
     be.gen.assign(slots, 0);
     be.stop_at.assign(slots, -1);
     try {
-        wmi::run_continuous_batching(q, slots, encode_batch, refill_min, off, token_buf, be, realtime != 0);
+        wmi::BatchPolicy pol;
+        pol.dynamic = batch_policy == 1;
+        pol.step_cost_us = step_cost_us;
+        pol.max_wait_us = max_wait_us;
+        wmi::run_continuous_batching(q, slots, encode_batch, refill_min, off, token_buf, be, realtime != 0, pol);
     } catch (const std::exception& e) {
         return fail(nullptr, WHISPER_E_INVAL, e.what());
     }

@@ -15,6 +15,16 @@ submission. Reports p90 latency per (concurrency, duration bucket) for both
 ways, and checks that both produce identical tokens for every segment.
 
     python -m paper_2507_01021_amd.replay [--model large-v3] [--rounds 2]
+
+With --policies it instead serves the turbo-u64-q512 queue (64 users,
+Poisson arrivals, 512 segments of 16-224 tokens, 128 slots) in real time,
+its arrival times compressed by several factors to load the GPU from light
+to beyond capacity, once with continuous batching (arrival order, refill
+threshold 16) and with the dynamic policy (shorter segments first with
+aging; refills held back, for at most a wait bound, until 16 segments are
+queued) at two wait bounds, reporting segment latency percentiles, the
+makespan and the engine's pass and step counts, and checking that every
+policy gives identical tokens.
 """
 from __future__ import annotations
 
@@ -78,6 +88,56 @@ def run_multiplexed(ctx, recs, dev):
     return lat, toks
 
 
+def policies(step_cost_us=1500, factors=(8, 16, 32), waits_ms=(50, 150)):
+    import copy
+    import torch
+
+    shape, segs0, slots = synth.workload("turbo-u64-q512")
+    blob = synth.pack_blob(synth.make_weights(shape, 0))
+    ctxs = {"continuous": binding.Context(blob, max_slots=slots, max_encode_batch=32)}
+    for w in waits_ms:
+        ctxs[f"dynamic-wait{w}ms"] = binding.Context(blob, max_slots=slots, max_encode_batch=32, batch_policy=1,
+                                                     step_cost_us=step_cost_us, max_wait_ms=w)
+    del blob
+    dev = [torch.from_numpy(s.audio).to("cuda:0") for s in segs0]
+    ptrs = [t.data_ptr() for t in dev]
+    audio_s = sum(s.seconds for s in segs0)
+    for ctx in ctxs.values():   # warm-up (graph capture per row count)
+        ctx.transcribe(segs0, device_audio=ptrs)
+    rows = []
+    for f in factors:
+        segs = [copy.copy(s) for s in segs0]
+        for s in segs:
+            s.arrival_us = s.arrival_us // f
+        span = max(s.arrival_us for s in segs) / 1e6
+        toks = {}
+        for name, ctx in ctxs.items():
+            for _ in range(2):  # the first pass also captures graphs for row counts not seen before
+                torch.cuda.synchronize()
+                ctx.stats(reset=True)
+                res = ctx.transcribe(segs, device_audio=ptrs, realtime=True)
+            st = ctx.stats()
+            lat = np.array([(r["finish_us"] - s.arrival_us) / 1e6 for s, r in zip(segs, res)])
+            toks[name] = [r["tokens"] for r in res]
+            row = {"arrivals_over_s": round(span, 2), "offered_audio_s_per_s": round(audio_s / span, 1),
+                   "policy": name, "latency_mean_s": round(float(lat.mean()), 3),
+                   "latency_p50_s": round(float(np.percentile(lat, 50)), 3),
+                   "latency_p90_s": round(float(np.percentile(lat, 90)), 3),
+                   "latency_p99_s": round(float(np.percentile(lat, 99)), 3),
+                   "makespan_s": round(max(r["finish_us"] for r in res) / 1e6, 3),
+                   "encode_passes": st["encode_passes"], "decode_steps": st["decode_steps"],
+                   "mean_active": round(st["rows_decoded"] / max(1, st["decode_steps"]), 1)}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+        for name in toks:
+            for a, b in zip(toks["continuous"], toks[name]):
+                if not np.array_equal(a, b):
+                    raise AssertionError(f"{name} produced other tokens than continuous batching")
+    for ctx in ctxs.values():
+        ctx.close()
+    return rows
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--model", default="large-v3", choices=sorted(MODELS))
@@ -85,7 +145,10 @@ def main(argv=None):
     ap.add_argument("--concurrency", default="5,10,20")
     ap.add_argument("--slots", type=int, default=64)
     ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--policies", action="store_true", help="compare the queue policies on turbo-u64-q512")
     a = ap.parse_args(argv)
+    if a.policies:
+        return policies()
     import torch
 
     shape = MODELS[a.model]

@@ -235,3 +235,76 @@ def test_end_of_text_stop_matches_bruteforce(lib, n, users, slots, eb, R):
             assert got[:want_n[j]] == fake_tokens(s[j], want_n[j])
             assert got[want_n[j]:] == [-1] * (m[j] - want_n[j])
             assert eot not in got[:want_n[j]]
+
+
+def simulate_dynamic(arrival, user, seg, new, slots, eb, R, enc_us, step_us, cost_us, wait_us):
+    """Brute force of the dynamic policy with real-time admission on the
+    fake clock: queue ordered by arrival + cost_us x steps (then user,
+    segment, index); refill when fewer than R slots are active, or when
+    min(queued, R) slots are free and R are queued, or all have arrived, or
+    the oldest queued segment has waited wait_us."""
+    n = len(arrival)
+    pending = sorted(range(n), key=lambda i: (arrival[i], user[i], seg[i], i))
+    key = lambda i: (arrival[i] + cost_us * new[i], user[i], seg[i], i)
+    queue, free = [], list(range(slots))
+    seg_of, left = [-1] * slots, [0] * slots
+    events, finish, clock = [], [0] * n, 0
+    while True:
+        while pending and arrival[pending[0]] <= clock:
+            queue.append(pending.pop(0))
+        queue.sort(key=key)
+        active = slots - len(free)
+        waited = queue and clock - min(arrival[i] for i in queue) >= wait_us
+        arrived_all = all(arrival[i] <= clock for i in range(len(arrival)))
+        if queue and free and (active < R or (len(free) >= min(R, len(queue)) and
+                                              (len(queue) >= R or arrived_all or waited))):
+            while queue and free:
+                k = 0
+                while queue and free and k < eb:
+                    i = queue.pop(0)
+                    s = min(free)
+                    free.remove(s)
+                    seg_of[s], left[s] = i, new[i]
+                    events.append((0, s, i))
+                    k += 1
+                clock += enc_us * k
+        if slots - len(free) == 0:
+            if not pending:
+                break
+            clock = max(clock, arrival[pending[0]])
+            continue
+        lst = [s for s in range(slots) if seg_of[s] >= 0]
+        events.append((1, len(lst), 0))
+        clock += step_us
+        for s in lst:
+            left[s] -= 1
+            if left[s] == 0:
+                finish[seg_of[s]] = clock
+                seg_of[s] = -1
+                free.append(s)
+    return events, finish
+
+
+@pytest.mark.parametrize("n,users,slots,eb,R,cost,wait", [(12, 3, 4, 2, 4, 400_000, 0),
+                                                          (40, 8, 8, 3, 4, 150_000, 300_000),
+                                                          (64, 8, 16, 16, 16, 30_000, 100_000),
+                                                          (64, 8, 40, 16, 8, 30_000, 2_000_000),
+                                                          (30, 5, 6, 7, 6, 1_000_000, 50_000)])
+def test_dynamic_policy_matches_bruteforce(lib, n, users, slots, eb, R, cost, wait):
+    a, u, s, m = workload(n, users, seed=n + 23)
+    toks, res, ev, fin = binding.test_batcher(a, u, s, m, slots, eb, R, realtime=True, encode_us=20_000,
+                                              step_us=150_000, policy=1, step_cost_us=cost, max_wait_us=wait)
+    want_ev, want_fin = simulate_dynamic(a, u, s, m, slots, eb, R, 20_000, 150_000, cost, wait)
+    assert [tuple(e) for e in ev] == want_ev
+    assert fin == want_fin
+    off = np.concatenate([[0], np.cumsum(m)[:-1]])
+    for i in range(n):
+        assert list(toks[off[i]: off[i] + m[i]]) == fake_tokens(s[i], m[i])
+
+
+def test_dynamic_order_prefers_short_segments_with_aging(lib):
+    """Arrivals 0, 1 ms, 2 ms with 9, 1, 5 steps and cost 1 ms per step:
+    keys 9, 2, 7 ms -> served 1, 2, 0 (one slot)."""
+    _, _, ev = binding.test_batcher([0, 1000, 2000], [0, 0, 0], [10, 11, 12], [9, 1, 5], 1, 1, 1,
+                                    policy=1, step_cost_us=1000)
+    assert [e[2] for e in ev if e[0] == 0] == [1, 2, 0]

@@ -185,6 +185,38 @@ def test_serve_realtime_admission_tokens_and_times(tiny):
     assert all(r["finish_us"] > 0 for r in offline)
 
 
+def test_dynamic_policy_same_tokens_as_continuous(tiny):
+    """The dynamic queue policy (shortest-first with aging, refills held back
+    for fuller encoder passes) changes only the schedule: 8 segments on 3
+    slots, arriving 0-140 ms apart, get the continuous batcher's tokens,
+    offline and with real-time admission."""
+    shape, W, segs, ref, ctx = tiny
+    import copy
+    late = []
+    for k in range(8):
+        t = copy.copy(segs[k % 2])
+        t.segment_id = 100 + k
+        t.arrival_us = 20_000 * k
+        t.max_new_tokens = 4 + 3 * (k % 4)
+        late.append(t)
+    cont = binding.Context(synth.pack_blob(W), max_slots=3, refill_min=2)
+    dyn = binding.Context(synth.pack_blob(W), max_slots=3, refill_min=2, batch_policy=1, step_cost_us=500,
+                          max_wait_ms=30)
+    try:
+        log("tiny: continuous vs dynamic policy, 8 segments on 3 slots")
+        want = cont.transcribe(late)
+        for realtime in (False, True):
+            got = dyn.transcribe(late, realtime=realtime)
+            for s, a, b in zip(late, want, got):
+                assert b["segment_id"] == s.segment_id
+                assert np.array_equal(a["tokens"], b["tokens"])
+                if realtime:
+                    assert b["finish_us"] >= s.arrival_us
+    finally:
+        cont.close()
+        dyn.close()
+
+
 def _filtered_margin_ok(lg, step, suppress, first, tol):
     """The filtered choice at this position is not a near tie."""
     o = np.array(lg, np.float64)
