@@ -218,6 +218,7 @@ class EngineT final : public Engine {
         st_ = own_stream_;
         if (const char* g = getenv("WHISPER_STEP_GRAPHS")) graphs_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_STEP_SPLIT")) split_ = g[0] != '0';
+        if (const char* g = getenv("WHISPER_FUSED_LN")) fused_ln_ = g[0] != '0';
         load_weights(blob, bytes);
         alloc_state();
         WMI_HIP(hipDeviceSynchronize());
@@ -359,8 +360,7 @@ class EngineT final : public Engine {
             prof_begin(WHISPER_K_SELF_ATTN, s);
             hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, s, sa);
             prof_end(WHISPER_K_SELF_ATTN, s);
-            proj_resid(L.Wo, datt, n, d, ks1, L.bo, L.ln2g, L.ln2b, pbuf, dx, dz, s);
-            proj(L.Wcq, d, dz, n, d, 1, EpiQ<T>{L.cbq, dq, d}, s);
+            self_out_cross_q(L, n, datt, dq, dx, dz, pbuf, s);
             DecAttnArgs ca{dq, ktc_ + sl * TC, vc_ + sl * TC, datt, list, nullptr, TC, H_, d};
             prof_begin(WHISPER_K_CROSS_ATTN, s);
             hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, s, ca);
@@ -378,6 +378,25 @@ class EngineT final : public Engine {
         hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, s, logits, V_, best, tf);
         hipLaunchKernelGGL(argmax_step_kernel, dim3((n + 63) / 64), dim3(64), 0, s, best, n, list, pos_, npr_, seq_,
                            gen_, forced ? forced_ + r0 : nullptr, outtok_ + r0, eot_, stop_at_);
+    }
+
+    // Self-attention output projection (x += W_o att + b_o) and the
+    // cross-attention queries from LN2(x). bf16 model: the output projection
+    // adds the residual itself (no split-K) and the query projection
+    // normalises its own input rows, one kernel fewer than the split-K
+    // partials + residual/LN kernel + projection of the fp32 model.
+    void self_out_cross_q(const DecLayerW<T>& L, int n, const T* datt, T* dq, float* dx, T* dz, float* pbuf,
+                          hipStream_t s) {
+        const int d = d_;
+        if constexpr (std::is_same<T, bf16>::value) {
+            if (fused_ln_) {
+                skinny_resid(L.Wo, d, datt, n, d, L.bo, dx, s);
+                skinny_ln(L.Wcq, d, dx, n, d, L.ln2g, L.ln2b, EpiQ<T>{L.cbq, dq, d}, s);
+                return;
+            }
+        }
+        proj_resid(L.Wo, datt, n, d, split_k(d), L.bo, L.ln2g, L.ln2b, pbuf, dx, dz, s);
+        proj(L.Wcq, d, dz, n, d, 1, EpiQ<T>{L.cbq, dq, d}, s);
     }
 
     void read_tokens(int slot, int count, int32_t* dst) override {
@@ -582,7 +601,7 @@ class EngineT final : public Engine {
     float *dx_, *logits_, *gpart_;
     unsigned long long* best_;
     std::vector<int> list_host_;
-    bool graphs_ = true, split_ = true;
+    bool graphs_ = true, split_ = true, fused_ln_ = true;
     std::map<int, std::array<hipGraphExec_t, 2>> step_graphs_;  // per row count: first and second half
     hipStream_t st2_ = nullptr;                                 // second half of a split step
     hipEvent_t fork_ev_ = nullptr, join_ev_ = nullptr;

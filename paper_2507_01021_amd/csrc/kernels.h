@@ -682,8 +682,9 @@ __global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {
 // take interleaved 32-wide k-steps, U steps' loads issued before their
 // MFMAs; the wave partial sums are added in LDS in a fixed order, so a row's
 // result never depends on which other rows are present (row tiles past n
-// re-read the last valid tile and are dropped).
-template <int RT, int NT, int U>
+// re-read the last valid tile and are dropped). NW waves per workgroup
+// (4, or more for long reductions), red: (NW - 1) * RT * NT * 4 * 64 floats.
+template <int RT, int NT, int U, int NW = 4>
 __device__ __forceinline__ void skinny_core(const bf16* __restrict__ W, const bf16* __restrict__ X, int nks_tot, int n,
                                             int Kc, float* red, float (&v)[RT][NT][4]) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -701,13 +702,13 @@ __device__ __forceinline__ void skinny_core(const bf16* __restrict__ W, const bf
 #pragma unroll
         for (int u = 0; u < NT; ++u) acc[t][u] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
     const int nks = Kc >> 5;
-    // Batches of U k-steps (s, s + 4, ...): all loads of a batch are issued
+    // Batches of U k-steps (s, s + NW, ...): all loads of a batch are issued
     // before its MFMAs; steps past the end re-read the last step and are skipped.
-    for (int s0 = wave; s0 < nks; s0 += 4 * U) {
+    for (int s0 = wave; s0 < nks; s0 += NW * U) {
         mfma_bf16x8 a[U][RT], b[U][NT];
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            const int off = min(s0 + 4 * q, nks - 1) * 512;
+            const int off = min(s0 + NW * q, nks - 1) * 512;
 #pragma unroll
             for (int t = 0; t < RT; ++t) a[q][t] = *reinterpret_cast<const mfma_bf16x8*>(wp[t] + off);
 #pragma unroll
@@ -715,7 +716,7 @@ __device__ __forceinline__ void skinny_core(const bf16* __restrict__ W, const bf
         }
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            if (s0 + 4 * q < nks) {
+            if (s0 + NW * q < nks) {
 #pragma unroll
                 for (int t = 0; t < RT; ++t)
 #pragma unroll
@@ -742,18 +743,20 @@ __device__ __forceinline__ void skinny_core(const bf16* __restrict__ W, const bf
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int idx = (t * NT + u) * 4 + e;
-                    v[t][u][e] = ((acc[t][u][e] + red[idx * 64 + lane]) + red[(F + idx) * 64 + lane]) +
-                                 red[(2 * F + idx) * 64 + lane];
+                    float sum = acc[t][u][e];
+#pragma unroll
+                    for (int w = 1; w < NW; ++w) sum += red[((w - 1) * F + idx) * 64 + lane];
+                    v[t][u][e] = sum;
                 }
     }
 }
 
 // Plain epilogue variant: wave 0 hands rows i..i+3 of column r to epi (its
 // loads, pre(), are issued before the main loop). z = ks.
-template <int RT, int NT, int U, class Epi>
-__global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict__ W, const bf16* __restrict__ X,
-                                                          int nks_tot, int MA, int n, int Kc, Epi epi) {
-    __shared__ float red[3 * RT * NT * 4 * 64];
+template <int RT, int NT, int U, class Epi, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void skinny_bf16_kernel(const bf16* __restrict__ W, const bf16* __restrict__ X,
+                                                              int nks_tot, int MA, int n, int Kc, Epi epi) {
+    __shared__ float red[(NW - 1) * RT * NT * 4 * 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int fr = lane & 15, fc = lane >> 4;
     const int i0 = blockIdx.x * 16 * RT;
@@ -768,7 +771,7 @@ __global__ __launch_bounds__(256) void skinny_bf16_kernel(const bf16* __restrict
             }
     }
     float v[RT][NT][4];
-    skinny_core<RT, NT, U>(W, X, nks_tot, n, Kc, red, v);
+    skinny_core<RT, NT, U, NW>(W, X, nks_tot, n, Kc, red, v);
     if (wave > 0) return;
 #pragma unroll
     for (int t = 0; t < RT; ++t)
@@ -788,6 +791,166 @@ struct EpiPartial {
         st4(part + ((long long)ks * n + r) * N + i, a, b, c, e);
     }
 };
+
+// Residual update without split-K: x[r][i..i+3] += (sum + bias), where the
+// workgroup owns weight rows i..i+3 for the whole reduction (x row-major,
+// width d; x and the bias are loaded before the main loop).
+struct EpiResidX {
+    const float* bias;
+    float* x;
+    int d;
+    __device__ EpiPre pre(int i, int r, int) const {
+        EpiPre p{};
+        p.a = ld4(bias + i);
+        p.b = ld4(x + (long long)r * d + i);
+        return p;
+    }
+    __device__ void operator()(int i, int r, int, float a, float b, float c, float e, const EpiPre& p) const {
+        st4(x + (long long)r * d + i, p.b.x + (a + p.a.x), p.b.y + (b + p.a.y), p.b.z + (c + p.a.z),
+            p.b.w + (e + p.a.w));
+    }
+};
+
+// Decode projection of layer-normed rows, C[i][r] = sum_k W[i][k] LN(x[r])[k],
+// for 16 activation rows per workgroup: grid (weight-row tiles of 16 * RT,
+// groups of 16 rows). The workgroup normalises its own rows from the fp32
+// residual stream x (row-major, width d = 64 E; fp32 mean, then biased
+// variance about it, eps 1e-5, gain and bias), rounds them to bf16 and keeps
+// them in LDS in the MFMA's B-operand fragment layout. Its weight loads (W
+// fragment-major, one batch covering each wave's k-steps) are issued first,
+// so they overlap the normalisation. The NW waves take interleaved 32-wide
+// k-steps and are summed in LDS in a fixed order: a row's result depends on
+// that row alone. Rows past n are zero and dropped.
+namespace sln {
+constexpr int NW = 8;
+}
+template <int RT, int E, class Epi>
+__global__ __launch_bounds__(64 * sln::NW) void skinny_ln_kernel(const bf16* __restrict__ W,
+                                                                 const float* __restrict__ x,
+                                                                 const float* __restrict__ g,
+                                                                 const float* __restrict__ b, int MA, int n,
+                                                                 Epi epi) {
+    constexpr int NW = sln::NW, d = 64 * E, nks = d / 32, U = (nks + NW - 1) / NW;
+    constexpr int NC = 8 * E, CH = (NC + 63) / 64, RPW = 16 / NW, F = RT * 4;
+    __shared__ __align__(16) bf16 zs[16 * d];
+    __shared__ float red[(NW - 1) * F * 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int fr = lane & 15, fc = lane >> 4;
+    const int i0 = blockIdx.x * 16 * RT, r0 = blockIdx.y * 16;
+    EpiPre pre[RT];
+    if (wave == 0) {
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+            const int i = i0 + t * 16 + fc * 4, r = r0 + fr;
+            if (i < MA && r < n) pre[t] = epi.pre(i, r, 0);
+        }
+    }
+    mfma_bf16x8 a[U][RT];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        const int st = min(wave + NW * q, nks - 1);
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+            a[q][t] = *reinterpret_cast<const mfma_bf16x8*>(
+                W + (((long long)(blockIdx.x * RT + t) * nks + st) * 64 + lane) * 8);
+    }
+    // This wave's rows: lane holds 8-column chunks lane, lane + 64, ...
+    float v[RPW][CH][8], gg[CH][8], bb[CH][8];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const int c8 = lane + 64 * c;
+        const bool ok = c8 < NC;
+        const float4 g0 = ok ? ld4(g + 8 * c8) : float4{}, g1 = ok ? ld4(g + 8 * c8 + 4) : float4{};
+        const float4 b0 = ok ? ld4(b + 8 * c8) : float4{}, b1 = ok ? ld4(b + 8 * c8 + 4) : float4{};
+        gg[c][0] = g0.x; gg[c][1] = g0.y; gg[c][2] = g0.z; gg[c][3] = g0.w;
+        gg[c][4] = g1.x; gg[c][5] = g1.y; gg[c][6] = g1.z; gg[c][7] = g1.w;
+        bb[c][0] = b0.x; bb[c][1] = b0.y; bb[c][2] = b0.z; bb[c][3] = b0.w;
+        bb[c][4] = b1.x; bb[c][5] = b1.y; bb[c][6] = b1.z; bb[c][7] = b1.w;
+    }
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) {
+        const int R = r0 + wave * RPW + rr;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int c8 = lane + 64 * c;
+            const bool ok = R < n && c8 < NC;
+            const float* xp = x + (long long)R * d + 8 * c8;
+            const float4 x0 = ok ? ld4(xp) : float4{}, x1 = ok ? ld4(xp + 4) : float4{};
+            v[rr][c][0] = x0.x; v[rr][c][1] = x0.y; v[rr][c][2] = x0.z; v[rr][c][3] = x0.w;
+            v[rr][c][4] = x1.x; v[rr][c][5] = x1.y; v[rr][c][6] = x1.z; v[rr][c][7] = x1.w;
+        }
+    }
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) {
+        const int row = wave * RPW + rr, R = r0 + row;
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s += v[rr][c][j];
+        const float mean = wave_sum(s) / d;
+        float q = 0.f;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            if (lane + 64 * c < NC) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) { const float e = v[rr][c][j] - mean; q += e * e; }
+            }
+        }
+        const float rstd = rsqrtf(wave_sum(q) / d + 1e-5f);
+        const bool live = R < n;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int c8 = lane + 64 * c;
+            if (c8 < NC) {
+                uint32_t w4[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float z0 = live ? (v[rr][c][2 * j] - mean) * rstd * gg[c][2 * j] + bb[c][2 * j] : 0.f;
+                    const float z1 =
+                        live ? (v[rr][c][2 * j + 1] - mean) * rstd * gg[c][2 * j + 1] + bb[c][2 * j + 1] : 0.f;
+                    w4[j] = pack_bf16x2(z0, z1);
+                }
+                *reinterpret_cast<uint4*>(zs + (((c8 >> 2) * 64 + (c8 & 3) * 16 + row) << 3)) =
+                    uint4{w4[0], w4[1], w4[2], w4[3]};
+            }
+        }
+    }
+    __syncthreads();
+    mfma_f32x4 acc[RT];
+#pragma unroll
+    for (int t = 0; t < RT; ++t) acc[t] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        const int st = wave + NW * q;
+        if (st < nks) {
+            const mfma_bf16x8 bx = *reinterpret_cast<const mfma_bf16x8*>(zs + ((st * 64 + lane) << 3));
+#pragma unroll
+            for (int t = 0; t < RT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q][t], bx, acc[t], 0, 0, 0);
+        }
+    }
+    if (wave > 0) {
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) red[((wave - 1) * F + t * 4 + e) * 64 + lane] = acc[t][e];
+    }
+    __syncthreads();
+    if (wave > 0) return;
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float sum = acc[t][e];
+#pragma unroll
+            for (int w = 1; w < NW; ++w) sum += red[((w - 1) * F + t * 4 + e) * 64 + lane];
+            o[e] = sum;
+        }
+        const int i = i0 + t * 16 + fc * 4, r = r0 + fr;
+        if (i < MA && r < n) epi(i, r, 0, o[0], o[1], o[2], o[3], pre[t]);
+    }
+}
 
 // U = k-steps per wave and batch for nks k-steps over 4 waves: all of a
 // wave's steps in one batch, up to 10 (4 with 8 row tiles, for registers).
@@ -817,6 +980,69 @@ constexpr int skinny_u(int nks, int NT) {
         else if ((n) <= 64) { constexpr int NT = 4; __VA_ARGS__; }     \
         else { constexpr int NT = 8; __VA_ARGS__; }                    \
     } while (0)
+
+// Waves per workgroup of a residual projection (whole reduction in one
+// workgroup): twice the usual, to keep more loads in flight. The same for
+// every row count, since the waves' k-step split fixes the summation order.
+constexpr int RESID_NW = 8;
+// k-steps per wave and batch for nks k-steps over NW waves (fewer with many
+// row tiles, for registers)
+constexpr int resid_u(int nks, int NW, int NT) {
+    return (nks + NW - 1) / NW <= 1 ? 1
+         : ((nks + NW - 1) / NW <= 2 || NT >= 8) ? 2
+         : (nks + NW - 1) / NW <= 3 ? 3
+         : (nks + NW - 1) / NW <= 4 ? 4
+         : (nks + NW - 1) / NW <= 6 ? 6 : 10;
+}
+#define WMI_RESID_U(nks, NW, NT, LAUNCH)                                              \
+    do {                                                                             \
+        const int u_ = resid_u(nks, NW, NT);                                          \
+        if (u_ == 1) { constexpr int U = 1; LAUNCH; }                                 \
+        else if (u_ == 2) { constexpr int U = 2; LAUNCH; }                            \
+        else if (u_ == 3) { constexpr int U = (NT) >= 8 ? 2 : 3; LAUNCH; }             \
+        else if (u_ == 4) { constexpr int U = (NT) >= 8 ? 2 : 4; LAUNCH; }             \
+        else if (u_ == 6) { constexpr int U = (NT) >= 8 ? 2 : 6; LAUNCH; }             \
+        else { constexpr int U = (NT) >= 8 ? 2 : (NT) >= 4 ? 6 : 10; LAUNCH; }        \
+    } while (0)
+
+// x[r] += W X[r] + bias for n rows (W fragment-major [d rounded up to 32][K],
+// X fragment-major [n rounded up to 16][K], x row-major fp32 [n][d]).
+// More than 64 rows go in launches of 64 (a row's result does not depend on
+// the other rows of its launch).
+inline void skinny_resid(const bf16* W, int d, const bf16* X, int n, int K, const float* bias, float* x,
+                         hipStream_t st) {
+    if (K % 32 || n <= 0 || n > 128 || d % 16) throw ArgError(-1, "skinny_resid: unsupported shape");
+    const int nks = K / 32;
+    const dim3 grid(d / 16, 1);
+    for (int r0 = 0; r0 < n; r0 += 64) {
+        const int m = min(64, n - r0);
+        const bf16* Xr = X + (size_t)r0 * K;
+        const EpiResidX epi{bias, x + (size_t)r0 * d, d};
+        auto launch = [&](auto nt) {
+            constexpr int NT = decltype(nt)::value;
+            WMI_RESID_U(nks, RESID_NW, NT,
+                        hipLaunchKernelGGL((skinny_bf16_kernel<1, NT, U, EpiResidX, RESID_NW>), grid,
+                                           dim3(64 * RESID_NW), 0, st, W, Xr, nks, d, m, K, epi));
+        };
+        if (m <= 16) launch(std::integral_constant<int, 1>{});
+        else if (m <= 32) launch(std::integral_constant<int, 2>{});
+        else launch(std::integral_constant<int, 4>{});
+    }
+}
+
+// C = W LN(x) for n rows of the fp32 residual stream x (row-major, width d),
+// with the layer norm's gain g and bias b; W fragment-major [MA][d], MA a
+// multiple of 16. Every workgroup of a row group repeats that group's
+// normalisation, which pays only where MA is small (the cross-attention
+// query projection, MA = d).
+template <class Epi>
+inline void skinny_ln(const bf16* W, int MA, const float* x, int n, int d, const float* g, const float* b,
+                      const Epi& epi, hipStream_t st) {
+    if (n <= 0 || n > 128 || MA <= 0 || MA % 16) throw ArgError(-1, "skinny_ln: unsupported shape");
+    const int groups = (n + 15) / 16;
+    WMI_SWITCH_E(d, hipLaunchKernelGGL((skinny_ln_kernel<1, E, Epi>), dim3(MA / 16, groups), dim3(64 * sln::NW), 0,
+                                       st, W, x, g, b, MA, n, epi));
+}
 
 // W: fragment-major [MA rounded up to 32][K], X: fragment-major [n rounded up
 // to 16][K]; KS workgroups split K.
