@@ -49,6 +49,23 @@ __device__ inline int swz32(int r, int c) { return r * 64 + ((c ^ ((r >> 1) & 3)
 // Byte offset of 16-byte chunk c (0..7) of row r inside a [rows][64] bf16 LDS tile.
 __device__ inline int swz(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
 
+// Tile of workgroup `bid` among tilesA x tilesB tiles, arranged for the L2
+// of each XCD: workgroups are handed to the 8 XCDs in turn (bid mod 8), so
+// XCD x gets a contiguous run of tiles, and runs are ordered in groups of
+// GA A-tiles (A-tile fastest): the ~32 workgroups an XCD holds at a time
+// then cover about 4 A-tiles x 8 B-tiles, and each tile's K-slices are
+// fetched into that XCD's L2 once for several workgroups.
+__device__ inline void xcd_tile(int bid, int tilesA, int tilesB, int& ta, int& tb) {
+    constexpr int GA = 4;
+    const int T = tilesA * tilesB, per = T >> 3, rem = T & 7;
+    const int x = bid & 7, j = bid >> 3;
+    const int v = x * per + min(x, rem) + j;
+    const int g = v / (GA * tilesB), ga = min(GA, tilesA - g * GA);
+    const int w = v - g * GA * tilesB;
+    tb = w / ga;
+    ta = g * GA + (w - tb * ga);
+}
+
 // C = A B^T for A [MA][K], B [MB][K] (bf16, row-major, batched over z):
 // a 256 x 256 workgroup tile, 8 waves (2 per SIMD) of 128 x 64 each on
 // 16x16x32 MFMAs, so one wave's MFMAs run while the other waits on its LDS
@@ -62,9 +79,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_kernel(
     const int z = blockIdx.z;
     A += (long long)z * sA;
     B += (long long)z * sB;
-    // Workgroups sharing a B tile (activations) run next to each other.
-    const int ta = blockIdx.x % tilesA;
-    const int tb = blockIdx.x / tilesA;
+    int ta, tb;
+    xcd_tile(blockIdx.x, tilesA, (int)(gridDim.x / tilesA), ta, tb);
     const int a0 = ta * gb::BM, b0 = tb * gb::BN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wa = (wave & 1) * 128, wb = (wave >> 1) * 64;
