@@ -301,6 +301,18 @@ enum {
 /* Starts (enable = 1) or stops (0) timing of `kernel`, clearing its totals. */
 whisper_status whisper_profile_enable(whisper_ctx* ctx, int32_t kernel, int32_t enable);
 
+/* Average duration in microseconds of `reps` back-to-back launches of one
+ * kernel over rows 0..n_rows-1 mapped to slots 0..n_rows-1, timed by two
+ * events on the context's stream (synchronises it). Only
+ * WHISPER_K_CROSS_ATTN (the decode cross-attention of Section 2.3's batched
+ * decoder: each launch reads the cached encoder keys and values of n_rows
+ * slots x all heads, layer i mod the decoder depth for launch i). The slots'
+ * caches are read as they are (encode them first for meaningful data) and
+ * the step's attention output buffer is overwritten; call it between decode
+ * steps, not during a transcribe call. Errors: WHISPER_E_INVAL for another
+ * kernel, n_rows outside 1..max_slots, reps < 1 or avg_us NULL. */
+whisper_status whisper_time_kernel(whisper_ctx* ctx, int32_t kernel, int32_t n_rows, int32_t reps, double* avg_us);
+
 /* Total milliseconds and launch count of `kernel` since it was enabled
  * (synchronises the stream). */
 whisper_status whisper_profile_read(whisper_ctx* ctx, int32_t kernel, double* total_ms,

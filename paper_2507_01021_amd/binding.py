@@ -22,8 +22,8 @@ EXPORTS = (
     "whisper_params_from_blob", "whisper_ctx_create", "whisper_ctx_destroy", "whisper_last_error",
     "whisper_ctx_set_stream", "whisper_batch_encode", "whisper_batch_decode_step",
     "whisper_slot_tokens", "whisper_batch_transcribe", "whisper_batch_serve", "whisper_debug_copy",
-    "whisper_profile_enable", "whisper_profile_read", "whisper_stats_read", "whisper_set_decoding",
-    "whisper_test_batcher",
+    "whisper_profile_enable", "whisper_profile_read", "whisper_time_kernel", "whisper_stats_read",
+    "whisper_set_decoding", "whisper_test_batcher",
 )
 
 
@@ -83,6 +83,7 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "whisper_debug_copy": (i32, [vp, i32, i32, vp, C.c_size_t]),
         "whisper_profile_enable": (i32, [vp, i32, i32]),
         "whisper_profile_read": (i32, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64)]),
+        "whisper_time_kernel": (i32, [vp, i32, i32, i32, C.POINTER(C.c_double)]),
         "whisper_stats_read": (i32, [vp, C.POINTER(whisper_stats), i32]),
         "whisper_set_decoding": (i32, [vp, i32, pi32, i32, pi32, i32]),
         "whisper_test_batcher": (i32, [i32, C.POINTER(i64), pi32, C.POINTER(i64), pi32, i32, i32, i32,
@@ -239,6 +240,12 @@ class Context:
         ms, n = C.c_double(), C.c_int64()
         self._check(load().whisper_profile_read(self.h, kernel, C.byref(ms), C.byref(n)))
         return ms.value, n.value
+
+    def time_kernel(self, kernel: int, n_rows: int, reps: int) -> float:
+        """Average microseconds of reps back-to-back launches over slots 0..n_rows-1."""
+        us = C.c_double()
+        self._check(load().whisper_time_kernel(self.h, kernel, n_rows, reps, C.byref(us)))
+        return us.value
 
     def set_decoding(self, eot: int = -1, suppress=(), suppress_first=()):
         a = np.ascontiguousarray(list(suppress), dtype=np.int32)

@@ -507,6 +507,18 @@ whisper_status whisper_profile_read(whisper_ctx* ctx, int32_t kernel, double* to
     });
 }
 
+whisper_status whisper_time_kernel(whisper_ctx* ctx, int32_t kernel, int32_t n_rows, int32_t reps, double* avg_us) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (kernel != WHISPER_K_CROSS_ATTN || !avg_us) return fail(ctx, WHISPER_E_INVAL, "only WHISPER_K_CROSS_ATTN; avg_us not NULL");
+    if (n_rows < 1 || n_rows > ctx->p.max_slots || reps < 1)
+        return fail(ctx, WHISPER_E_INVAL, "n_rows in 1..max_slots and reps >= 1");
+    return guarded(ctx, [&]() -> whisper_status {
+        *avg_us = ctx->eng->time_cross_attn(n_rows, reps);
+        return WHISPER_OK;
+    });
+}
+
 whisper_status whisper_stats_read(whisper_ctx* ctx, whisper_stats* out, int32_t reset) {
     if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
     if (!out) return fail(ctx, WHISPER_E_INVAL, "out is NULL");

@@ -46,6 +46,11 @@ class Engine {
     virtual void debug_copy(int tensor, int index, void* dst, size_t bytes) = 0;
     virtual void profile_enable(int kernel, bool on) = 0;
     virtual void profile_read(int kernel, double* ms, int64_t* launches) = 0;
+    // Average microseconds of `reps` back-to-back launches of the decode
+    // cross-attention kernel over slots 0..n-1 (launch i reads layer i mod
+    // the decoder depth), between two events on the stream. The slots'
+    // caches are read as they are; the attention output buffer is written.
+    virtual double time_cross_attn(int n, int reps) = 0;
     // Completion-time marks: mark_reset() starts the clock on the stream,
     // mark() records a point after the work queued so far and returns its
     // index, mark_times_us() waits for the stream and returns every mark's

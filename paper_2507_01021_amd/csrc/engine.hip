@@ -544,6 +544,32 @@ class EngineT final : public Engine {
         prof_[k].total_ms = 0.0;
         prof_[k].launches = 0;
     }
+    double time_cross_attn(int n, int reps) override {
+        WMI_HIP(hipSetDevice(dev_));
+        if (n < 1 || n > S_ || reps < 1) throw ArgError(WHISPER_E_INVAL, "time_cross_attn: n in 1..max_slots, reps >= 1");
+        std::vector<int> rows(n);
+        for (int i = 0; i < n; ++i) rows[i] = i;
+        list_host_ = rows;
+        upload(0, list_, rows.data(), n * sizeof(int));
+        hipEvent_t e0, e1;
+        WMI_HIP(hipEventCreate(&e0));
+        WMI_HIP(hipEventCreate(&e1));
+        WMI_HIP(hipEventRecord(e0, st_));
+        for (int i = 0; i < reps; ++i) {
+            const long long sl = (long long)(i % Ld_) * S_ * H_ * 64;
+            DecAttnArgs ca{dq_, ktc_ + sl * TC, vc_ + sl * TC, datt_, list_, nullptr, TC, H_, d_};
+            hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, st_, ca);
+        }
+        WMI_HIP(hipEventRecord(e1, st_));
+        WMI_HIP(hipEventSynchronize(e1));
+        float ms = 0.f;
+        const hipError_t e = hipEventElapsedTime(&ms, e0, e1);
+        (void)hipEventDestroy(e0);
+        (void)hipEventDestroy(e1);
+        WMI_HIP(e);
+        return 1000.0 * ms / reps;
+    }
+
     void profile_read(int k, double* ms, int64_t* launches) override {
         WMI_HIP(hipStreamSynchronize(st_));
         recycle(k);

@@ -104,4 +104,6 @@ def test_null_context_calls_fail_cleanly(lib):
     assert lib.whisper_batch_transcribe(None, None, 1, None, 0, None) == binding.E_INVAL
     st = binding.whisper_stats()
     assert lib.whisper_stats_read(None, C.byref(st), 0) == binding.E_INVAL
+    us = C.c_double()
+    assert lib.whisper_time_kernel(None, binding.K_CROSS_ATTN, 1, 1, C.byref(us)) == binding.E_INVAL
     lib.whisper_ctx_destroy(None)

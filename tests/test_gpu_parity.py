@@ -94,6 +94,22 @@ def test_tiny_transcribe_maps_ids_and_matches_oracle(tiny):
         check_tokens(r["tokens"], o["logits"], TOL["f32"])
 
 
+def test_time_kernel_cross_attention(tiny):
+    """whisper_time_kernel: back-to-back cross-attention launches give a
+    positive average, bad arguments are refused, and a transcribe call
+    afterwards still matches the oracle."""
+    shape, W, segs, ref, ctx = tiny
+    us = ctx.time_kernel(binding.K_CROSS_ATTN, 2, 8)
+    log(f"tiny cross-attention, 2 rows: {us:.2f} us per launch")
+    assert us > 0
+    for kernel, rows, reps in ((binding.K_SELF_ATTN, 2, 1), (binding.K_CROSS_ATTN, 3, 1), (binding.K_CROSS_ATTN, 1, 0)):
+        with pytest.raises(binding.WhisperError):
+            ctx.time_kernel(kernel, rows, reps)
+    res = ctx.transcribe(segs)
+    for s, r, o in zip(segs, res, ref):
+        check_tokens(r["tokens"], o["logits"], TOL["f32"])
+
+
 def test_base_bf16_teacher_forced(base):
     shape, W, segs, ref, ctx = base
     log("base: encode 3 segments")
