@@ -100,10 +100,11 @@ def counter_traffic(workload):
 
 
 def cpu_baseline(shape, W, segs):
-    """The oracle, as is, on a bounded sample: one segment's front end, conv
-    stem, two encoder layers, two layers of cross-attention keys/values and
-    three decode steps of a two-layer decoder (plus the output head alone),
-    extrapolated per layer to the full model and the workload's token count."""
+    """The oracle, as is, on a bounded sample (about 10 s of CPU work on
+    large-v3 shapes): one segment's front end, conv stem, NL encoder layers,
+    NL layers of cross-attention keys/values and three decode steps of an
+    NL-layer decoder (plus the output head alone), extrapolated per layer to
+    the full model and the workload's token count."""
     import oracle
     from oracle import model as M
 
@@ -119,35 +120,36 @@ def cpu_baseline(shape, W, segs):
     t = time.perf_counter()
     x = M.conv_stem(W, mel[None]) + M.sinusoid_pe(1500, shape.d)[None]
     t_stem = time.perf_counter() - t
-    sh2 = shape.with_(n_enc=2, n_dec=2)
+    NL = min(6, shape.n_enc, shape.n_dec)
+    shl = shape.with_(n_enc=NL, n_dec=NL)
     t = time.perf_counter()
-    E = M.encoder(W, sh2, mel[None])
-    t_enc2 = time.perf_counter() - t
-    t_layer = max(t_enc2 - t_stem, 1e-9) / 2
+    E = M.encoder(W, shl, mel[None])
+    t_encl = time.perf_counter() - t
+    t_layer = max(t_encl - t_stem, 1e-9) / NL
     t = time.perf_counter()
-    ckv = M._seg_ckv(M.cross_kv(W, sh2, E), 0)
-    t_ckv = (time.perf_counter() - t) / 2
-    cache = M.DecoderCache(sh2)
+    ckv = M._seg_ckv(M.cross_kv(W, shl, E), 0)
+    t_ckv = (time.perf_counter() - t) / NL
+    cache = M.DecoderCache(shl)
     t = time.perf_counter()
     for tok in s0.prompt[:3]:
-        M.decoder_step(W, sh2, tok, cache, ckv)
-    t_step2 = (time.perf_counter() - t) / 3
+        M.decoder_step(W, shl, tok, cache, ckv)
+    t_stepl = (time.perf_counter() - t) / 3
     z = np.zeros((1, shape.d))
     t = time.perf_counter()
     _ = M.layer_norm(z, M._w(W, "dec.ln.g"), M._w(W, "dec.ln.b")) @ M._w(W, "dec.tok_emb").T
     t_head = time.perf_counter() - t
-    t_step = t_head + (t_step2 - t_head) / 2 * shape.n_dec
+    t_step = t_head + (t_stepl - t_head) / NL * shape.n_dec
     per_seg = []
     for s in segs:
         per_seg.append(t_fe + t_stem + shape.n_enc * t_layer + shape.n_dec * t_ckv
                        + (len(s.prompt) - 1 + s.max_new_tokens) * t_step)
     audio = sum(s.seconds for s in segs)
-    sample_s = t_fe + t_enc2 + 2 * t_ckv + 3 * t_step2 + t_head
+    sample_s = t_fe + t_encl + NL * t_ckv + 3 * t_stepl + t_head
     return {
         "value": audio / sum(per_seg), "unit": "audio-s/s", "cores": int(threads), "kind": "oracle",
         "cpu": cpu_model(), "host_cpus": os.cpu_count(),
-        "sample": (f"1 segment: front end, conv stem, 2 of {shape.n_enc} encoder layers, 2 of "
-                   f"{shape.n_dec} cross-KV layers, 3 decode steps of a 2-layer decoder + output head; "
+        "sample": (f"1 segment: front end, conv stem, {NL} of {shape.n_enc} encoder layers, {NL} of "
+                   f"{shape.n_dec} cross-KV layers, 3 decode steps of a {NL}-layer decoder + output head; "
                    f"extrapolated per layer and per token to the workload ({sample_s:.1f} s of CPU work)"),
     }
 
