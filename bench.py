@@ -163,6 +163,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
+    ap.add_argument("--pad-mode", type=int, default=0, choices=(0, 1),
+                    help="0: pad the audio to 30 s, then the front end (default); 1: front end on the "
+                         "segment alone, features padded to 3000 frames")
     ap.add_argument("--max-new", type=int, default=0,
                     help="profiling runs only: decode this many tokens per segment instead of the workload's")
     a = ap.parse_args()
@@ -183,7 +186,7 @@ def main():
     blob = synth.pack_blob(W)
     dev_audio = [torch.from_numpy(s.audio).to("cuda:0") for s in segs]
     ptrs = [t.data_ptr() for t in dev_audio]
-    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=min(slots, 32))
+    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=min(slots, 32), pad_mode=a.pad_mode)
     del blob
     audio_s = sum(s.seconds for s in segs)
     torch.cuda.synchronize()
@@ -274,7 +277,8 @@ def main():
         "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
         "config": {"workload": a.workload, "segments": len(segs), "slots": slots,
                    "new_tokens": [int(min(s.max_new_tokens for s in segs)), int(max(s.max_new_tokens for s in segs))],
-                   "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1},
+                   "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1,
+                   "pad_mode": a.pad_mode},
         "roofline": roof, "encoder": enc, "decode": dec, "batcher": batcher,
     }
     if not a.no_cpu_baseline:
