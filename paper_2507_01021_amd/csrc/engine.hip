@@ -212,12 +212,15 @@ class EngineT final : public Engine {
         EB_ = p.max_encode_batch;
         WMI_HIP(hipSetDevice(dev_));
         WMI_HIP(hipStreamCreateWithFlags(&own_stream_, hipStreamNonBlocking));
-        WMI_HIP(hipStreamCreateWithFlags(&st2_, hipStreamNonBlocking));
+        for (int c = 1; c < MAXC; ++c) {
+            WMI_HIP(hipStreamCreateWithFlags(&cst_[c], hipStreamNonBlocking));
+            WMI_HIP(hipEventCreateWithFlags(&join_ev_[c], hipEventDisableTiming));
+        }
         WMI_HIP(hipEventCreateWithFlags(&fork_ev_, hipEventDisableTiming));
-        WMI_HIP(hipEventCreateWithFlags(&join_ev_, hipEventDisableTiming));
         st_ = own_stream_;
         if (const char* g = getenv("WHISPER_STEP_GRAPHS")) graphs_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_STEP_SPLIT")) split_ = g[0] != '0';
+        if (const char* g = getenv("WHISPER_STEP_CHAINS")) chains_ = std::max(1, std::min(MAXC, atoi(g)));
         if (const char* g = getenv("WHISPER_FUSED_LN")) fused_ln_ = g[0] != '0';
         load_weights(blob, bytes);
         alloc_state();
@@ -232,7 +235,8 @@ class EngineT final : public Engine {
         for (auto e : event_pool_) (void)hipEventDestroy(e);
         for (auto e : marks_) (void)hipEventDestroy(e);
         if (mark_start_) (void)hipEventDestroy(mark_start_);
-        if (st2_) (void)hipStreamSynchronize(st2_);
+        for (int c = 1; c < MAXC; ++c)
+            if (cst_[c]) (void)hipStreamSynchronize(cst_[c]);
         for (auto& g : step_graphs_)
             for (auto ge : g.second)
                 if (ge) (void)hipGraphExecDestroy(ge);
@@ -247,8 +251,10 @@ class EngineT final : public Engine {
         }
         for (void* q : allocs_) (void)hipFree(q);
         if (fork_ev_) (void)hipEventDestroy(fork_ev_);
-        if (join_ev_) (void)hipEventDestroy(join_ev_);
-        if (st2_) (void)hipStreamDestroy(st2_);
+        for (int c = 1; c < MAXC; ++c) {
+            if (join_ev_[c]) (void)hipEventDestroy(join_ev_[c]);
+            if (cst_[c]) (void)hipStreamDestroy(cst_[c]);
+        }
         if (own_stream_) (void)hipStreamDestroy(own_stream_);
     }
 
@@ -281,30 +287,29 @@ class EngineT final : public Engine {
         // depends on the row count because the slot list lives in device memory.
         bool timed = false;
         for (auto& pr : prof_) timed = timed || pr.on;
-        const int h0 = timed ? n : split_rows(n);
-        const bool split = h0 < n;
+        int r0[MAXC + 1];
+        const int nc = timed ? (r0[0] = 0, r0[1] = n, 1) : chain_rows(n, r0);
+        auto stream = [&](int c) { return c == 0 ? st_ : cst_[c]; };
         prof_begin(WHISPER_K_DEC_STEP, st_);
-        if (split) {  // fork: the second half waits for everything enqueued so far
+        if (nc > 1) {  // fork: every chain waits for everything enqueued so far
             WMI_HIP(hipEventRecord(fork_ev_, st_));
-            WMI_HIP(hipStreamWaitEvent(st2_, fork_ev_, 0));
+            for (int c = 1; c < nc; ++c) WMI_HIP(hipStreamWaitEvent(cst_[c], fork_ev_, 0));
         }
         if (graphs_ && !forced && !out_tok && !out_logits && !timed) {
             auto it = step_graphs_.find(n);
             if (it == step_graphs_.end()) {
-                std::array<hipGraphExec_t, 2> ge{nullptr, nullptr};
-                ge[0] = capture(st_, [&] { launch_rows(0, h0, false, st_, 0); });
-                if (split) ge[1] = capture(st2_, [&] { launch_rows(h0, n - h0, false, st2_, 1); });
+                std::array<hipGraphExec_t, MAXC> ge{};
+                for (int c = 0; c < nc; ++c)
+                    ge[c] = capture(stream(c), [&] { launch_rows(r0[c], r0[c + 1] - r0[c], false, stream(c), c); });
                 it = step_graphs_.emplace(n, ge).first;
             }
-            WMI_HIP(hipGraphLaunch(it->second[0], st_));
-            if (split) WMI_HIP(hipGraphLaunch(it->second[1], st2_));
+            for (int c = 0; c < nc; ++c) WMI_HIP(hipGraphLaunch(it->second[c], stream(c)));
         } else {
-            launch_rows(0, h0, forced != nullptr, st_, 0);
-            if (split) launch_rows(h0, n - h0, forced != nullptr, st2_, 1);
+            for (int c = 0; c < nc; ++c) launch_rows(r0[c], r0[c + 1] - r0[c], forced != nullptr, stream(c), c);
         }
-        if (split) {  // join
-            WMI_HIP(hipEventRecord(join_ev_, st2_));
-            WMI_HIP(hipStreamWaitEvent(st_, join_ev_, 0));
+        for (int c = 1; c < nc; ++c) {  // join
+            WMI_HIP(hipEventRecord(join_ev_[c], cst_[c]));
+            WMI_HIP(hipStreamWaitEvent(st_, join_ev_[c], 0));
         }
         prof_end(WHISPER_K_DEC_STEP, st_);
         WMI_HIP(hipGetLastError());
@@ -314,11 +319,18 @@ class EngineT final : public Engine {
         if (sync_ || out_tok || out_logits || forced) WMI_HIP(hipStreamSynchronize(st_));
     }
 
-    // Rows of the first half of a step of n rows: all of them below 32 rows
-    // (or in fp32), else a whole number of 16-row tiles near n / 2.
-    int split_rows(int n) const {
-        if (!split_ || !std::is_same<T, bf16>::value || n < 32) return n;
-        return 16 * std::max(1, (n + 16) / 32);
+    // Rows of a step of n rows cut into chains (independent launch
+    // sequences on their own streams): one chain below 32 rows (or in fp32),
+    // else up to chains_ chains of whole 16-row tiles, as even as the tiles
+    // allow. r0[c] .. r0[c + 1] - 1 are chain c's rows; returns the count.
+    int chain_rows(int n, int* r0) const {
+        const int tiles = (n + 15) / 16;
+        const int k = (!split_ || !std::is_same<T, bf16>::value || n < 32) ? 1 : std::min(chains_, tiles);
+        r0[0] = 0;
+        for (int c = 1; c < k; ++c)  // boundary c: the tile nearest c * n / k, one tile per chain at least
+            r0[c] = 16 * std::max(r0[c - 1] / 16 + 1, std::min(tiles - (k - c), (2 * c * n + 16 * k) / (32 * k)));
+        r0[k] = n;
+        return k;
     }
 
     template <class F>
@@ -335,10 +347,10 @@ class EngineT final : public Engine {
     }
 
     // The kernels of one decode step for rows r0 .. r0+n-1 of the slot list,
-    // on stream s, with split-K partial buffer `half` (0 or 1). r0 is a
-    // multiple of 16, so the fragment-major activations of these rows start
-    // at element r0 * K.
-    void launch_rows(int r0, int n, bool forced, hipStream_t s, int half) {
+    // on stream s, with chain c's split-K partial buffer. r0 is a multiple
+    // of 16, so the fragment-major activations of these rows start at
+    // element r0 * K.
+    void launch_rows(int r0, int n, bool forced, hipStream_t s, int c) {
         const int d = d_;
         const int ks1 = split_k(d), ks4 = split_k(4 * d);
         const int* list = list_ + r0;
@@ -348,7 +360,7 @@ class EngineT final : public Engine {
         T* dh = dh_ + (size_t)r0 * 4 * d;
         float* dx = dx_ + (size_t)r0 * d;
         int* rowlen = rowlen_ + r0;
-        float* pbuf = gpart_ + (size_t)half * 4 * S_ * d;
+        float* pbuf = gpart_ + (size_t)c * 4 * S_ * d;
         WMI_SWITCH_E(d, hipLaunchKernelGGL((embed_ln_kernel<T, E>), dim3(n), dim3(64), 0, s, tok_emb_, pos_emb_,
                                            list, pos_, seq_, dx, dz, dec_[0].ln1g, dec_[0].ln1b));
         for (int l = 0; l < Ld_; ++l) {
@@ -628,9 +640,11 @@ class EngineT final : public Engine {
     unsigned long long* best_;
     std::vector<int> list_host_;
     bool graphs_ = true, split_ = true, fused_ln_ = true;
-    std::map<int, std::array<hipGraphExec_t, 2>> step_graphs_;  // per row count: first and second half
-    hipStream_t st2_ = nullptr;                                 // second half of a split step
-    hipEvent_t fork_ev_ = nullptr, join_ev_ = nullptr;
+    static constexpr int MAXC = 4;                                  // chains of a step (hardware queues)
+    int chains_ = 2;
+    std::map<int, std::array<hipGraphExec_t, MAXC>> step_graphs_;  // per row count: one graph per chain
+    hipStream_t cst_[MAXC] = {};                                   // streams of chains 1.. (chain 0: st_)
+    hipEvent_t fork_ev_ = nullptr, join_ev_[MAXC] = {};
     // host staging
     Stage stage_[3];
     int32_t* tokpin_ = nullptr;
@@ -986,7 +1000,7 @@ class EngineT final : public Engine {
         datt_ = dalloc<T>(S16 * d);
         dh_ = dalloc<T>(S16 * 4 * d);
         logits_ = dalloc<float>(S * (size_t)V_);
-        gpart_ = dalloc<float>(2 * 4 * S * d);  // split-K partials [half][4][rows][d]
+        gpart_ = dalloc<float>((size_t)MAXC * 4 * S * d);  // split-K partials [chain][4][rows][d]
         best_ = dalloc<unsigned long long>(S);
     }
 };
