@@ -16,6 +16,10 @@ public Whisper architecture (pre-LN transformer encoder-decoder, conv stem,
 sinusoidal encoder positions, learned decoder positions, tied output head)
 and its log-mel recipe. Every such reading is listed in the design doc.
 
+The CTC variant (oracle/ctc.py) reads the paper's remark on encoder-only
+CTC recognisers as the same encoder with a linear head and greedy best-path
+decoding.
+
 Pins (tests/test_oracle_*.py): DFT vs numpy.fft, a bin-centred tone's closed
 form, Parseval, Slaney mel closed forms and a library filter bank, the whole
 front end and the whole network against an independent library
@@ -28,6 +32,7 @@ from .frontend import (hann_periodic, frame_audio, power_spectrum, hz_to_mel, me
 from .model import (layer_norm, gelu, softmax, mha, conv_stem, sinusoid_pe, encoder,
                     cross_kv, decoder_logits_full, DecoderCache, decoder_step, greedy,
                     transcribe, transcribe_batch)
+from .ctc import valid_frames, ctc_logits, best_path, collapse, transcribe_ctc
 
 __all__ = [
     "hann_periodic", "frame_audio", "power_spectrum", "hz_to_mel", "mel_to_hz",

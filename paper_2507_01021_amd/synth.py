@@ -56,13 +56,19 @@ BASE = ModelShape("base", 80, 512, 8, 6, 6, 51865, "bf16")
 SMALL = ModelShape("small", 80, 768, 12, 12, 12, 51865, "bf16")
 LARGE_V3 = ModelShape("large-v3", 128, 1280, 20, 32, 32, 51866, "bf16")
 TURBO = ModelShape("large-v3-turbo", 128, 1280, 20, 32, 4, 51866, "bf16")
-SHAPES = {s.name: s for s in (TINY, BASE, SMALL, LARGE_V3, TURBO)}
+# Encoder-only CTC models (n_dec = 0): the encoder of the named shape and a
+# linear head to n_vocab ids, id 0 the blank.
+CTC_TINY = ModelShape("ctc-tiny", 80, 384, 6, 4, 0, 256, "f32")
+CTC_BASE = ModelShape("ctc-base", 80, 512, 8, 6, 0, 1024, "bf16")
+SHAPES = {s.name: s for s in (TINY, BASE, SMALL, LARGE_V3, TURBO, CTC_TINY, CTC_BASE)}
 
 
 def prompt_for(shape: ModelShape) -> list[int]:
     """Start-of-transcript, language, task and no-timestamps ids (the prompt
     plus no-timestamp token of Section 2.3). With random weights only their
     range matters; both sides receive the same list."""
+    if shape.n_dec == 0:
+        return []  # CTC models take no prompt
     if shape.n_vocab >= 51866:
         return [50258, 50259, 50360, 50364]
     return [50258, 50259, 50359, 50363]
@@ -106,6 +112,8 @@ def tensor_specs(shape: ModelShape):
         specs += _ln_specs(p + ".attn_ln", d) + _attn_specs(p + ".attn", d)
         specs += _ln_specs(p + ".mlp_ln", d) + _mlp_specs(p + ".mlp", d)
     specs += _ln_specs("enc.ln_post", d)
+    if shape.n_dec == 0:  # encoder-only CTC model: the head instead of a decoder
+        return specs + [("ctc.w", (shape.n_vocab, d), "w"), ("ctc.b", (shape.n_vocab,), "w")]
     specs += [("dec.tok_emb", (shape.n_vocab, d), "w"),
               ("dec.pos_emb", (shape.n_text_ctx, d), "w")]
     for i in range(shape.n_dec):
@@ -297,10 +305,22 @@ def workload(name: str, seed: int = 1):
     if name == "turbo-u64-q512":
         s = TURBO
         return s, poisson_users(s, 64, 512, 5.0, 16, 224, seed), 128
+    if name == "ctc-tiny-b2":
+        s = CTC_TINY
+        return s, fixed_batch(s, [48000, 112000], 1500, seed), 2
+    if name == "ctc-base-u64-q512":
+        # the turbo queue's arrivals and lengths, served by an encoder-only
+        # CTC model (output capacity 1500 labels, one per encoder frame)
+        s = CTC_BASE
+        segs = poisson_users(s, 64, 512, 5.0, 16, 224, seed)
+        for g in segs:
+            g.max_new_tokens = 1500
+        return s, segs, 32
     raise KeyError(name)
 
 
-WORKLOADS = ("tiny-b2", "base-b16", "small-u8-b64", "large-v3-b32", "turbo-u64-q512")
+WORKLOADS = ("tiny-b2", "base-b16", "small-u8-b64", "large-v3-b32", "turbo-u64-q512", "ctc-tiny-b2",
+             "ctc-base-u64-q512")
 
 
 def recording(shape: ModelShape, rng: np.random.Generator, seconds: float, user_id: int, first_id: int,
