@@ -39,6 +39,8 @@ def encoder_flops(shape):
     f = 2 * 3000 * d * 3 * shape.n_mels + 2 * T * d * 3 * d
     f += shape.n_enc * (2 * T * 12 * d * d + 4 * T * T * d)
     f += 2 * T * d * 2 * d * shape.n_dec
+    if shape.n_dec == 0:  # encoder-only CTC model: the head over every frame
+        f += 2 * T * d * shape.n_vocab
     return float(f)
 
 
@@ -154,6 +156,27 @@ def cpu_baseline(shape, W, segs):
     }
 
 
+def cpu_baseline_ctc(shape, W, segs):
+    """The CTC oracle, as is, on one segment (front end, stem, every encoder
+    layer, head, best path and collapse), extrapolated to the workload."""
+    from oracle import ctc as OC
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    t = time.perf_counter()
+    done = 0
+    while done < min(len(segs), 32) and time.perf_counter() - t < 10.0:  # about 10 s of CPU work
+        OC.transcribe_ctc(W, shape, [segs[done]])
+        done += 1
+    spent = time.perf_counter() - t
+    audio = sum(s.seconds for s in segs[:done])
+    return {"value": audio / spent, "unit": "audio-s/s", "cores": int(threads), "kind": "oracle",
+            "cpu": cpu_model(), "host_cpus": os.cpu_count(),
+            "sample": f"the first {done} segments, each through the whole CTC oracle ({spent:.1f} s of CPU work)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -200,7 +223,11 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st_timed = ctx.stats(reset=True)
-    assert all(r["status"] == 0 and r["tokens"].size == s.max_new_tokens for r, s in zip(res, segs))
+    ctc = shape.n_dec == 0
+    assert all(r["status"] == 0 and (r["tokens"].size <= s.max_new_tokens if ctc else r["tokens"].size == s.max_new_tokens)
+               for r, s in zip(res, segs))
+    if ctc:
+        return bench_ctc(a, ctx, shape, W, segs, slots, ptrs, audio_s, wall, st_timed)
     # Per-kernel timing: the same steps again with HIP events around every
     # launch of the named kernels on the library's stream (decode steps then
     # run as individual launches instead of one captured graph per step).
@@ -283,6 +310,56 @@ def main():
     }
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, W, segs)
+    ctx.close()
+    print(json.dumps(out), flush=True)
+
+
+def bench_ctc(a, ctx, shape, W, segs, slots, ptrs, audio_s, wall, st_timed):
+    """Encoder-only CTC workload: the queue in encoder passes; its roofline is
+    the encoder's fc1 GEMM (MFMA-bound), timed with HIP events around every
+    launch in a second run of the same calls."""
+    import torch
+
+    from paper_2507_01021_amd import binding
+
+    kinds = (binding.K_ENC_PASS, binding.K_ENC_GEMM, binding.K_FRONT_END)
+    for k in kinds:
+        ctx.profile_enable(k, True)
+    for _ in range(a.steps):
+        ctx.transcribe(segs, device_audio=ptrs)
+    torch.cuda.synchronize()
+    prof = {k: ctx.profile_read(k) for k in kinds}
+    peak_f = PEAK_BF16 if shape.dtype == "bf16" else PEAK_F32
+    enc_ms, enc_n = prof[binding.K_ENC_PASS]
+    fl = encoder_flops(shape) * len(segs) * a.steps
+    g_ms, g_n = prof[binding.K_ENC_GEMM]
+    fc1_flops = 2 * 1500 * shape.d * 4 * shape.d * len(segs) * shape.n_enc * a.steps
+    fc1_tf = fc1_flops / (g_ms / 1e3) / 1e12
+    roof = {"bound": "mfma", "achieved": round(fc1_tf, 1), "peak": peak_f / 1e12, "unit": "TFLOP/s",
+            "frac": round(fc1_tf * 1e12 / peak_f, 4), "traffic": None,
+            "kernel": "gemm_bf16_kernel<EpiGelu> (encoder fc1 + GELU)",
+            "flops_per_launch": fc1_flops / max(g_n, 1), "avg_launch_us": round(g_ms * 1e3 / max(g_n, 1), 2),
+            "launches": g_n}
+    fe_ms, fe_n = prof[binding.K_FRONT_END]
+    enc = {"ms_per_pass": round(enc_ms / max(enc_n, 1), 3), "passes": enc_n,
+           "tflops": round(fl / (enc_ms / 1e3) / 1e12, 1), "mfma_frac": round(fl / (enc_ms / 1e3) / peak_f, 4),
+           "front_end_ms_per_pass": round(fe_ms / max(fe_n, 1), 3), "fc1_gemm_tflops": round(fc1_tf, 1)}
+    batcher = {"passes_per_call": st_timed["encode_passes"] // a.steps,
+               "host_ms_per_call": round(st_timed["batcher_host_ms"] / a.steps, 3),
+               "engine_host_ms_per_call": round(st_timed["engine_host_ms"] / a.steps, 2)}
+    value = audio_s * a.steps / wall
+    out = {
+        "metric": "audio-sec transcribed/sec (RTFx) at batch B; encoder MFMA util; decode HBM GB/s",
+        "value": round(value, 2), "unit": "audio-s/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(wall / a.steps * 1e3, 2), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
+        "config": {"workload": a.workload, "segments": len(segs), "encode_batch": slots,
+                   "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1, "pad_mode": a.pad_mode,
+                   "decoding": "CTC best path"},
+        "roofline": roof, "encoder": enc, "batcher": batcher,
+    }
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_ctc(shape, W, segs)
     ctx.close()
     print(json.dumps(out), flush=True)
 

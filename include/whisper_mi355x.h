@@ -149,6 +149,20 @@ typedef struct whisper_ctx whisper_ctx;
  * dtype, n_mels, n_audio_ctx, n_audio_state, n_audio_head, n_audio_layer,
  * n_vocab, n_text_ctx, n_text_state, n_text_head, n_text_layer, n_tensors,
  * reserved; zeros to byte 256.
+ * n_text_layer = 0 marks an encoder-only CTC model (the paper's remark that
+ * CTC-based recognisers are served the same way, Introduction and the end of
+ * Section 2.3): its tensors end after enc.ln_post with ctc.w [n_vocab, d]
+ * and ctc.b [n_vocab], and id 0 is the CTC blank. Such a context decodes
+ * greedily by best path: over the ceil(n_samples / 320) encoder frames that
+ * cover a segment's audio (at most 1500), the most likely id per frame
+ * (lowest id on ties), runs of one id merged, blanks dropped. Its segments
+ * need no prompt (prompt and n_prompt are ignored) and max_new_tokens
+ * (1..1500) is the output capacity: n_tokens <= max_new_tokens labels.
+ * whisper_batch_transcribe / _serve run the same queue in encoder passes
+ * of up to max_encode_batch segments; whisper_batch_encode (n <=
+ * max_encode_batch, slots ignored) feeds the debug tensors; the decoder
+ * calls (decode step, slot tokens, decoding options, cross-attention timing)
+ * return WHISPER_E_STATE.
  * Canonical order (d = state, matrices are [out, in], conv [out, in, 3]):
  *   enc.conv1.w [d, n_mels, 3], enc.conv1.b, enc.conv2.w [d, d, 3], enc.conv2.b,
  *   per encoder layer: attn_ln.{g,b}, attn.{q.w, q.b, k.w, v.w, v.b, o.w, o.b},
@@ -278,7 +292,10 @@ enum {
                               of the last encode pass */
     WHISPER_T_ENC_OUT = 1, /* fp32 [1500][d] encoder output of that entry */
     WHISPER_T_CROSS_K = 2, /* fp32 [n_text_layer][n_head][1500][64] of slot `index` */
-    WHISPER_T_CROSS_V = 3  /* same shape, values */
+    WHISPER_T_CROSS_V = 3, /* same shape, values */
+    WHISPER_T_CTC_LOGITS = 4, /* CTC models: fp32 [1500][n_vocab] head output of entry `index`
+                                 of the last encode pass */
+    WHISPER_T_CTC_IDS = 5     /* CTC models: int32 [1500] most likely id of every frame of it */
 };
 
 /* Copies a stage's tensor to dst (host, `bytes` must equal its size). */

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwhisper_
 
 OK, E_INVAL, E_NOMEM, E_DEVICE, E_CAPACITY, E_STATE, E_BUFFER, E_FORMAT = 0, -1, -2, -3, -4, -5, -6, -7
 DTYPE_F32, DTYPE_BF16 = 0, 1
-T_MEL, T_ENC_OUT, T_CROSS_K, T_CROSS_V = 0, 1, 2, 3
+T_MEL, T_ENC_OUT, T_CROSS_K, T_CROSS_V, T_CTC_LOGITS, T_CTC_IDS = 0, 1, 2, 3, 4, 5
 K_CROSS_ATTN, K_ENC_GEMM, K_SELF_ATTN, K_ENC_ATTN, K_ENC_PASS, K_DEC_STEP, K_FRONT_END = 0, 1, 2, 3, 4, 5, 6
 
 EXPORTS = (
@@ -228,8 +228,8 @@ class Context:
                         "finish_us": r.finish_us, "tokens": buf[r.token_offset: r.token_offset + r.n_tokens].copy()})
         return out
 
-    def debug_copy(self, tensor: int, index: int, shape):
-        out = np.empty(shape, dtype=np.float32)
+    def debug_copy(self, tensor: int, index: int, shape, dtype=np.float32):
+        out = np.empty(shape, dtype=dtype)
         self._check(load().whisper_debug_copy(self.h, tensor, index, out.ctypes.data, out.nbytes))
         return out
 

@@ -113,4 +113,37 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
     be.finish();
 }
 
+void run_queue_passes(const std::vector<QueuedSegment>& segs, int encode_batch, BatchBackend& be, bool realtime,
+                      const BatchPolicy& policy) {
+    if (encode_batch < 1) throw std::invalid_argument("batcher: bad parameters");
+    const int n = (int)segs.size();
+    std::vector<int> order(n);
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::sort(order.begin(), order.end(), [&](int a, int b) {
+        return std::make_tuple(segs[a].arrival_us, segs[a].user_id, segs[a].segment_id, a) <
+               std::make_tuple(segs[b].arrival_us, segs[b].user_id, segs[b].segment_id, b);
+    });
+    size_t next = 0, head = 0;  // order[head, next): queued; order[next, n): still to arrive
+    std::vector<int> idx;
+    while (head < (size_t)n) {
+        const int64_t now = realtime ? be.now_us() : 0;
+        while (next < (size_t)n && (!realtime || segs[order[next]].arrival_us <= now)) ++next;
+        if (head == next) {  // nothing queued: wait for the next arrival
+            be.wait_until(segs[order[next]].arrival_us);
+            continue;
+        }
+        if (realtime && policy.dynamic && (int)(next - head) < encode_batch && next < (size_t)n) {
+            const int64_t deadline = segs[order[head]].arrival_us + policy.max_wait_us;
+            if (now < deadline) {
+                be.wait_until(std::min(deadline, segs[order[next]].arrival_us));
+                continue;
+            }
+        }
+        idx.clear();
+        while (head < next && (int)idx.size() < encode_batch) idx.push_back(order[head++]);
+        be.encode(idx.data(), (int)idx.size(), nullptr);
+    }
+    be.finish();
+}
+
 }  // namespace wmi

@@ -82,4 +82,13 @@ void run_continuous_batching(const std::vector<QueuedSegment>& segs, int n_slots
                              const std::vector<int64_t>& offsets, int32_t* token_buf, BatchBackend& be,
                              bool realtime = false, const BatchPolicy& policy = BatchPolicy());
 
+// Encoder-only models (CTC): the same queue (arrival order, real-time
+// admission) served in passes of up to encode_batch segments, with no slots
+// or decode steps; be.encode(idx, n, nullptr) computes and delivers the
+// segments' results. With the dynamic policy and real-time admission, a
+// pass is held back (while more segments are still to arrive) until
+// encode_batch are queued or the oldest queued one has waited max_wait_us.
+void run_queue_passes(const std::vector<QueuedSegment>& segs, int encode_batch, BatchBackend& be,
+                      bool realtime = false, const BatchPolicy& policy = BatchPolicy());
+
 }  // namespace wmi

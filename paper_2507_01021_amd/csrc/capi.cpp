@@ -68,6 +68,10 @@ std::string check_segment(const whisper_params& p, const whisper_segment& s, int
     if (!s.audio) return at + "audio is NULL";
     if (s.n_samples < 1 || s.n_samples > 480000) return at + "n_samples must be in 1..480000";
     if (s.audio_on_device != 0 && s.audio_on_device != 1) return at + "audio_on_device must be 0 or 1";
+    if (p.n_text_layer == 0) {  // CTC model: no prompt, max_new_tokens is the output capacity
+        if (s.max_new_tokens < 1 || s.max_new_tokens > 1500) return at + "max_new_tokens must be in 1..1500";
+        return "";
+    }
     if (s.n_prompt < 1 || !s.prompt) return at + "needs a prompt of at least one token";
     if (s.max_new_tokens < 1) return at + "max_new_tokens must be >= 1";
     if ((int64_t)s.n_prompt + s.max_new_tokens > p.n_text_ctx)
@@ -91,7 +95,8 @@ std::string check_params(const whisper_params& p, const whisper_params& blob) {
     if (p.n_audio_head < 1 || p.n_audio_state != 64 * p.n_audio_head) return "head size must be 64";
     if (p.n_audio_state > 2048) return "width above 2048 is not supported";
     if (p.n_mels < 4 || p.n_mels > 128 || p.n_mels % 4) return "n_mels must be a multiple of 4 in 4..128";
-    if (p.n_audio_layer < 1 || p.n_text_layer < 1 || p.n_vocab < 1) return "layer counts and vocabulary must be >= 1";
+    if (p.n_audio_layer < 1 || p.n_text_layer < 0 || p.n_vocab < (p.n_text_layer == 0 ? 2 : 1))
+        return "encoder layers >= 1, decoder layers >= 0 (0: CTC model), vocabulary >= 1 (CTC: >= 2)";
     if (p.max_slots < 1 || p.max_slots > 128) return "max_slots must be in 1..128";
     if (p.max_encode_batch < 0 || p.max_encode_batch > p.max_slots) return "max_encode_batch must be in 0..max_slots";
     if (p.pad_mode != 0 && p.pad_mode != 1) return "pad_mode must be 0 or 1";
@@ -232,6 +237,86 @@ std::vector<int64_t> offsets_of(const std::vector<wmi::QueuedSegment>& q, int64_
     return off;
 }
 
+// Batch backend of encoder-only CTC models: each pass computes and delivers
+// its segments' labels (truncated to max_new_tokens) and completion mark.
+struct CtcBackend : wmi::BatchBackend {
+    using clock = std::chrono::steady_clock;
+    whisper_ctx* c = nullptr;
+    const whisper_segment* segs = nullptr;
+    const std::vector<int64_t>* off = nullptr;
+    int32_t* token_buf = nullptr;
+    whisper_result* results = nullptr;
+    clock::time_point t0 = clock::now();
+    std::vector<int> mark_of;
+    std::vector<int32_t> tok, cnt;
+    double engine_ms = 0.0;
+    void encode(const int* idx, int n, const int*) override {
+        const clock::time_point t = clock::now();
+        std::vector<wmi::SegmentDesc> d(n);
+        for (int k = 0; k < n; ++k) {
+            const whisper_segment& s = segs[idx[k]];
+            d[k] = wmi::SegmentDesc{s.audio, s.n_samples, s.audio_on_device == 1, nullptr, 0};
+        }
+        c->eng->encode_ctc(d.data(), n);
+        const int m = c->eng->mark();
+        tok.resize((size_t)n * 1500);
+        cnt.resize(n);
+        c->eng->read_ctc(n, tok.data(), cnt.data());
+        for (int k = 0; k < n; ++k) {
+            const int i = idx[k];
+            const int32_t k_tok = std::min(cnt[k], segs[i].max_new_tokens);
+            int32_t* dst = token_buf + (*off)[i];
+            std::copy(tok.begin() + (size_t)k * 1500, tok.begin() + (size_t)k * 1500 + k_tok, dst);
+            std::fill(dst + k_tok, dst + segs[i].max_new_tokens, -1);
+            results[i].n_tokens = k_tok;
+            mark_of[i] = m;
+        }
+        c->stats.encode_passes += 1;
+        c->stats.segments_encoded += n;
+        c->stats.refill_batches += 1;
+        engine_ms += std::chrono::duration<double, std::milli>(clock::now() - t).count();
+    }
+    void step(const int*, int) override {}
+    void retire(int, int, int, int32_t*) override {}
+    void finish() override {}
+    int64_t now_us() override {
+        return std::chrono::duration_cast<std::chrono::microseconds>(clock::now() - t0).count();
+    }
+    void wait_until(int64_t t) override {
+        const int64_t dt = t - now_us();
+        if (dt > 0) std::this_thread::sleep_for(std::chrono::microseconds(dt));
+    }
+};
+
+whisper_status serve_ctc(whisper_ctx* ctx, const whisper_segment* segs, int n, const std::vector<wmi::QueuedSegment>& q,
+                         const std::vector<int64_t>& off, int32_t* token_buf, whisper_result* results, bool realtime) {
+    const whisper_status r = guarded(ctx, [&]() -> whisper_status {
+        CtcBackend be;
+        be.c = ctx;
+        be.segs = segs;
+        be.off = &off;
+        be.token_buf = token_buf;
+        be.results = results;
+        be.mark_of.assign(n, -1);
+        ctx->eng->mark_reset();
+        be.t0 = CtcBackend::clock::now();
+        wmi::BatchPolicy pol;
+        pol.dynamic = ctx->p.batch_policy == 1;
+        pol.max_wait_us = 1000LL * ctx->p.max_wait_ms;
+        wmi::run_queue_passes(q, ctx->p.max_encode_batch, be, realtime, pol);
+        const double total_ms = std::chrono::duration<double, std::milli>(CtcBackend::clock::now() - be.t0).count();
+        ctx->stats.engine_host_ms += be.engine_ms;
+        ctx->stats.batcher_host_ms += total_ms - be.engine_ms;
+        const std::vector<double> t = ctx->eng->mark_times_us();
+        for (int i = 0; i < n; ++i)
+            if (be.mark_of[i] >= 0) results[i].finish_us = (int64_t)t[be.mark_of[i]];
+        return WHISPER_OK;
+    });
+    if (r != WHISPER_OK)
+        for (int i = 0; i < n; ++i) { results[i].status = r; results[i].n_tokens = 0; }
+    return r;
+}
+
 }  // namespace
 
 extern "C" {
@@ -293,6 +378,24 @@ whisper_status whisper_batch_encode(whisper_ctx* ctx, const whisper_segment* seg
     if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
     if (n < 0) return fail(ctx, WHISPER_E_INVAL, "n must be >= 0");
     if (n == 0) return WHISPER_OK;
+    if (ctx->p.n_text_layer == 0) {  // CTC model: one pass of n segments, slots ignored
+        if (!segs) return fail(ctx, WHISPER_E_INVAL, "segs must not be NULL");
+        if (n > ctx->p.max_encode_batch) return fail(ctx, WHISPER_E_CAPACITY, "a CTC encode takes at most max_encode_batch segments");
+        for (int i = 0; i < n; ++i) {
+            const std::string bad = check_segment(ctx->p, segs[i], i);
+            if (!bad.empty()) return fail(ctx, WHISPER_E_INVAL, bad);
+        }
+        return guarded(ctx, [&]() -> whisper_status {
+            std::vector<wmi::SegmentDesc> d(n);
+            for (int i = 0; i < n; ++i)
+                d[i] = wmi::SegmentDesc{segs[i].audio, segs[i].n_samples, segs[i].audio_on_device == 1, nullptr, 0};
+            ctx->eng->encode_ctc(d.data(), n);
+            ctx->eng->sync();
+            ctx->stats.encode_passes += 1;
+            ctx->stats.segments_encoded += n;
+            return WHISPER_OK;
+        });
+    }
     if (!segs || !slots) return fail(ctx, WHISPER_E_INVAL, "segs and slots must not be NULL");
     std::set<int> seen;
     for (int i = 0; i < n; ++i) {
@@ -328,6 +431,7 @@ whisper_status whisper_batch_decode_step(whisper_ctx* ctx, const int32_t* slots,
                                          int32_t* out_tokens, float* out_logits) {
     if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
     if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (ctx->p.n_text_layer == 0) return fail(ctx, WHISPER_E_STATE, "not available for an encoder-only CTC model");
     if (n < 0 || n > ctx->p.max_slots) return fail(ctx, WHISPER_E_INVAL, "n must be in 0..max_slots");
     if (n == 0) return WHISPER_OK;
     if (!slots) return fail(ctx, WHISPER_E_INVAL, "slots must not be NULL");
@@ -359,6 +463,7 @@ whisper_status whisper_batch_decode_step(whisper_ctx* ctx, const int32_t* slots,
 whisper_status whisper_slot_tokens(whisper_ctx* ctx, int32_t slot, int32_t* dst, int32_t cap, int32_t* n_out) {
     if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
     if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (ctx->p.n_text_layer == 0) return fail(ctx, WHISPER_E_STATE, "not available for an encoder-only CTC model");
     if (slot < 0 || slot >= ctx->p.max_slots) return fail(ctx, WHISPER_E_CAPACITY, "slot outside 0..max_slots-1");
     if (!n_out || (cap > 0 && !dst) || cap < 0) return fail(ctx, WHISPER_E_INVAL, "bad output buffer");
     const int g = ctx->slots[slot].generated;
@@ -385,6 +490,7 @@ whisper_status whisper_set_decoding(whisper_ctx* ctx, int32_t eot, const int32_t
                                     const int32_t* suppress_first, int32_t n_first) {
     if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
     if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (ctx->p.n_text_layer == 0) return fail(ctx, WHISPER_E_STATE, "not available for an encoder-only CTC model");
     const int V = ctx->p.n_vocab;
     if (eot < -1 || eot >= V) return fail(ctx, WHISPER_E_INVAL, "eot must be -1 or a token id");
     if (n_suppress < 0 || n_first < 0 || (n_suppress > 0 && !suppress) || (n_first > 0 && !suppress_first))
@@ -437,6 +543,7 @@ whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs
     for (int i = 0; i < n; ++i)
         results[i] = whisper_result{segs[i].segment_id, off[i], 0, segs[i].user_id, WHISPER_OK,
                                     segs[i].max_new_tokens, 0};
+    if (ctx->p.n_text_layer == 0) return serve_ctc(ctx, segs, n, q, off, token_buf, results, realtime != 0);
     const whisper_status r = guarded(ctx, [&]() -> whisper_status {
         EngineBackend be;
         be.c = ctx;
@@ -510,6 +617,7 @@ whisper_status whisper_profile_read(whisper_ctx* ctx, int32_t kernel, double* to
 whisper_status whisper_time_kernel(whisper_ctx* ctx, int32_t kernel, int32_t n_rows, int32_t reps, double* avg_us) {
     if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
     if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (ctx->p.n_text_layer == 0) return fail(ctx, WHISPER_E_STATE, "not available for an encoder-only CTC model");
     if (kernel != WHISPER_K_CROSS_ATTN || !avg_us) return fail(ctx, WHISPER_E_INVAL, "only WHISPER_K_CROSS_ATTN; avg_us not NULL");
     if (n_rows < 1 || n_rows > ctx->p.max_slots || reps < 1)
         return fail(ctx, WHISPER_E_INVAL, "n_rows in 1..max_slots and reps >= 1");

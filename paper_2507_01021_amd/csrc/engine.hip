@@ -86,6 +86,11 @@ static std::vector<TensorSpec> canonical_specs(const whisper_params& p) {
         add_mlp(v, q + ".mlp", d);
     }
     add_ln(v, "enc.ln_post", d);
+    if (p.n_text_layer == 0) {  // encoder-only CTC model: the head instead of a decoder
+        v.push_back({"ctc.w", {p.n_vocab, d}});
+        v.push_back({"ctc.b", {p.n_vocab}});
+        return v;
+    }
     v.push_back({"dec.tok_emb", {p.n_vocab, d}});
     v.push_back({"dec.pos_emb", {p.n_text_ctx, d}});
     for (int i = 0; i < p.n_text_layer; ++i) {
@@ -210,6 +215,7 @@ class EngineT final : public Engine {
         d_ = p.n_audio_state; H_ = p.n_audio_head; Le_ = p.n_audio_layer; Ld_ = p.n_text_layer;
         V_ = p.n_vocab; nm_ = p.n_mels; S_ = p.max_slots;
         EB_ = p.max_encode_batch;
+        ctc_ = Ld_ == 0;
         WMI_HIP(hipSetDevice(dev_));
         WMI_HIP(hipStreamCreateWithFlags(&own_stream_, hipStreamNonBlocking));
         for (int c = 1; c < MAXC; ++c) {
@@ -519,6 +525,12 @@ class EngineT final : public Engine {
                             out[(((size_t)l * H_ + hh) * N_CTX + t) * 64 + j] = HostElem<T>::to_f(h.data(), src);
                         }
             }
+        } else if (tensor == WHISPER_T_CTC_LOGITS && ctc_) {
+            need(bytes, (size_t)N_CTX * V_ * 4, index < last_nb_);
+            WMI_HIP(hipMemcpy(out, ctc_logits_ + (size_t)index * N_CTX * V_, bytes, hipMemcpyDeviceToHost));
+        } else if (tensor == WHISPER_T_CTC_IDS && ctc_) {
+            need(bytes, (size_t)N_CTX * 4, index < last_nb_);
+            WMI_HIP(hipMemcpy(dst, ctc_ids_ + (size_t)index * N_CTX, bytes, hipMemcpyDeviceToHost));
         } else {
             throw ArgError(WHISPER_E_INVAL, "unknown debug tensor");
         }
@@ -556,6 +568,23 @@ class EngineT final : public Engine {
         prof_[k].total_ms = 0.0;
         prof_[k].launches = 0;
     }
+    void encode_ctc(const SegmentDesc* segs, int n) override {
+        WMI_HIP(hipSetDevice(dev_));
+        if (!ctc_) throw ArgError(WHISPER_E_STATE, "not a CTC model");
+        if (n < 1 || n > EB_) throw ArgError(WHISPER_E_INVAL, "encode_ctc: 1..max_encode_batch segments");
+        const std::vector<int> none(n, 0);
+        encode_pass(segs, n, none.data());
+        WMI_HIP(hipGetLastError());
+    }
+
+    void read_ctc(int n, int32_t* tokens, int32_t* counts) override {
+        WMI_HIP(hipSetDevice(dev_));
+        if (!ctc_ || n < 1 || n > EB_) throw ArgError(WHISPER_E_INVAL, "read_ctc: 1..max_encode_batch entries of a CTC model");
+        WMI_HIP(hipMemcpyAsync(counts, ctc_cnt_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
+        WMI_HIP(hipMemcpyAsync(tokens, ctc_tok_, (size_t)n * N_CTX * sizeof(int), hipMemcpyDeviceToHost, st_));
+        WMI_HIP(hipStreamSynchronize(st_));
+    }
+
     double time_cross_attn(int n, int reps) override {
         WMI_HIP(hipSetDevice(dev_));
         if (n < 1 || n > S_ || reps < 1) throw ArgError(WHISPER_E_INVAL, "time_cross_attn: n in 1..max_slots, reps >= 1");
@@ -640,6 +669,11 @@ class EngineT final : public Engine {
     unsigned long long* best_;
     std::vector<int> list_host_;
     bool graphs_ = true, split_ = true, fused_ln_ = true;
+    bool ctc_ = false;  // encoder-only CTC model (no decoder layers)
+    T* Wctc_ = nullptr;
+    float* bctc_ = nullptr;
+    float* ctc_logits_ = nullptr;  // [max_encode_batch * 1500][n_vocab]
+    int *ctc_ids_ = nullptr, *ctc_tok_ = nullptr, *ctc_cnt_ = nullptr;
     static constexpr int MAXC = 4;                                  // chains of a step (hardware queues)
     int chains_ = 2;
     std::map<int, std::array<hipGraphExec_t, MAXC>> step_graphs_;  // per row count: one graph per chain
@@ -787,7 +821,9 @@ class EngineT final : public Engine {
                 src[i] = SegSrc{dst, s.n_samples, 0};
             }
             nv[i] = P_.pad_mode == 0 ? 3000 : s.n_samples / 160;
-            so[i] = slots[i];
+            // decoder models: the slot; CTC models: the encoder frames covering
+            // the audio (320 samples each), the frames greedy decoding reads
+            so[i] = ctc_ ? std::min(N_CTX, (s.n_samples + 319) / 320) : slots[i];
             npv[i] = s.n_prompt;
             memcpy(pr + (size_t)i * 448, s.prompt, s.n_prompt * sizeof(int));
         }
@@ -828,6 +864,14 @@ class EngineT final : public Engine {
             gemm(L.W2, 4 * d, 0, hb_, 4 * d, 0, d, M, 4 * d, 1, EpiResid{L.b2, x_, d});
         }
         ln(x_, zb_, lnpg_, lnpb_, M);
+        if (ctc_) {  // CTC head, per-frame argmax, collapse of each entry's frames
+            gemm(Wctc_, d, 0, zb_, d, 0, V_, M, d, 1, EpiCTC{bctc_, ctc_logits_, V_});
+            hipLaunchKernelGGL(ctc_argmax_kernel, dim3((M + 3) / 4), dim3(256), 0, st_, ctc_logits_, V_, M, ctc_ids_);
+            hipLaunchKernelGGL(ctc_collapse_kernel, dim3(nb), dim3(1024), 0, st_, ctc_ids_, slot_of_, ctc_tok_,
+                               ctc_cnt_);
+            prof_end(WHISPER_K_ENC_PASS, st_);
+            return;
+        }
         gemm(zb_, d, 0, WcK_, d, 0, M, Ld_ * d, d, 1, EpiCrossK<T>{ktc_, slot_of_, d, H_, S_});
         gemm(WcV_, d, 0, zb_, d, 0, Ld_ * d, M, d, 1, EpiCrossV<T>{bcV_, vc_, slot_of_, d, H_, S_});
         hipLaunchKernelGGL(seat_kernel, dim3(nb), dim3(256), 0, st_, slot_of_, seat_np_, seat_prompts_, seq_, pos_, npr_,
@@ -924,6 +968,14 @@ class EngineT final : public Engine {
         }
         lnpg_ = vecf("enc.ln_post.g");
         lnpb_ = vecf("enc.ln_post.b");
+        basis_ = upload_new(dft_basis());
+        melfb_ = upload_new(mel_bank(nm_));
+        pe_ = upload_new(sinusoids(N_CTX, d));
+        if (ctc_) {
+            Wctc_ = mat("ctc.w");
+            bctc_ = vecf("ctc.b");
+            return;
+        }
         tok_emb_ = dec_mat({"dec.tok_emb"}, d);
         pos_emb_ = mat("dec.pos_emb");
         std::vector<std::string> ck, cv;
@@ -952,9 +1004,6 @@ class EngineT final : public Engine {
         bcV_ = upload_new(bcv);
         lnfg_ = vecf("dec.ln.g");
         lnfb_ = vecf("dec.ln.b");
-        basis_ = upload_new(dft_basis());
-        melfb_ = upload_new(mel_bank(nm_));
-        pe_ = upload_new(sinusoids(N_CTX, d));
     }
 
     void alloc_state() {
@@ -1002,6 +1051,12 @@ class EngineT final : public Engine {
         logits_ = dalloc<float>(S * (size_t)V_);
         gpart_ = dalloc<float>((size_t)MAXC * 4 * S * d);  // split-K partials [chain][4][rows][d]
         best_ = dalloc<unsigned long long>(S);
+        if (ctc_) {
+            ctc_logits_ = dalloc<float>(EB * N_CTX * (size_t)V_);
+            ctc_ids_ = dalloc<int>(EB * N_CTX);
+            ctc_tok_ = dalloc<int>(EB * N_CTX);
+            ctc_cnt_ = dalloc<int>(EB);
+        }
     }
 };
 

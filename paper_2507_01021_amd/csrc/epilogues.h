@@ -243,6 +243,18 @@ struct EpiQ {  // cross-attention queries, scaled by 1/8
     }
 };
 
+// CTC head: A = head weights [n_vocab][d], B = encoder output rows (frames);
+// logits[frame][i..i+3] = acc + bias[i..i+3] (fp32, row-major [frames][n_vocab]).
+struct EpiCTC {
+    const float* bias;
+    float* out;
+    int V;
+    __device__ EpiPre pre(int i, int, int) const { EpiPre p{}; p.a = ld4(bias + i); return p; }
+    __device__ void operator()(int i, int j, int, float a, float b, float c, float e, const EpiPre& p) const {
+        st4(out + (long long)j * V + i, a + p.a.x, b + p.a.y, c + p.a.z, e + p.a.w);
+    }
+};
+
 struct EpiLogits {  // out[r][i..i+3] (fp32), rows beyond n_vocab dropped
     float* out;
     int V;

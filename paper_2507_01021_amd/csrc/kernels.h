@@ -1061,6 +1061,68 @@ inline void skinny_bf16(const bf16* W, int MA, const bf16* X, int n, int K, int 
     }
 }
 
+// ------------------------------------------------------------- CTC greedy decoding
+//
+// Best-path decoding of an encoder-only CTC model (blank = id 0): the most
+// likely id of every frame, then each entry's frames 0..T-1 collapsed
+// (runs of one id merged, blanks dropped).
+
+// One wave per frame: argmax over the V logits of the frame, the lowest id
+// among equal maxima.
+__global__ __launch_bounds__(256) void ctc_argmax_kernel(const float* __restrict__ logits, int V, int frames,
+                                                         int* __restrict__ ids) {
+    const int f = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (f >= frames) return;
+    const float* row = logits + (long long)f * V;
+    float best = -INFINITY;
+    int bi = V;
+    for (int v = lane; v < V; v += 64) {
+        const float x = row[v];
+        if (x > best) { best = x; bi = v; }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float ob = __shfl_xor(best, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+    }
+    if (lane == 0) ids[f] = bi;
+}
+
+// One workgroup (1024 threads) per batch entry b over its 1500 frame ids:
+// frame t is kept when t < T[b], its id is not the blank and differs from
+// frame t-1's; kept ids are compacted in frame order (workgroup prefix sum)
+// into tok[b][.], their number into cnt[b].
+__global__ __launch_bounds__(1024) void ctc_collapse_kernel(const int* __restrict__ ids, const int* __restrict__ nframes,
+                                                            int* __restrict__ tok, int* __restrict__ cnt) {
+    __shared__ int wsum[16];
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int T = nframes[b];
+    const int* id = ids + (long long)b * N_CTX;
+    const int t0 = 2 * tid, t1 = t0 + 1;
+    const int i0 = t0 < T ? id[t0] : 0, i1 = t1 < T ? id[t1] : 0;
+    const int prev = (t0 > 0 && t0 < T) ? id[t0 - 1] : -1;
+    const int k0 = (t0 < T && i0 != 0 && i0 != prev) ? 1 : 0;
+    const int k1 = (t1 < T && i1 != 0 && i1 != i0) ? 1 : 0;
+    const int c = k0 + k1;
+    int x = c;  // inclusive prefix over the wave
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    if (tid == 0)
+        for (int i = 1; i < 16; ++i) wsum[i] += wsum[i - 1];
+    __syncthreads();
+    const int pos = x - c + (w > 0 ? wsum[w - 1] : 0);
+    int* out = tok + (long long)b * N_CTX;
+    if (k0) out[pos] = i0;
+    if (k1) out[pos + k0] = i1;
+    if (tid == 0) cnt[b] = wsum[15];
+}
+
 // ------------------------------------------------------------- greedy step
 //
 // argmax over the logits in two kernels: (1) grid (chunks, rows), each

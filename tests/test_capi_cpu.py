@@ -107,3 +107,16 @@ def test_null_context_calls_fail_cleanly(lib):
     us = C.c_double()
     assert lib.whisper_time_kernel(None, binding.K_CROSS_ATTN, 1, 1, C.byref(us)) == binding.E_INVAL
     lib.whisper_ctx_destroy(None)
+
+
+def test_params_from_ctc_blob(lib):
+    """An encoder-only CTC blob (n_text_layer 0) parses; its layout ends with the head."""
+    shape = synth.CTC_TINY
+    lay, total = synth.blob_layout(shape)
+    assert [n for n, _, _ in lay][-2:] == ["ctc.w", "ctc.b"]
+    blob = np.zeros(total, dtype=np.uint8)
+    w = synth.make_weights(shape.with_(n_enc=1), 0)
+    hdr = synth.pack_blob(w)[:256]
+    p = binding.whisper_params()
+    assert lib.whisper_params_from_blob(hdr.ctypes.data, hdr.size, C.byref(p)) == 0
+    assert (p.n_text_layer, p.n_vocab, p.n_audio_layer) == (0, 256, 1)
