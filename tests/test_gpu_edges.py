@@ -1,0 +1,91 @@
+"""GPU edge cases against the oracle, through the C ABI: the empty call, the
+shortest and longest segments (1 and 480000 samples), and a decode that
+fills the text context to its last position (4 prompt tokens + 444 new =
+448). Tolerances as in test_gpu_parity (fp32 model)."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import ctc as OC
+from paper_2507_01021_amd import binding, synth
+
+from parity import TOL, check_tokens, drive_teacher_forced, oracle_run, rel_row_err
+
+pytestmark = pytest.mark.gpu
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    shape = synth.TINY
+    W = synth.make_weights(shape, 0)
+    with binding.Context(synth.pack_blob(W), max_slots=4) as ctx:
+        yield shape, W, ctx
+
+
+def test_empty_call(tiny):
+    shape, W, ctx = tiny
+    assert ctx.transcribe([]) == []
+    assert ctx.transcribe([], realtime=True) == []
+
+
+def test_shortest_and_longest_segments(tiny):
+    shape, W, ctx = tiny
+    segs = synth.fixed_batch(shape, [1, 480000], 8, seed=11)
+    ref = oracle_run(W, shape, segs, n_new=8)
+    log("tiny: encode segments of 1 and 480000 samples")
+    ctx.encode(segs, [0, 1])
+    for i, r in enumerate(ref):
+        mel = ctx.debug_copy(binding.T_MEL, i, (shape.n_mels, 3000))
+        assert np.abs(mel - r["mel"]).max() < 2e-5
+        E = ctx.debug_copy(binding.T_ENC_OUT, i, (1500, shape.d))
+        assert rel_row_err(E, r["E"]).max() < TOL["f32"]
+    toks, lgs = drive_teacher_forced(ctx, [0, 1], segs, ref, 8)
+    for k in range(2):
+        assert rel_row_err(lgs[k], ref[k]["logits"]).max() < TOL["f32"]
+        check_tokens(toks[k], ref[k]["logits"], TOL["f32"])
+
+
+def test_decode_to_the_last_text_position(tiny):
+    """n_prompt + max_new_tokens = 448: the self-attention caches fill up."""
+    shape, W, ctx = tiny
+    n_new = shape.n_text_ctx - 4
+    segs = synth.fixed_batch(shape, [32000, 96000], n_new, seed=12)
+    ref = oracle_run(W, shape, segs, n_new=n_new)
+    log(f"tiny: teacher-forced decode of {n_new} tokens in 2 slots")
+    ctx.encode(segs, [2, 3])
+    toks, lgs = drive_teacher_forced(ctx, [2, 3], segs, ref, n_new)
+    for k in range(2):
+        e = rel_row_err(lgs[k], ref[k]["logits"])
+        log(f"slot {k}: logits rel err max {e.max():.2e} (last position {e[-1]:.2e})")
+        assert e.max() < TOL["f32"]
+        check_tokens(toks[k], ref[k]["logits"], TOL["f32"])
+    with pytest.raises(binding.WhisperError):  # the slots retired with their last token
+        ctx.decode_step([2])
+    res = ctx.transcribe(segs)
+    for r, s in zip(res, segs):
+        assert r["tokens"].size == n_new
+
+
+def test_ctc_shortest_and_longest_segments():
+    shape = synth.CTC_TINY
+    W = synth.make_weights(shape, 0)
+    segs = synth.fixed_batch(shape, [1, 480000], 1500, seed=13)
+    ref = OC.transcribe_ctc(W, shape, segs)
+    with binding.Context(synth.pack_blob(W), max_slots=2) as ctx:
+        ctx.encode(segs, [0, 1])
+        ids = [ctx.debug_copy(binding.T_CTC_IDS, b, (1500,), np.int32) for b in range(2)]
+        res = ctx.transcribe(segs)
+        for s, r, i, g in zip(segs, ref, ids, res):
+            T = OC.valid_frames(s.audio.size)
+            log(f"ctc-tiny: {s.audio.size} samples, {T} frames, {g['tokens'].size} labels")
+            assert T == (1 if s.audio.size == 1 else 1500)
+            assert g["tokens"].size <= T
+            if np.array_equal(i[:T], np.asarray(r["ids"])):
+                assert g["tokens"].tolist() == r["tokens"]
