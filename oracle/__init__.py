@@ -14,7 +14,7 @@ are independent units, so batching changes speed, not results.
 The paper fixes neither the network nor the front end; both follow the
 public Whisper architecture (pre-LN transformer encoder-decoder, conv stem,
 sinusoidal encoder positions, learned decoder positions, tied output head)
-and its log-mel recipe. Every such reading is listed in the design doc.
+and its log-mel recipe; both sides of every comparison use the same readings.
 
 The CTC variant (oracle/ctc.py) reads the paper's remark on encoder-only
 CTC recognisers as the same encoder with a linear head and greedy best-path
