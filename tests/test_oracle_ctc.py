@@ -89,3 +89,76 @@ def test_ctc_logits_affine_in_encoder_output():
     # a head that copies the first V features of the frame returns them plus the bias
     W2 = {"ctc.w": np.eye(V, d), "ctc.b": W["ctc.b"]}
     assert np.allclose(ctc.ctc_logits(W2, E1), E1[:, :V] + W["ctc.b"])
+
+
+def _label_probs_brute_force(logits):
+    """P(y) for every label sequence y: the sum over all frame paths that
+    collapse to y of the product of per-frame softmax probabilities."""
+    T, V = logits.shape
+    p = np.exp(logits - logits.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    out = {}
+    for path in itertools.product(range(V), repeat=T):
+        y = tuple(ctc.collapse(path))
+        out[y] = out.get(y, 0.0) + float(np.prod([p[t, path[t]] for t in range(T)]))
+    return out
+
+
+def test_prefix_beam_search_unpruned_is_exact_by_brute_force():
+    """With every label a candidate at every frame and a beam wider than the
+    number of prefixes, prefix beam search returns the most probable label
+    sequence (brute force over all frame paths)."""
+    rng = np.random.default_rng(11)
+    for _ in range(25):
+        T, V = int(rng.integers(1, 5)), int(rng.integers(2, 4))
+        logits = rng.normal(size=(T, V)) * 2
+        probs = _label_probs_brute_force(logits)
+        best = max(probs, key=probs.get)
+        labels, _ = ctc.prefix_beam_search(logits, T, beam=10_000, per_frame=V - 1)
+        assert tuple(labels) == best
+
+
+def test_prefix_beam_search_conserves_probability_when_unpruned():
+    """Unpruned, the final prefixes' probabilities sum to one (every path is
+    accounted for exactly once) and each equals its brute-force P(y)."""
+    rng = np.random.default_rng(12)
+    T, V = 4, 3
+    logits = rng.normal(size=(T, V))
+    probs = _label_probs_brute_force(logits)
+    # run the search keeping every prefix, then read the probabilities back
+    beams = [((), 0.0, -np.inf)]
+    import math
+    for t in range(T):
+        lpb, cands = ctc.frame_candidates(logits[t], V - 1)
+        nxt = {}
+        for prefix, pb, pnb in beams:
+            tot = np.logaddexp(pb, pnb)
+            e = nxt.setdefault(prefix, [-np.inf, -np.inf])
+            e[0] = np.logaddexp(e[0], tot + lpb)
+            if prefix:
+                e[1] = np.logaddexp(e[1], pnb + dict(cands)[prefix[-1]])
+            for c, lpc in cands:
+                src = pb if (prefix and c == prefix[-1]) else tot
+                f = nxt.setdefault(prefix + (c,), [-np.inf, -np.inf])
+                f[1] = np.logaddexp(f[1], src + lpc)
+        beams = [(p, e[0], e[1]) for p, e in nxt.items()]
+    got = {p: math.exp(np.logaddexp(pb, pnb)) for p, pb, pnb in beams}
+    assert abs(sum(got.values()) - 1.0) < 1e-12
+    for y, pr in probs.items():
+        assert abs(got.get(y, 0.0) - pr) < 1e-12
+
+
+def test_prefix_beam_search_pruned_properties():
+    """A pruned search returns a valid label sequence, its margin is
+    non-negative, and widening the beam never lowers the returned
+    sequence's exact probability on these cases."""
+    rng = np.random.default_rng(13)
+    for _ in range(20):
+        T, V = 4, 4
+        logits = rng.normal(size=(T, V)) * 2
+        probs = _label_probs_brute_force(logits)
+        l1, m1 = ctc.prefix_beam_search(logits, T, beam=1, per_frame=1)
+        l3, m3 = ctc.prefix_beam_search(logits, T, beam=8, per_frame=3)
+        assert all(1 <= c < V for c in l1 + l3) and m1 >= 0 and m3 >= 0
+        assert probs[tuple(l3)] >= probs[tuple(l1)] - 1e-12
+    assert ctc.prefix_beam_search(np.zeros((0, 3)), 0, 4, 2) == ([], float("inf"))
