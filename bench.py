@@ -189,6 +189,8 @@ def main():
     ap.add_argument("--pad-mode", type=int, default=0, choices=(0, 1),
                     help="0: pad the audio to 30 s, then the front end (default); 1: front end on the "
                          "segment alone, features padded to 3000 frames")
+    ap.add_argument("--ctc-beam", type=int, default=0,
+                    help="CTC workloads: 0 greedy best path, 2..16 prefix beam search with that beam")
     ap.add_argument("--max-new", type=int, default=0,
                     help="profiling runs only: decode this many tokens per segment instead of the workload's")
     a = ap.parse_args()
@@ -209,7 +211,8 @@ def main():
     blob = synth.pack_blob(W)
     dev_audio = [torch.from_numpy(s.audio).to("cuda:0") for s in segs]
     ptrs = [t.data_ptr() for t in dev_audio]
-    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=min(slots, 32), pad_mode=a.pad_mode)
+    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=min(slots, 32), pad_mode=a.pad_mode,
+                          ctc_beam=a.ctc_beam)
     del blob
     audio_s = sum(s.seconds for s in segs)
     torch.cuda.synchronize()
@@ -355,7 +358,7 @@ def bench_ctc(a, ctx, shape, W, segs, slots, ptrs, audio_s, wall, st_timed):
         "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
         "config": {"workload": a.workload, "segments": len(segs), "encode_batch": slots,
                    "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1, "pad_mode": a.pad_mode,
-                   "decoding": "CTC best path"},
+                   "decoding": "CTC best path" if a.ctc_beam < 2 else f"CTC prefix beam search, beam {a.ctc_beam}"},
         "roofline": roof, "encoder": enc, "batcher": batcher,
     }
     if not a.no_cpu_baseline:

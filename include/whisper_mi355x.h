@@ -85,6 +85,10 @@ enum { WHISPER_DTYPE_F32 = 0, WHISPER_DTYPE_BF16 = 1 };
  *                     slots are active; results never depend on it
  *   step_cost_us      dynamic policy: estimated decode step time (0 selects 2000)
  *   max_wait_ms       dynamic policy: longest wait for a fuller refill
+ *   ctc_beam          CTC models only (0 for others): 0 or 1 greedy best-path
+ *                     decoding; 2..16 prefix beam search with that beam and as
+ *                     many candidate labels per frame (the frame's most likely
+ *                     non-blank ids), no language model; n_vocab <= 4096
  */
 typedef struct {
     int32_t n_mels, n_audio_ctx, n_audio_state, n_audio_head, n_audio_layer;
@@ -97,7 +101,8 @@ typedef struct {
     int32_t batch_policy;
     int32_t step_cost_us;
     int32_t max_wait_ms;
-    int32_t reserved[2];
+    int32_t ctc_beam;
+    int32_t reserved[1];
 } whisper_params;
 
 /*

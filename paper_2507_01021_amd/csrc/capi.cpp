@@ -103,6 +103,9 @@ std::string check_params(const whisper_params& p, const whisper_params& blob) {
     if (p.refill_min < 0) return "refill_min must be >= 0";
     if (p.batch_policy < 0 || p.batch_policy > 1) return "batch_policy must be 0 or 1";
     if (p.step_cost_us < 0 || p.max_wait_ms < 0) return "step_cost_us and max_wait_ms must be >= 0";
+    if (p.ctc_beam < 0 || p.ctc_beam > 16) return "ctc_beam must be in 0..16";
+    if (p.ctc_beam > 1 && (p.n_text_layer != 0 || p.n_vocab > 4096))
+        return "ctc_beam >= 2 needs a CTC model with n_vocab <= 4096";
     return "";
 }
 

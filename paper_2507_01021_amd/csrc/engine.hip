@@ -674,6 +674,8 @@ class EngineT final : public Engine {
     float* bctc_ = nullptr;
     float* ctc_logits_ = nullptr;  // [max_encode_batch * 1500][n_vocab]
     int *ctc_ids_ = nullptr, *ctc_tok_ = nullptr, *ctc_cnt_ = nullptr;
+    float *ctc_lpb_ = nullptr, *ctc_clp_ = nullptr;  // beam search: per-frame blank and candidate log-probs
+    int *ctc_cid_ = nullptr, *ctc_bp_ = nullptr;     // candidate ids, backpointers
     static constexpr int MAXC = 4;                                  // chains of a step (hardware queues)
     int chains_ = 2;
     std::map<int, std::array<hipGraphExec_t, MAXC>> step_graphs_;  // per row count: one graph per chain
@@ -869,6 +871,12 @@ class EngineT final : public Engine {
             hipLaunchKernelGGL(ctc_argmax_kernel, dim3((M + 3) / 4), dim3(256), 0, st_, ctc_logits_, V_, M, ctc_ids_);
             hipLaunchKernelGGL(ctc_collapse_kernel, dim3(nb), dim3(1024), 0, st_, ctc_ids_, slot_of_, ctc_tok_,
                                ctc_cnt_);
+            if (P_.ctc_beam >= 2) {  // prefix beam search replaces the greedy labels
+                hipLaunchKernelGGL(ctc_frame_topk_kernel, dim3((M + 3) / 4), dim3(256), 0, st_, ctc_logits_, V_, M,
+                                   P_.ctc_beam, ctc_lpb_, ctc_cid_, ctc_clp_);
+                hipLaunchKernelGGL(ctc_beam_kernel, dim3(nb), dim3(64), 0, st_, ctc_lpb_, ctc_cid_, ctc_clp_, slot_of_,
+                                   P_.ctc_beam, P_.ctc_beam, ctc_bp_, ctc_tok_, ctc_cnt_);
+            }
             prof_end(WHISPER_K_ENC_PASS, st_);
             return;
         }
@@ -1056,6 +1064,12 @@ class EngineT final : public Engine {
             ctc_ids_ = dalloc<int>(EB * N_CTX);
             ctc_tok_ = dalloc<int>(EB * N_CTX);
             ctc_cnt_ = dalloc<int>(EB);
+            if (P_.ctc_beam >= 2) {
+                ctc_lpb_ = dalloc<float>(EB * N_CTX);
+                ctc_cid_ = dalloc<int>(EB * N_CTX * cb::KMAX);
+                ctc_clp_ = dalloc<float>(EB * N_CTX * cb::KMAX);
+                ctc_bp_ = dalloc<int>(EB * N_CTX * cb::KMAX);
+            }
         }
     }
 };

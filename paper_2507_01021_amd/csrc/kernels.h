@@ -1123,6 +1123,223 @@ __global__ __launch_bounds__(1024) void ctc_collapse_kernel(const int* __restric
     if (tid == 0) cnt[b] = wsum[15];
 }
 
+// ------------------------------------------------------------- CTC prefix beam search
+//
+// Decoding variant of the CTC model: prefix beam search without a language
+// model, the frame's candidates pruned to its K most likely non-blank ids.
+namespace cb {
+constexpr int KMAX = 16;           // largest beam (and candidates per frame)
+constexpr int CMAX = KMAX * (1 + KMAX);  // stays + extensions of one frame
+}
+
+// One wave per frame: log-softmax normaliser, the blank's log-probability
+// and the K most likely non-blank ids with theirs (lowest id on ties),
+// written to lpb[f], cid[f][0..K), clp[f][0..K).
+__global__ __launch_bounds__(256) void ctc_frame_topk_kernel(const float* __restrict__ logits, int V, int frames,
+                                                             int K, float* __restrict__ lpb, int* __restrict__ cid,
+                                                             float* __restrict__ clp) {
+    const int f = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (f >= frames) return;
+    const float* row = logits + (long long)f * V;
+    float mx = -INFINITY;
+    for (int v = lane; v < V; v += 64) mx = fmaxf(mx, row[v]);
+    mx = wave_max(mx);
+    float sum = 0.f;
+    for (int v = lane; v < V; v += 64) sum += expf(row[v] - mx);
+    const float lse = mx + logf(wave_sum(sum));
+    if (lane == 0) lpb[f] = row[0] - lse;
+    uint64_t taken = 0;  // bit i: this lane's (i)-th value v = lane + 64 i was chosen (V <= 4096)
+    for (int k = 0; k < K; ++k) {
+        float best = -INFINITY;
+        int bi = V;
+        for (int i = 0, v = lane; v < V; ++i, v += 64) {
+            if (v == 0 || ((taken >> i) & 1)) continue;
+            const float x = row[v];
+            if (x > best) { best = x; bi = v; }
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const float ob = __shfl_xor(best, o, 64);
+            const int oi = __shfl_xor(bi, o, 64);
+            if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+        }
+        if (bi < V && (bi & 63) == lane) taken |= 1ull << (bi >> 6);
+        if (lane == 0) {
+            cid[(long long)f * cb::KMAX + k] = bi < V ? bi : 0;
+            clp[(long long)f * cb::KMAX + k] = bi < V ? best - lse : -INFINITY;
+        }
+    }
+}
+
+__device__ inline float lae_dev(float a, float b) {  // log(exp a + exp b)
+    if (a == -INFINITY) return b;
+    if (b == -INFINITY) return a;
+    const float m = fmaxf(a, b);
+    return m + log1pf(expf(-fabsf(a - b)));
+}
+
+// Prefix identity: a 64-bit hash of the label sequence, extended one label
+// at a time (equal prefixes merge when their hashes are equal).
+__device__ inline uint64_t prefix_hash(uint64_t h, int c) {
+    uint64_t x = (h ^ (uint64_t)(c + 1)) * 0x9E3779B97F4A7C15ull;
+    x ^= x >> 31;
+    x *= 0xBF58476D1CE4E5B9ull;
+    return x ^ (x >> 29);
+}
+
+// One wave per batch entry b over its T[b] frames. Beams: (hash, length,
+// last label, pb, pnb) in LDS; the candidates of a frame are every beam's
+// "stay" (in beam order) then its K extensions (beam by beam, candidate
+// order); an extension equal to a kept prefix merges into that prefix's
+// stay; the B most probable candidates survive (ties: earlier candidate).
+// bp[b][t][j] = (parent beam << 20) | (appended label + 1, 0 for none) of
+// beam j after frame t; the best final beam is traced back into tok[b][.],
+// its length into cnt[b].
+__global__ __launch_bounds__(64) void ctc_beam_kernel(const float* __restrict__ lpb, const int* __restrict__ cid,
+                                                     const float* __restrict__ clp, const int* __restrict__ nframes,
+                                                     int B, int K, int* __restrict__ bp, int* __restrict__ tok,
+                                                     int* __restrict__ cnt) {
+    using namespace cb;
+    __shared__ uint64_t bh[2][KMAX];
+    __shared__ int blen[2][KMAX], blast[2][KMAX];
+    __shared__ float bpb[2][KMAX], bpnb[2][KMAX];
+    __shared__ uint64_t ch[CMAX];
+    __shared__ int clen[CMAX], clast[CMAX], cpar[CMAX], capp[CMAX], cmerge[CMAX];
+    __shared__ float cpb[CMAX], cpnb[CMAX], cscore[CMAX];
+    __shared__ int nbeam;
+    __shared__ float s_lpb[64];           // the candidates of 64 frames, staged per chunk
+    __shared__ int s_id[64][KMAX];
+    __shared__ float s_lp[64][KMAX];
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int T = nframes[b];
+    const long long f0 = (long long)b * N_CTX;
+    int* bpe = bp + (long long)b * N_CTX * KMAX;
+    if (lane == 0) {
+        bh[0][0] = 0x243F6A8885A308D3ull;  // the empty prefix
+        blen[0][0] = 0;
+        blast[0][0] = -1;
+        bpb[0][0] = 0.f;
+        bpnb[0][0] = -INFINITY;
+        nbeam = 1;
+    }
+    __syncthreads();
+    int cur = 0;
+    for (int t = 0; t < T; ++t) {
+        if ((t & 63) == 0) {  // lane l stages frame t + l
+            const int tf = t + lane;
+            if (tf < T) {
+                s_lpb[lane] = lpb[f0 + tf];
+                for (int k = 0; k < K; ++k) {
+                    s_id[lane][k] = cid[(f0 + tf) * KMAX + k];
+                    s_lp[lane][k] = clp[(f0 + tf) * KMAX + k];
+                }
+            }
+            __syncthreads();
+        }
+        const int nb = nbeam, nc = nb * (1 + K);
+        const float lb = s_lpb[t & 63];
+        const int* fid = s_id[t & 63];
+        const float* flp = s_lp[t & 63];
+        for (int j = lane; j < nc; j += 64) {
+            if (j < nb) {  // stay j: through the blank, or repeat of the last label
+                const float tot = lae_dev(bpb[cur][j], bpnb[cur][j]);
+                float rep = -INFINITY;
+                if (blen[cur][j] > 0)
+                    for (int k = 0; k < K; ++k)
+                        if (fid[k] == blast[cur][j]) rep = bpnb[cur][j] + flp[k];
+                ch[j] = bh[cur][j];
+                clen[j] = blen[cur][j];
+                clast[j] = blast[cur][j];
+                cpar[j] = j;
+                capp[j] = 0;
+                cpb[j] = tot + lb;
+                cpnb[j] = rep;
+                cmerge[j] = -1;
+            } else {  // extension of beam i by candidate k
+                const int i = (j - nb) / K, k = (j - nb) - i * K;
+                const int c = fid[k];
+                const bool again = blen[cur][i] > 0 && c == blast[cur][i];
+                const float src = again ? bpb[cur][i] : lae_dev(bpb[cur][i], bpnb[cur][i]);
+                const uint64_t h = prefix_hash(bh[cur][i], c);
+                ch[j] = h;
+                clen[j] = blen[cur][i] + 1;
+                clast[j] = c;
+                cpar[j] = i;
+                capp[j] = c + 1;
+                cpb[j] = -INFINITY;
+                cpnb[j] = src + flp[k];
+                int m = -1;
+                for (int q = 0; q < nb; ++q)
+                    if (bh[cur][q] == h && blen[cur][q] == clen[j]) m = q;
+                cmerge[j] = m;
+            }
+        }
+        __syncthreads();
+        // merge: each kept prefix receives at most one extension equal to it
+        for (int j = lane + nb; j < nc; j += 64) {
+            const int m = cmerge[j];
+            if (m >= 0) {
+                cpnb[m] = lae_dev(cpnb[m], cpnb[j]);
+                cpnb[j] = -INFINITY;
+            }
+        }
+        __syncthreads();
+        for (int j = lane; j < nc; j += 64)
+            cscore[j] = (j >= nb && cmerge[j] >= 0) ? -INFINITY : lae_dev(cpb[j], cpnb[j]);
+        __syncthreads();
+        // the B best candidates, in order (ties: lower candidate index)
+        const int nxt = cur ^ 1;
+        int kept = 0;
+        for (int r = 0; r < B; ++r) {
+            float best = -INFINITY;
+            int bi = CMAX;
+            for (int j = lane; j < nc; j += 64)
+                if (cscore[j] > best || (cscore[j] == best && j < bi && cscore[j] > -INFINITY)) {
+                    best = cscore[j];
+                    bi = j;
+                }
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) {
+                const float ob = __shfl_xor(best, o, 64);
+                const int oi = __shfl_xor(bi, o, 64);
+                if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+            }
+            if (bi >= CMAX || best == -INFINITY) break;
+            if (lane == 0) {
+                bh[nxt][r] = ch[bi];
+                blen[nxt][r] = clen[bi];
+                blast[nxt][r] = clast[bi];
+                bpb[nxt][r] = cpb[bi];
+                bpnb[nxt][r] = cpnb[bi];
+                bpe[(long long)t * KMAX + r] = (cpar[bi] << 20) | capp[bi];
+                cscore[bi] = -INFINITY;
+            }
+            __syncthreads();
+            ++kept;
+        }
+        if (lane == 0) nbeam = kept;
+        __syncthreads();
+        cur = nxt;
+    }
+    if (lane == 0) {  // trace the best final beam back to frame 0
+        int best = 0;
+        float bs = lae_dev(bpb[cur][0], bpnb[cur][0]);
+        for (int j = 1; j < nbeam; ++j) {
+            const float sj = lae_dev(bpb[cur][j], bpnb[cur][j]);
+            if (sj > bs) { bs = sj; best = j; }
+        }
+        const int n = blen[cur][best];
+        int* out = tok + f0;
+        int w = n, beam = best;
+        for (int t = T - 1; t >= 0; --t) {
+            const int e = bpe[(long long)t * KMAX + beam];
+            if ((e & 0xFFFFF) != 0) out[--w] = (e & 0xFFFFF) - 1;
+            beam = e >> 20;
+        }
+        cnt[b] = n;
+    }
+}
+
 // ------------------------------------------------------------- greedy step
 //
 // argmax over the logits in two kernels: (1) grid (chunks, rows), each

@@ -123,3 +123,48 @@ def test_ctc_decoder_calls_refused(tiny):
         ctx.decode_step([0], logits=True)
     with pytest.raises(binding.WhisperError):
         ctx.time_kernel(binding.K_CROSS_ATTN, 1, 1)
+
+
+@pytest.mark.parametrize("beam,scale", [(2, 30.0), (4, 30.0), (8, 30.0), (4, 1.0)])
+def test_ctc_prefix_beam_search_matches_oracle(beam, scale):
+    """ctc_beam >= 2: the GPU's prefix beam search against the oracle's on
+    the fp32 tiny model, with the head's weights scaled by `scale`. With a
+    peaked head (scale 30) the pruning decisions are clear-cut and the labels
+    must be identical wherever the oracle's smallest pruning margin exceeds
+    1e-2 nats. With the plain head many decisions are near ties; the labels
+    must then be identical or the margin must lie within 5e-3 nats, the
+    budget of fp32 scores summed over up to 350 frames."""
+    shape, segs, slots = synth.workload("ctc-tiny-b2")
+    W = synth.make_weights(shape, 0)
+    W.values["ctc.w"] = (W.values["ctc.w"] * np.float32(scale)).astype(np.float32)
+    ref = OC.transcribe_ctc(W, shape, segs, beam=beam)
+    with binding.Context(synth.pack_blob(W), max_slots=2, ctc_beam=beam) as ctx:
+        res = ctx.transcribe(segs)
+        solo = [ctx.transcribe([s])[0] for s in segs]
+    same = 0
+    for s, r, g, g1 in zip(segs, ref, res, solo):
+        eq = g["tokens"].tolist() == r["tokens"]
+        log(f"beam {beam}, scale {scale}, segment {s.segment_id}: {len(r['tokens'])} labels (oracle), "
+            f"{g['tokens'].size} (device), margin {r['margin']:.3g}, identical {eq}")
+        assert np.array_equal(g["tokens"], g1["tokens"])          # batch = solo
+        assert g["status"] == 0 and all(1 <= c < shape.n_vocab for c in g["tokens"])
+        if scale > 1 and r["margin"] > 1e-2:
+            assert eq
+        if not eq:
+            assert r["margin"] < 5e-3
+        same += eq
+    if scale > 1:
+        assert same == len(segs)
+
+
+def test_ctc_beam_base_bf16_runs_and_is_batch_independent():
+    shape = synth.CTC_BASE
+    W = synth.make_weights(shape, 0)
+    segs = synth.uniform_batch(shape, 4, 1500, seed=5)
+    with binding.Context(synth.pack_blob(W), max_slots=4, ctc_beam=4) as ctx:
+        res = ctx.transcribe(segs)
+        solo = [ctx.transcribe([s])[0] for s in segs]
+    for s, g, g1 in zip(segs, res, solo):
+        assert np.array_equal(g["tokens"], g1["tokens"])
+        assert 0 < g["tokens"].size <= OC.valid_frames(s.audio.size)
+        assert all(1 <= c < shape.n_vocab for c in g["tokens"])
