@@ -253,6 +253,10 @@ struct CtcBackend : wmi::BatchBackend {
     std::vector<int> mark_of;
     std::vector<int32_t> tok, cnt;
     double engine_ms = 0.0;
+    struct Pending {
+        int ticket = -1, mark = -1;
+        std::vector<int> idx;
+    } pending;  // the batch encoded last, read once the next one is queued
     void encode(const int* idx, int n, const int*) override {
         const clock::time_point t = clock::now();
         std::vector<wmi::SegmentDesc> d(n);
@@ -260,28 +264,43 @@ struct CtcBackend : wmi::BatchBackend {
             const whisper_segment& s = segs[idx[k]];
             d[k] = wmi::SegmentDesc{s.audio, s.n_samples, s.audio_on_device == 1, nullptr, 0};
         }
-        c->eng->encode_ctc(d.data(), n);
-        const int m = c->eng->mark();
-        tok.resize((size_t)n * 1500);
-        cnt.resize(n);
-        c->eng->read_ctc(n, tok.data(), cnt.data());
-        for (int k = 0; k < n; ++k) {
-            const int i = idx[k];
-            const int32_t k_tok = std::min(cnt[k], segs[i].max_new_tokens);
-            int32_t* dst = token_buf + (*off)[i];
-            std::copy(tok.begin() + (size_t)k * 1500, tok.begin() + (size_t)k * 1500 + k_tok, dst);
-            std::fill(dst + k_tok, dst + segs[i].max_new_tokens, -1);
-            results[i].n_tokens = k_tok;
-            mark_of[i] = m;
-        }
+        int mark = -1;
+        const int ticket = c->eng->encode_ctc(d.data(), n, &mark);
+        deliver();
+        pending.ticket = ticket;
+        pending.mark = mark;
+        pending.idx.assign(idx, idx + n);
         c->stats.encode_passes += 1;
         c->stats.segments_encoded += n;
         c->stats.refill_batches += 1;
         engine_ms += std::chrono::duration<double, std::milli>(clock::now() - t).count();
     }
+    // Reads the pending batch's labels (truncated to max_new_tokens, the rest
+    // of each segment's region set to -1) into token_buf.
+    void deliver() {
+        if (pending.ticket < 0) return;
+        const int n = (int)pending.idx.size();
+        tok.resize((size_t)n * 1500);
+        cnt.resize(n);
+        c->eng->read_ctc(pending.ticket, n, tok.data(), cnt.data());
+        for (int k = 0; k < n; ++k) {
+            const int i = pending.idx[k];
+            const int32_t k_tok = std::min(cnt[k], segs[i].max_new_tokens);
+            int32_t* dst = token_buf + (*off)[i];
+            std::copy(tok.begin() + (size_t)k * 1500, tok.begin() + (size_t)k * 1500 + k_tok, dst);
+            std::fill(dst + k_tok, dst + segs[i].max_new_tokens, -1);
+            results[i].n_tokens = k_tok;
+            mark_of[i] = pending.mark;
+        }
+        pending.ticket = -1;
+    }
     void step(const int*, int) override {}
     void retire(int, int, int, int32_t*) override {}
-    void finish() override {}
+    void finish() override {
+        const clock::time_point t = clock::now();
+        deliver();
+        engine_ms += std::chrono::duration<double, std::milli>(clock::now() - t).count();
+    }
     int64_t now_us() override {
         return std::chrono::duration_cast<std::chrono::microseconds>(clock::now() - t0).count();
     }
@@ -392,7 +411,7 @@ whisper_status whisper_batch_encode(whisper_ctx* ctx, const whisper_segment* seg
             std::vector<wmi::SegmentDesc> d(n);
             for (int i = 0; i < n; ++i)
                 d[i] = wmi::SegmentDesc{segs[i].audio, segs[i].n_samples, segs[i].audio_on_device == 1, nullptr, 0};
-            ctx->eng->encode_ctc(d.data(), n);
+            ctx->eng->encode_ctc(d.data(), n, nullptr);
             ctx->eng->sync();
             ctx->stats.encode_passes += 1;
             ctx->stats.segments_encoded += n;

@@ -51,11 +51,15 @@ class Engine {
     // the decoder depth), between two events on the stream. The slots'
     // caches are read as they are; the attention output buffer is written.
     virtual double time_cross_attn(int n, int reps) = 0;
-    // Encoder-only CTC models: front end, encoder, head and greedy decoding of
-    // n (1..max_encode_batch) segments; read_ctc then copies each entry's
-    // labels (tokens [n][1500]) and their counts, synchronising the stream.
-    virtual void encode_ctc(const SegmentDesc* segs, int n) = 0;
-    virtual void read_ctc(int n, int32_t* tokens, int32_t* counts) = 0;
+    // Encoder-only CTC models: enqueues the front end, encoder, head and
+    // decoding of n (1..max_encode_batch) segments and returns the batch's
+    // ticket (with mark_out: its completion mark). Beam search runs on a
+    // second stream, beside the next batch's encoder. read_ctc(ticket)
+    // waits for that batch and copies each entry's labels (tokens [n][1500])
+    // and their counts; a batch's buffers are reused two batches later, so
+    // read each ticket before encoding the batch after next.
+    virtual int encode_ctc(const SegmentDesc* segs, int n, int* mark_out) = 0;
+    virtual void read_ctc(int ticket, int n, int32_t* tokens, int32_t* counts) = 0;
     // Completion-time marks: mark_reset() starts the clock on the stream,
     // mark() records a point after the work queued so far and returns its
     // index, mark_times_us() waits for the stream and returns every mark's

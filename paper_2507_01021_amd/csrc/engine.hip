@@ -236,6 +236,7 @@ class EngineT final : public Engine {
     ~EngineT() override {
         (void)hipSetDevice(dev_);
         if (st_) (void)hipStreamSynchronize(st_);
+        if (ctc_st_) (void)hipStreamSynchronize(ctc_st_);
         for (auto& pr : prof_)
             for (auto& e : pr.used) { (void)hipEventDestroy(e.first); (void)hipEventDestroy(e.second); }
         for (auto e : event_pool_) (void)hipEventDestroy(e);
@@ -261,6 +262,11 @@ class EngineT final : public Engine {
             if (join_ev_[c]) (void)hipEventDestroy(join_ev_[c]);
             if (cst_[c]) (void)hipStreamDestroy(cst_[c]);
         }
+        for (int q = 0; q < 2; ++q) {
+            if (ctc_head_[q]) (void)hipEventDestroy(ctc_head_[q]);
+            if (ctc_done_[q]) (void)hipEventDestroy(ctc_done_[q]);
+        }
+        if (ctc_st_) (void)hipStreamDestroy(ctc_st_);
         if (own_stream_) (void)hipStreamDestroy(own_stream_);
     }
 
@@ -269,7 +275,10 @@ class EngineT final : public Engine {
         st_ = s ? static_cast<hipStream_t>(s) : own_stream_;
     }
 
-    void sync() override { WMI_HIP(hipStreamSynchronize(st_)); }
+    void sync() override {
+        WMI_HIP(hipStreamSynchronize(st_));
+        if (ctc_st_) WMI_HIP(hipStreamSynchronize(ctc_st_));
+    }
 
     // -------------------------------------------------------------- encode
     void encode(const SegmentDesc* segs, int n, const int* slots, bool sync_) override {
@@ -551,6 +560,7 @@ class EngineT final : public Engine {
     }
     std::vector<double> mark_times_us() override {
         WMI_HIP(hipStreamSynchronize(st_));
+        if (ctc_st_) WMI_HIP(hipStreamSynchronize(ctc_st_));
         std::vector<double> t(marks_.size());
         for (size_t i = 0; i < marks_.size(); ++i) {
             float ms = 0.f;
@@ -568,21 +578,31 @@ class EngineT final : public Engine {
         prof_[k].total_ms = 0.0;
         prof_[k].launches = 0;
     }
-    void encode_ctc(const SegmentDesc* segs, int n) override {
+    int encode_ctc(const SegmentDesc* segs, int n, int* mark_out) override {
         WMI_HIP(hipSetDevice(dev_));
         if (!ctc_) throw ArgError(WHISPER_E_STATE, "not a CTC model");
         if (n < 1 || n > EB_) throw ArgError(WHISPER_E_INVAL, "encode_ctc: 1..max_encode_batch segments");
         const std::vector<int> none(n, 0);
         encode_pass(segs, n, none.data());
         WMI_HIP(hipGetLastError());
+        const int ticket = ctc_ticket_++;
+        if (mark_out) {  // completion: after the batch's decoding, on the stream that ran it
+            hipEvent_t e = get_event();
+            WMI_HIP(hipEventRecord(e, P_.ctc_beam >= 2 ? ctc_st_ : st_));
+            marks_.push_back(e);
+            *mark_out = (int)marks_.size() - 1;
+        }
+        return ticket;
     }
 
-    void read_ctc(int n, int32_t* tokens, int32_t* counts) override {
+    void read_ctc(int ticket, int n, int32_t* tokens, int32_t* counts) override {
         WMI_HIP(hipSetDevice(dev_));
-        if (!ctc_ || n < 1 || n > EB_) throw ArgError(WHISPER_E_INVAL, "read_ctc: 1..max_encode_batch entries of a CTC model");
-        WMI_HIP(hipMemcpyAsync(counts, ctc_cnt_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
-        WMI_HIP(hipMemcpyAsync(tokens, ctc_tok_, (size_t)n * N_CTX * sizeof(int), hipMemcpyDeviceToHost, st_));
-        WMI_HIP(hipStreamSynchronize(st_));
+        if (!ctc_ || n < 1 || n > EB_ || ticket < 0 || ticket < ctc_ticket_ - 2 || ticket >= ctc_ticket_)
+            throw ArgError(WHISPER_E_INVAL, "read_ctc: one of the last two batches of a CTC model, 1..max_encode_batch entries");
+        const int q = ticket & 1;
+        WMI_HIP(hipEventSynchronize(ctc_done_[q]));
+        WMI_HIP(hipMemcpy(counts, ctc_cnt_[q], n * sizeof(int), hipMemcpyDeviceToHost));
+        WMI_HIP(hipMemcpy(tokens, ctc_tok_[q], (size_t)n * N_CTX * sizeof(int), hipMemcpyDeviceToHost));
     }
 
     double time_cross_attn(int n, int reps) override {
@@ -673,9 +693,16 @@ class EngineT final : public Engine {
     T* Wctc_ = nullptr;
     float* bctc_ = nullptr;
     float* ctc_logits_ = nullptr;  // [max_encode_batch * 1500][n_vocab]
-    int *ctc_ids_ = nullptr, *ctc_tok_ = nullptr, *ctc_cnt_ = nullptr;
-    float *ctc_lpb_ = nullptr, *ctc_clp_ = nullptr;  // beam search: per-frame blank and candidate log-probs
-    int *ctc_cid_ = nullptr, *ctc_bp_ = nullptr;     // candidate ids, backpointers
+    int* ctc_ids_ = nullptr;
+    // per ticket parity (two batches in flight): labels and counts; beam
+    // search: frame counts, per-frame blank and candidate log-probs,
+    // candidate ids, backpointers
+    int *ctc_tok_[2] = {}, *ctc_cnt_[2] = {}, *ctc_T_[2] = {};
+    float *ctc_lpb_[2] = {}, *ctc_clp_[2] = {};
+    int *ctc_cid_[2] = {}, *ctc_bp_[2] = {};
+    int ctc_ticket_ = 0;
+    hipStream_t ctc_st_ = nullptr;  // beam search of one batch beside the next batch's encoder
+    hipEvent_t ctc_head_[2] = {}, ctc_done_[2] = {};
     static constexpr int MAXC = 4;                                  // chains of a step (hardware queues)
     int chains_ = 2;
     std::map<int, std::array<hipGraphExec_t, MAXC>> step_graphs_;  // per row count: one graph per chain
@@ -866,16 +893,28 @@ class EngineT final : public Engine {
             gemm(L.W2, 4 * d, 0, hb_, 4 * d, 0, d, M, 4 * d, 1, EpiResid{L.b2, x_, d});
         }
         ln(x_, zb_, lnpg_, lnpb_, M);
-        if (ctc_) {  // CTC head, per-frame argmax, collapse of each entry's frames
+        if (ctc_) {  // CTC head, per-frame argmax, then decoding into the ticket's buffers
+            const int q = ctc_ticket_ & 1;
             gemm(Wctc_, d, 0, zb_, d, 0, V_, M, d, 1, EpiCTC{bctc_, ctc_logits_, V_});
             hipLaunchKernelGGL(ctc_argmax_kernel, dim3((M + 3) / 4), dim3(256), 0, st_, ctc_logits_, V_, M, ctc_ids_);
-            hipLaunchKernelGGL(ctc_collapse_kernel, dim3(nb), dim3(1024), 0, st_, ctc_ids_, slot_of_, ctc_tok_,
-                               ctc_cnt_);
-            if (P_.ctc_beam >= 2) {  // prefix beam search replaces the greedy labels
+            // the batch before last used these buffers: its search must be done
+            WMI_HIP(hipStreamWaitEvent(st_, ctc_done_[q], 0));
+            if (P_.ctc_beam >= 2) {
+                // candidates on this stream; the search itself on the side
+                // stream, where it overlaps the next batch's encoder
                 hipLaunchKernelGGL(ctc_frame_topk_kernel, dim3((M + 3) / 4), dim3(256), 0, st_, ctc_logits_, V_, M,
-                                   P_.ctc_beam, ctc_lpb_, ctc_cid_, ctc_clp_);
-                hipLaunchKernelGGL(ctc_beam_kernel, dim3(nb), dim3(64), 0, st_, ctc_lpb_, ctc_cid_, ctc_clp_, slot_of_,
-                                   P_.ctc_beam, P_.ctc_beam, ctc_bp_, ctc_tok_, ctc_cnt_);
+                                   P_.ctc_beam, ctc_lpb_[q], ctc_cid_[q], ctc_clp_[q]);
+                WMI_HIP(hipMemcpyAsync(ctc_T_[q], slot_of_, nb * sizeof(int), hipMemcpyDeviceToDevice, st_));
+                WMI_HIP(hipEventRecord(ctc_head_[q], st_));
+                WMI_HIP(hipStreamWaitEvent(ctc_st_, ctc_head_[q], 0));
+                hipLaunchKernelGGL(ctc_beam_kernel, dim3(nb), dim3(64), 0, ctc_st_, ctc_lpb_[q], ctc_cid_[q],
+                                   ctc_clp_[q], ctc_T_[q], P_.ctc_beam, P_.ctc_beam, ctc_bp_[q], ctc_tok_[q],
+                                   ctc_cnt_[q]);
+                WMI_HIP(hipEventRecord(ctc_done_[q], ctc_st_));
+            } else {
+                hipLaunchKernelGGL(ctc_collapse_kernel, dim3(nb), dim3(1024), 0, st_, ctc_ids_, slot_of_, ctc_tok_[q],
+                                   ctc_cnt_[q]);
+                WMI_HIP(hipEventRecord(ctc_done_[q], st_));
             }
             prof_end(WHISPER_K_ENC_PASS, st_);
             return;
@@ -1062,13 +1101,20 @@ class EngineT final : public Engine {
         if (ctc_) {
             ctc_logits_ = dalloc<float>(EB * N_CTX * (size_t)V_);
             ctc_ids_ = dalloc<int>(EB * N_CTX);
-            ctc_tok_ = dalloc<int>(EB * N_CTX);
-            ctc_cnt_ = dalloc<int>(EB);
-            if (P_.ctc_beam >= 2) {
-                ctc_lpb_ = dalloc<float>(EB * N_CTX);
-                ctc_cid_ = dalloc<int>(EB * N_CTX * cb::KMAX);
-                ctc_clp_ = dalloc<float>(EB * N_CTX * cb::KMAX);
-                ctc_bp_ = dalloc<int>(EB * N_CTX * cb::KMAX);
+            WMI_HIP(hipStreamCreateWithFlags(&ctc_st_, hipStreamNonBlocking));
+            for (int q = 0; q < 2; ++q) {  // two batches in flight: buffers by ticket parity
+                ctc_tok_[q] = dalloc<int>(EB * N_CTX);
+                ctc_cnt_[q] = dalloc<int>(EB);
+                WMI_HIP(hipEventCreateWithFlags(&ctc_head_[q], hipEventDisableTiming));
+                WMI_HIP(hipEventCreateWithFlags(&ctc_done_[q], hipEventDisableTiming));
+                WMI_HIP(hipEventRecord(ctc_done_[q], st_));
+                if (P_.ctc_beam >= 2) {
+                    ctc_T_[q] = dalloc<int>(EB);
+                    ctc_lpb_[q] = dalloc<float>(EB * N_CTX);
+                    ctc_cid_[q] = dalloc<int>(EB * N_CTX * cb::KMAX);
+                    ctc_clp_[q] = dalloc<float>(EB * N_CTX * cb::KMAX);
+                    ctc_bp_[q] = dalloc<int>(EB * N_CTX * cb::KMAX);
+                }
             }
         }
     }
