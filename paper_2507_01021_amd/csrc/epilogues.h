@@ -7,7 +7,7 @@
 //   Ypad  [nb][3002][128]   normalised log-mel, row 1 + frame, zero rows 0 and 3001
 //   H1pad [nb][3002][d]     first conv output, row 1 + t, zero row 0
 //   x     [nb * 1500][d]    fp32 residual stream
-//   Qh,Kh [nb][H][TQ][64]   per-head queries (scaled by 1/8) and keys
+//   Qh,Kh [nb][H][TQ][64]   per-head queries (scaled by log2(e)/8) and keys
 //   Vt    [nb][H][64][TQ]   per-head values, transposed
 // Decoder caches (slot s, layer l, head h):
 //   self  Kt [l][s][h][64][TS], V [l][s][h][TS][64]
@@ -99,8 +99,10 @@ struct EpiQK {  // A = [Wq; Wk] (2d rows), B = tokens
         const int bseg = m / N_CTX, t = m - bseg * N_CTX;
         if (i < d) {
             const int h = i >> 6, jj = i & 63;
-            st4(q + (((long long)bseg * H + h) * TQ + t) * 64 + jj, (a + p.a.x) * 0.125f, (b + p.a.y) * 0.125f,
-                (c + p.a.z) * 0.125f, (e + p.a.w) * 0.125f);
+            // 1/8 = 1/sqrt(64), and log2(e) so that attention works in base 2
+            constexpr float qs = 0.125f * 1.4426950408889634f;
+            st4(q + (((long long)bseg * H + h) * TQ + t) * 64 + jj, (a + p.a.x) * qs, (b + p.a.y) * qs,
+                (c + p.a.z) * qs, (e + p.a.w) * qs);
         } else {
             const int f = i - d, h = f >> 6, jj = f & 63;
             st4(k + (((long long)bseg * H + h) * TQ + t) * 64 + jj, a, b, c, e);

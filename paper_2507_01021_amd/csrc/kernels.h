@@ -267,10 +267,18 @@ __global__ __launch_bounds__(256, 2) void enc_attn_bf16_kernel(const bf16* __res
     for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int u = 0; u < 4; ++u) o[a][u] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-    float mrun[4], lrun[4];
+    // Queries arrive scaled by log2(e)/8, so scores are in log2 units. Each
+    // query keeps a reference mref (a score it has seen, at most 8 below its
+    // running maximum) and the score MFMAs start from -mref, so they return
+    // s - mref and the weights are plain exp2 of the result, at most 2^8.
+    float mref[4], lrun[4];
+    mfma_f32x4 negm[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) { mrun[u] = -INFINITY; lrun[u] = 0.f; }
-
+    for (int u = 0; u < 4; ++u) {
+        mref[u] = 0.f;
+        lrun[u] = 0.f;
+        negm[u] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+    }
     // staging: thread copies 16-byte chunk (tid & 7) of rows (tid >> 3) and +32
     const int lc = tid & 7, lr = tid >> 3;
     u32x4 rk[2], rv[2];
@@ -298,60 +306,79 @@ __global__ __launch_bounds__(256, 2) void enc_attn_bf16_kernel(const bf16* __res
         if (kt + 1 < ntiles) gload((kt + 1) * ea::KT);
         const unsigned char* tk = lds + (kt & 1) * 2 * ea::TILE;
         const unsigned char* tv = tk + ea::TILE;
-        // S^T = K Q^T : sc[key tile][query tile]
-        mfma_f32x4 sc[4][4];
+        // K fragments (A operand of S^T = K Q^T): key a*16 + fr, dims s*32 + fc*8 .. +7
+        mfma_bf16x8 kf[4][2];
 #pragma unroll
-        for (int a = 0; a < 4; ++a) {
-            const mfma_bf16x8 k0f = *reinterpret_cast<const mfma_bf16x8*>(tk + swz(a * 16 + fr, fc));
-            const mfma_bf16x8 k1f = *reinterpret_cast<const mfma_bf16x8*>(tk + swz(a * 16 + fr, 4 + fc));
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                mfma_f32x4 t = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
-                t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[u][0], t, 0, 0, 0);
-                sc[a][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[u][1], t, 0, 0, 0);
-            }
-        }
-        // mask keys beyond the window (last tile only)
+            for (int s = 0; s < 2; ++s)
+                kf[a][s] = *reinterpret_cast<const mfma_bf16x8*>(tk + swz(a * 16 + fr, 4 * s + fc));
         const int kbase = kt * ea::KT;
-        if (kbase + ea::KT > N_CTX) {
+        const bool tail = kbase + ea::KT > N_CTX;
+        // scores of query tile u relative to its mref: sc[key tile]; keys
+        // beyond the window (last tile only) get -inf
+        auto scores = [&](int u, mfma_f32x4 (&sc)[4]) {
 #pragma unroll
-            for (int a = 0; a < 4; ++a)
+            for (int a = 0; a < 4; ++a) {
+                const mfma_f32x4 t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[a][0], qf[u][0], negm[u], 0, 0, 0);
+                sc[a] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[a][1], qf[u][1], t, 0, 0, 0);
+            }
+            if (tail) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (kbase + a * 16 + fc * 4 + r >= N_CTX)
+                for (int a = 0; a < 4; ++a)
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) sc[a][u][r] = -INFINITY;
-        }
-        // online softmax per query column (log2 domain)
+                    for (int r = 0; r < 4; ++r)
+                        if (kbase + a * 16 + fc * 4 + r >= N_CTX) sc[a][r] = -INFINITY;
+            }
+        };
+        // Software pipeline over the 4 query tiles: the softmax of tile u
+        // runs while the score MFMAs of tile u+1 execute, so the vector ALU
+        // and the matrix cores work at the same time.
+        mfma_f32x4 scur[4], snext[4];
         mfma_bf16x8 pf[4][2];
+        scores(0, scur);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             float mx = -INFINITY;
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[a][u][r]);
+                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, scur[a][r]);
             mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
             mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float mnew = fmaxf(mrun[u], mx * LOG2E);
-            const float alpha = exp2_softmax(mrun[u] - mnew);
-            mrun[u] = mnew;
+            // The first tile sets mref to its maximum; later tiles move it
+            // only when their maximum is more than 8 above it, and then scale
+            // the sums so far by 2^-(the move).
+            if (kt == 0 || __any(mx > 8.f)) {
+                const float delta = (kt == 0 || mx > 8.f) ? mx : 0.f;
+#pragma unroll
+                for (int a = 0; a < 4; ++a)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) scur[a][r] -= delta;
+                mref[u] += delta;
+                negm[u] = mfma_f32x4{-mref[u], -mref[u], -mref[u], -mref[u]};
+                if (kt > 0) {
+                    const float alpha = exp2_softmax(-delta);
+                    lrun[u] *= alpha;
+#pragma unroll
+                    for (int a = 0; a < 4; ++a)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) o[a][u][r] *= alpha;
+                }
+            }
+            if (u < 3) scores(u + 1, snext);
             float ls = 0.f;
             float pv[4][4];
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    pv[a][r] = exp2_softmax(fmaf(sc[a][u][r], LOG2E, -mnew));
+                    pv[a][r] = exp2_softmax(scur[a][r]);
                     ls += pv[a][r];
                 }
             ls += __shfl_xor(ls, 16, 64);
             ls += __shfl_xor(ls, 32, 64);
-            lrun[u] = lrun[u] * alpha + ls;
-#pragma unroll
-            for (int a = 0; a < 4; ++a)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) o[a][u][r] *= alpha;
+            lrun[u] += ls;
             // P operand for key half s: keys s*32 + fc*4 + {0..3} and s*32 + 16 + fc*4 + {0..3}
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
@@ -363,6 +390,8 @@ __global__ __launch_bounds__(256, 2) void enc_attn_bf16_kernel(const bf16* __res
                 }
                 pf[u][s] = p;
             }
+#pragma unroll
+            for (int a = 0; a < 4; ++a) scur[a] = snext[a];
         }
         // O^T += V^T P^T
 #pragma unroll
@@ -423,7 +452,6 @@ __global__ __launch_bounds__(64) void enc_attn_f32_kernel(const float* __restric
             float s = 0.f;
 #pragma unroll
             for (int j = 0; j < 64; ++j) s = fmaf(qv[j], ks[kk][j], s);
-            s *= LOG2E;
             const float mnew = fmaxf(m, s);
             const float alpha = exp2_softmax(m - mnew), p = exp2_softmax(s - mnew);
             l = l * alpha + p;
