@@ -189,6 +189,9 @@ def main():
     ap.add_argument("--pad-mode", type=int, default=0, choices=(0, 1),
                     help="0: pad the audio to 30 s, then the front end (default); 1: front end on the "
                          "segment alone, features padded to 3000 frames")
+    ap.add_argument("--prefill", type=int, default=0, choices=(0, 1),
+                    help="decoder workloads: 1 runs each segment's prompt through the decoder in one pass at "
+                         "encode time instead of one position per decode step")
     ap.add_argument("--ctc-beam", type=int, default=0,
                     help="CTC workloads: 0 greedy best path, 2..16 prefix beam search with that beam")
     ap.add_argument("--max-new", type=int, default=0,
@@ -212,7 +215,7 @@ def main():
     dev_audio = [torch.from_numpy(s.audio).to("cuda:0") for s in segs]
     ptrs = [t.data_ptr() for t in dev_audio]
     ctx = binding.Context(blob, max_slots=slots, max_encode_batch=min(slots, 32), pad_mode=a.pad_mode,
-                          ctc_beam=a.ctc_beam)
+                          ctc_beam=a.ctc_beam, prefill=a.prefill if shape.n_dec else 0)
     del blob
     audio_s = sum(s.seconds for s in segs)
     torch.cuda.synchronize()
@@ -308,7 +311,7 @@ def main():
         "config": {"workload": a.workload, "segments": len(segs), "slots": slots,
                    "new_tokens": [int(min(s.max_new_tokens for s in segs)), int(max(s.max_new_tokens for s in segs))],
                    "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1,
-                   "pad_mode": a.pad_mode},
+                   "pad_mode": a.pad_mode, "prefill": a.prefill},
         "roofline": roof, "encoder": enc, "decode": dec, "batcher": batcher,
     }
     if not a.no_cpu_baseline:

@@ -89,6 +89,13 @@ enum { WHISPER_DTYPE_F32 = 0, WHISPER_DTYPE_BF16 = 1 };
  *                     decoding; 2..16 prefix beam search with that beam and as
  *                     many candidate labels per frame (the frame's most likely
  *                     non-blank ids), no language model; n_vocab <= 4096
+ *   prefill           decoder models: 0 feeds the prompt one position per
+ *                     decode step (a segment's first n_prompt - 1 steps
+ *                     return no token); 1 runs positions 0..n_prompt-2 of
+ *                     every encoded segment through the decoder in one pass
+ *                     at encode time, so its first decode step returns its
+ *                     first token. The tokens are the same either way.
+ *                     CTC models: 0
  */
 typedef struct {
     int32_t n_mels, n_audio_ctx, n_audio_state, n_audio_head, n_audio_layer;
@@ -102,7 +109,7 @@ typedef struct {
     int32_t step_cost_us;
     int32_t max_wait_ms;
     int32_t ctc_beam;
-    int32_t reserved[1];
+    int32_t prefill;
 } whisper_params;
 
 /*
@@ -208,8 +215,10 @@ whisper_status whisper_ctx_set_stream(whisper_ctx* ctx, void* hip_stream);
  * segs[i]; host array of n distinct indices in [0, max_slots)): log-mel
  * front end, conv stem, encoder, and the cross-attention keys and values of
  * every decoder layer, written into each slot's cache. The slot's
- * self-attention cache is reset and its prompt seated; the slot is then
- * active. n = 0 is a no-op. Errors: E_INVAL (bad segment or slot), E_STATE
+ * self-attention cache is reset and its prompt seated (prefill = 1: prompt
+ * positions 0..n_prompt-2 also run through the decoder, filling the cache,
+ * so the first decode step is at the last prompt position); the slot is
+ * then active. n = 0 is a no-op. Errors: E_INVAL (bad segment or slot), E_STATE
  * (a slot is active), E_CAPACITY (slot >= max_slots). Section 2.3, Listing 1
  * (features, pad to 30 s, stack, encode).
  */
@@ -224,6 +233,7 @@ whisper_status whisper_batch_encode(whisper_ctx* ctx, const whisper_segment* seg
  *               argmax; else forced[i] (host) replaces it (teacher forcing)
  *   out_tokens  NULL or n int32 (host): the argmax of this step (lowest id on
  *               ties), or -1 while the slot is still inside its prompt
+ *               (never with prefill = 1)
  *   out_logits  NULL or n * n_vocab fp32 (host): this step's logits
  * A slot whose generated count reaches max_new_tokens becomes idle; its
  * tokens stay readable with whisper_slot_tokens until it is encoded again.

@@ -32,7 +32,7 @@ class whisper_params(C.Structure):
         "n_mels", "n_audio_ctx", "n_audio_state", "n_audio_head", "n_audio_layer",
         "n_vocab", "n_text_ctx", "n_text_state", "n_text_head", "n_text_layer",
         "dtype", "max_slots", "max_encode_batch", "pad_mode", "refill_min", "batch_policy",
-        "step_cost_us", "max_wait_ms", "ctc_beam")] + [("reserved", C.c_int32 * 1)]
+        "step_cost_us", "max_wait_ms", "ctc_beam", "prefill")]
 
 
 class whisper_segment(C.Structure):
@@ -152,13 +152,13 @@ class Context:
 
     def __init__(self, blob: np.ndarray, max_slots: int = 32, max_encode_batch: int = 0,
                  pad_mode: int = 0, refill_min: int = 0, device: int = 0, batch_policy: int = 0,
-                 step_cost_us: int = 0, max_wait_ms: int = 0, ctc_beam: int = 0):
+                 step_cost_us: int = 0, max_wait_ms: int = 0, ctc_beam: int = 0, prefill: int = 0):
         lib = load()
         p = params_from_blob(blob)
         p.max_slots, p.max_encode_batch, p.pad_mode, p.refill_min = (
             max_slots, max_encode_batch, pad_mode, refill_min)
         p.batch_policy, p.step_cost_us, p.max_wait_ms = batch_policy, step_cost_us, max_wait_ms
-        p.ctc_beam = ctc_beam
+        p.ctc_beam, p.prefill = ctc_beam, prefill
         self.params = p
         h = C.c_void_p()
         _check(lib.whisper_ctx_create(C.byref(p), blob.ctypes.data, blob.nbytes, device, C.byref(h)))

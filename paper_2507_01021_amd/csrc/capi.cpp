@@ -104,6 +104,8 @@ std::string check_params(const whisper_params& p, const whisper_params& blob) {
     if (p.batch_policy < 0 || p.batch_policy > 1) return "batch_policy must be 0 or 1";
     if (p.step_cost_us < 0 || p.max_wait_ms < 0) return "step_cost_us and max_wait_ms must be >= 0";
     if (p.ctc_beam < 0 || p.ctc_beam > 16) return "ctc_beam must be in 0..16";
+    if (p.prefill != 0 && p.prefill != 1) return "prefill must be 0 or 1";
+    if (p.prefill != 0 && p.n_text_layer == 0) return "prefill needs a decoder model";
     if (p.ctc_beam > 1 && (p.n_text_layer != 0 || p.n_vocab > 4096))
         return "ctc_beam >= 2 needs a CTC model with n_vocab <= 4096";
     return "";
@@ -137,7 +139,7 @@ struct EngineBackend : wmi::BatchBackend {
         for (int k = 0; k < n; ++k) {
             const whisper_segment& s = segs[idx[k]];
             descs[k] = wmi::SegmentDesc{s.audio, s.n_samples, s.audio_on_device == 1, s.prompt, s.n_prompt};
-            steps[slots[k]] = 0;
+            steps[slots[k]] = c->p.prefill ? s.n_prompt - 1 : 0;  // prefilled prompt positions
         }
         c->eng->encode(descs.data(), n, slots, realtime);
         c->stats.encode_passes += (n + c->p.max_encode_batch - 1) / c->p.max_encode_batch;
@@ -442,7 +444,7 @@ whisper_status whisper_batch_encode(whisper_ctx* ctx, const whisper_segment* seg
             s.active = true;
             s.n_prompt = segs[i].n_prompt;
             s.max_new = segs[i].max_new_tokens;
-            s.steps = 0;
+            s.steps = ctx->p.prefill ? segs[i].n_prompt - 1 : 0;  // prefilled prompt positions
             s.generated = 0;
         }
         return WHISPER_OK;
@@ -555,8 +557,9 @@ whisper_status whisper_batch_serve(whisper_ctx* ctx, const whisper_segment* segs
         if (!bad.empty()) return fail(ctx, WHISPER_E_INVAL, bad);
         if (realtime && segs[i].arrival_us < 0)
             return fail(ctx, WHISPER_E_INVAL, "segment " + std::to_string(i) + ": arrival_us must be >= 0");
-        q[i] = wmi::QueuedSegment{segs[i].arrival_us, segs[i].user_id, segs[i].segment_id, segs[i].n_prompt,
-                                  segs[i].max_new_tokens};
+        // with prefill, a segment's decode steps are its max_new_tokens alone
+        q[i] = wmi::QueuedSegment{segs[i].arrival_us, segs[i].user_id, segs[i].segment_id,
+                                  ctx->p.prefill ? 1 : segs[i].n_prompt, segs[i].max_new_tokens};
     }
     int64_t total = 0;
     const std::vector<int64_t> off = offsets_of(q, &total);

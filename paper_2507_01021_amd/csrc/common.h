@@ -111,10 +111,10 @@ __device__ inline float erf_as(float z) {
 // GELU, erf form: x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)).
 __device__ inline float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f)); }
 
-// 2^x for softmax weights (x <= 0, or -inf for masked terms): the hardware
-// exponential alone, without the library wrapper's rescaling of results
-// below the normal range (such weights are negligible next to the row
-// maximum's weight of 1).
+// 2^x for softmax weights (x at most a few units above 0, or -inf for
+// masked terms): the hardware exponential alone, without the library
+// wrapper's rescaling of results below the normal range (such weights are
+// negligible next to the row maximum's weight of at least 1).
 __device__ inline float exp2_softmax(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ inline float wave_sum(float v) {

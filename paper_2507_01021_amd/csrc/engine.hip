@@ -216,6 +216,7 @@ class EngineT final : public Engine {
         V_ = p.n_vocab; nm_ = p.n_mels; S_ = p.max_slots;
         EB_ = p.max_encode_batch;
         ctc_ = Ld_ == 0;
+        prefill_ = !ctc_ && p.prefill != 0;
         WMI_HIP(hipSetDevice(dev_));
         WMI_HIP(hipStreamCreateWithFlags(&own_stream_, hipStreamNonBlocking));
         for (int c = 1; c < MAXC; ++c) {
@@ -361,50 +362,104 @@ class EngineT final : public Engine {
         return ge;
     }
 
+    // Device buffers of a set of decoder rows: the slot (and, for prefill
+    // rows, the position) of each row, the activations and the split-K
+    // partial sums.
+    struct RowBufs {
+        const int* list;
+        const int* rowpos;  // null: each row is at its slot's current position
+        float* dx;
+        T* dz;
+        T* dq;
+        T* datt;
+        T* dh;
+        int* rowlen;
+        float* pbuf;
+    };
+
+    // Embedding and every decoder layer for n rows; leaves the final layer
+    // norm of each row in b.dz.
+    void decoder_layers(const RowBufs& b, int n, hipStream_t s) {
+        const int d = d_;
+        const int ks1 = split_k(d), ks4 = split_k(4 * d);
+        WMI_SWITCH_E(d, hipLaunchKernelGGL((embed_ln_kernel<T, E>), dim3(n), dim3(64), 0, s, tok_emb_, pos_emb_,
+                                           b.list, pos_, b.rowpos, seq_, b.dx, b.dz, dec_[0].ln1g, dec_[0].ln1b));
+        for (int l = 0; l < Ld_; ++l) {
+            const DecLayerW<T>& L = dec_[l];
+            const long long sl = (long long)l * S_ * H_ * 64;
+            proj(L.Wqkv, 3 * d, b.dz, n, d, 1,
+                 EpiDecQKV<T>{L.bq, L.bv, b.dq, kts_ + sl * TS, vs_ + sl * TS, b.list, pos_, b.rowpos, b.rowlen, d,
+                              H_},
+                 s);
+            DecAttnArgs sa{b.dq, kts_ + sl * TS, vs_ + sl * TS, b.datt, b.list, b.rowlen, TS, H_, d};
+            prof_begin(WHISPER_K_SELF_ATTN, s);
+            hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, s, sa);
+            prof_end(WHISPER_K_SELF_ATTN, s);
+            self_out_cross_q(L, n, b.datt, b.dq, b.dx, b.dz, b.pbuf, s);
+            DecAttnArgs ca{b.dq, ktc_ + sl * TC, vc_ + sl * TC, b.datt, b.list, nullptr, TC, H_, d};
+            prof_begin(WHISPER_K_CROSS_ATTN, s);
+            hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, s, ca);
+            prof_end(WHISPER_K_CROSS_ATTN, s);
+            proj_resid(L.Wco, b.datt, n, d, ks1, L.cbo, L.ln3g, L.ln3b, b.pbuf, b.dx, b.dz, s);
+            proj(L.W1, 4 * d, b.dz, n, d, 1, EpiGelu<T, true>{L.b1, b.dh, 4 * d}, s);
+            const bool last = l + 1 == Ld_;
+            proj_resid(L.W2, b.dh, n, 4 * d, ks4, L.b2, last ? lnfg_ : dec_[l + 1].ln1g,
+                       last ? lnfb_ : dec_[l + 1].ln1b, b.pbuf, b.dx, b.dz, s);
+        }
+    }
+
     // The kernels of one decode step for rows r0 .. r0+n-1 of the slot list,
     // on stream s, with chain c's split-K partial buffer. r0 is a multiple
     // of 16, so the fragment-major activations of these rows start at
     // element r0 * K.
     void launch_rows(int r0, int n, bool forced, hipStream_t s, int c) {
         const int d = d_;
-        const int ks1 = split_k(d), ks4 = split_k(4 * d);
+        const RowBufs b{list_ + r0,
+                        nullptr,
+                        dx_ + (size_t)r0 * d,
+                        dz_ + (size_t)r0 * d,
+                        dq_ + (size_t)r0 * d,
+                        datt_ + (size_t)r0 * d,
+                        dh_ + (size_t)r0 * 4 * d,
+                        rowlen_ + r0,
+                        gpart_ + (size_t)c * 4 * S_ * d};
+        decoder_layers(b, n, s);
         const int* list = list_ + r0;
-        T* dz = dz_ + (size_t)r0 * d;
-        T* dq = dq_ + (size_t)r0 * d;
-        T* datt = datt_ + (size_t)r0 * d;
-        T* dh = dh_ + (size_t)r0 * 4 * d;
-        float* dx = dx_ + (size_t)r0 * d;
-        int* rowlen = rowlen_ + r0;
-        float* pbuf = gpart_ + (size_t)c * 4 * S_ * d;
-        WMI_SWITCH_E(d, hipLaunchKernelGGL((embed_ln_kernel<T, E>), dim3(n), dim3(64), 0, s, tok_emb_, pos_emb_,
-                                           list, pos_, seq_, dx, dz, dec_[0].ln1g, dec_[0].ln1b));
-        for (int l = 0; l < Ld_; ++l) {
-            const DecLayerW<T>& L = dec_[l];
-            const long long sl = (long long)l * S_ * H_ * 64;
-            proj(L.Wqkv, 3 * d, dz, n, d, 1,
-                 EpiDecQKV<T>{L.bq, L.bv, dq, kts_ + sl * TS, vs_ + sl * TS, list, pos_, rowlen, d, H_}, s);
-            DecAttnArgs sa{dq, kts_ + sl * TS, vs_ + sl * TS, datt, list, rowlen, TS, H_, d};
-            prof_begin(WHISPER_K_SELF_ATTN, s);
-            hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, s, sa);
-            prof_end(WHISPER_K_SELF_ATTN, s);
-            self_out_cross_q(L, n, datt, dq, dx, dz, pbuf, s);
-            DecAttnArgs ca{dq, ktc_ + sl * TC, vc_ + sl * TC, datt, list, nullptr, TC, H_, d};
-            prof_begin(WHISPER_K_CROSS_ATTN, s);
-            hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, s, ca);
-            prof_end(WHISPER_K_CROSS_ATTN, s);
-            proj_resid(L.Wco, datt, n, d, ks1, L.cbo, L.ln3g, L.ln3b, pbuf, dx, dz, s);
-            proj(L.W1, 4 * d, dz, n, d, 1, EpiGelu<T, true>{L.b1, dh, 4 * d}, s);
-            const bool last = l + 1 == Ld_;
-            proj_resid(L.W2, dh, n, 4 * d, ks4, L.b2, last ? lnfg_ : dec_[l + 1].ln1g,
-                       last ? lnfb_ : dec_[l + 1].ln1b, pbuf, dx, dz, s);
-        }
         float* logits = logits_ + (size_t)r0 * V_;
         unsigned long long* best = best_ + r0;
-        proj(tok_emb_, V_, dz, n, d, 1, EpiLogits{logits, V_}, s);
+        proj(tok_emb_, V_, b.dz, n, d, 1, EpiLogits{logits, V_}, s);
         const TokenFilter tf{use_never_ ? never_mask_ : nullptr, use_first_ ? first_mask_ : nullptr, list, pos_, npr_};
         hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, s, logits, V_, best, tf);
         hipLaunchKernelGGL(argmax_step_kernel, dim3((n + 63) / 64), dim3(64), 0, s, best, n, list, pos_, npr_, seq_,
                            gen_, forced ? forced_ + r0 : nullptr, outtok_ + r0, eot_, stop_at_);
+    }
+
+    // Prompt prefill of one encoder pass (prefill_ on): every seated slot's
+    // positions 0 .. n_prompt - 2 run through the decoder layers as rows of
+    // their own (no output head), writing the self-attention caches. Rows
+    // are ordered by position, so a chunk of PF_ROWS rows never needs a
+    // position of a later chunk; within a chunk, each layer appends all keys
+    // and values before its attention reads them.
+    void prefill_pass(const SegmentDesc* segs, int nb, const int* slots) {
+        std::vector<int> rows;  // PF list block, then the position block
+        int maxp = 0;
+        for (int i = 0; i < nb; ++i) maxp = std::max(maxp, segs[i].n_prompt - 1);
+        std::vector<int> rl, rp;
+        for (int p = 0; p < maxp; ++p)
+            for (int i = 0; i < nb; ++i)
+                if (p < segs[i].n_prompt - 1) { rl.push_back(slots[i]); rp.push_back(p); }
+        const int R = (int)rl.size();
+        if (R == 0) return;
+        rows.resize(2 * (size_t)pf_cap_);
+        for (int c0 = 0; c0 < R; c0 += pf_cap_) {
+            const int n = std::min(pf_cap_, R - c0);
+            std::copy(rl.begin() + c0, rl.begin() + c0 + n, rows.begin());
+            std::copy(rp.begin() + c0, rp.begin() + c0 + n, rows.begin() + pf_cap_);
+            upload(3, pf_list_, rows.data(), rows.size() * sizeof(int));
+            const RowBufs b{pf_list_, pf_list_ + pf_cap_, pf_dx_, pf_dz_, pf_dq_, pf_datt_, pf_dh_, pf_rowlen_,
+                            pf_part_};
+            decoder_layers(b, n, st_);
+        }
     }
 
     // Self-attention output projection (x += W_o att + b_o) and the
@@ -670,7 +725,7 @@ class EngineT final : public Engine {
     std::vector<DecLayerW<T>> dec_;
     float *basis_, *melfb_, *pe_;
     // encoder workspace
-    float *stage_audio_, *xpad_, *power_, *logmel_, *x_;
+    float *stage_audio_, *xpad_, *power_, *logmel_, *melmax_, *x_;
     SegSrc* segsrc_;
     int *nvalid_, *slot_of_, *seat_np_, *seat_prompts_;
     T *ypad_, *h1_, *zb_, *qh_, *kh_, *vt_, *ob_, *hb_;
@@ -689,6 +744,13 @@ class EngineT final : public Engine {
     unsigned long long* best_;
     std::vector<int> list_host_;
     bool graphs_ = true, split_ = true, fused_ln_ = true;
+    // prompt prefill: rows per chunk (the skinny projections take up to 128)
+    // and the chunk's buffers; the list block is followed by the positions
+    bool prefill_ = false;
+    int pf_cap_ = 0;
+    int *pf_list_ = nullptr, *pf_rowlen_ = nullptr;
+    float *pf_dx_ = nullptr, *pf_part_ = nullptr;
+    T *pf_dz_ = nullptr, *pf_dq_ = nullptr, *pf_datt_ = nullptr, *pf_dh_ = nullptr;
     bool ctc_ = false;  // encoder-only CTC model (no decoder layers)
     T* Wctc_ = nullptr;
     float* bctc_ = nullptr;
@@ -709,7 +771,7 @@ class EngineT final : public Engine {
     hipStream_t cst_[MAXC] = {};                                   // streams of chains 1.. (chain 0: st_)
     hipEvent_t fork_ev_ = nullptr, join_ev_[MAXC] = {};
     // host staging
-    Stage stage_[3];
+    Stage stage_[4];
     int32_t* tokpin_ = nullptr;
     size_t tokpin_cap_ = 0, tokpin_used_ = 0;
     std::vector<PendingRead> pending_;
@@ -868,7 +930,8 @@ class EngineT final : public Engine {
                            P_.pad_mode);
         gemm_simt(basis_, 400, 0, xpad_, 160, 480400, 404, 3000, 400, nb, EpiPower{power_}, st_);
         gemm_simt(melfb_, 201, 0, power_, 201, 0, nm_, nb * 3000, 201, 1, EpiLogMel{logmel_, nm_}, st_);
-        hipLaunchKernelGGL(mel_norm_kernel<T>, dim3(nb), dim3(1024), 0, st_, logmel_, ypad_, nvalid_, nm_);
+        hipLaunchKernelGGL(mel_max_kernel, dim3(MEL_CHUNKS, nb), dim3(256), 0, st_, logmel_, nvalid_, nm_, melmax_);
+        hipLaunchKernelGGL(mel_norm_kernel<T>, dim3(64, nb), dim3(256), 0, st_, logmel_, ypad_, nvalid_, nm_, melmax_);
         prof_end(WHISPER_K_FRONT_END, st_);
         gemm(W1r_, 3 * CP, 0, ypad_, CP, 3002LL * CP, d, 3000, 3 * CP, nb, EpiConv1<T>{cb1_, h1_, d});
         gemm(W2r_, 3 * d, 0, h1_, 2 * d, 3002LL * d, d, N_CTX, 3 * d, nb, EpiConv2{cb2_, pe_, x_, d});
@@ -922,8 +985,9 @@ class EngineT final : public Engine {
         gemm(zb_, d, 0, WcK_, d, 0, M, Ld_ * d, d, 1, EpiCrossK<T>{ktc_, slot_of_, d, H_, S_});
         gemm(WcV_, d, 0, zb_, d, 0, Ld_ * d, M, d, 1, EpiCrossV<T>{bcV_, vc_, slot_of_, d, H_, S_});
         hipLaunchKernelGGL(seat_kernel, dim3(nb), dim3(256), 0, st_, slot_of_, seat_np_, seat_prompts_, seq_, pos_, npr_,
-                           stop_at_);
+                           stop_at_, prefill_ ? 1 : 0);
         prof_end(WHISPER_K_ENC_PASS, st_);
+        if (prefill_) prefill_pass(segs, nb, slots);
     }
 
     // -------------------------------------------------------------- setup
@@ -1064,6 +1128,7 @@ class EngineT final : public Engine {
         xpad_ = dalloc<float>(EB * 480400);
         power_ = dalloc<float>(EB * 3000 * 201);
         logmel_ = dalloc<float>(EB * 3000 * nm_);
+        melmax_ = dalloc<float>(EB * MEL_CHUNKS);
         ypad_ = dalloc<T>(EB * 3002 * CP);
         h1_ = dalloc<T>(EB * 3002 * d);
         x_ = dalloc<float>(EB * N_CTX * d);
@@ -1098,6 +1163,17 @@ class EngineT final : public Engine {
         logits_ = dalloc<float>(S * (size_t)V_);
         gpart_ = dalloc<float>((size_t)MAXC * 4 * S * d);  // split-K partials [chain][4][rows][d]
         best_ = dalloc<unsigned long long>(S);
+        if (prefill_) {
+            pf_cap_ = 128;
+            pf_list_ = dalloc<int>(2 * pf_cap_);
+            pf_rowlen_ = dalloc<int>(pf_cap_);
+            pf_dx_ = dalloc<float>((size_t)pf_cap_ * d);
+            pf_dz_ = dalloc<T>((size_t)pf_cap_ * d);
+            pf_dq_ = dalloc<T>((size_t)pf_cap_ * d);
+            pf_datt_ = dalloc<T>((size_t)pf_cap_ * d);
+            pf_dh_ = dalloc<T>((size_t)pf_cap_ * 4 * d);
+            pf_part_ = dalloc<float>((size_t)4 * pf_cap_ * d);
+        }
         if (ctc_) {
             ctc_logits_ = dalloc<float>(EB * N_CTX * (size_t)V_);
             ctc_ids_ = dalloc<int>(EB * N_CTX);

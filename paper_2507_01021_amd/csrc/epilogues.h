@@ -186,7 +186,8 @@ struct EpiCrossV {  // A = [Wv of every layer], B = encoder output
     }
 };
 
-// Decoder: A = [Wq; Wk; Wv] of one layer, B = normalised rows (row r -> slot list[r]).
+// Decoder: A = [Wq; Wk; Wv] of one layer, B = normalised rows (row r -> slot
+// list[r] at position rowpos[r], or at pos[list[r]] when rowpos is null).
 // Queries go to q (scaled by 1/8); this position's key and value are appended
 // to the slot's self-attention cache, and rowlen[r] = position + 1 (the
 // number of cached positions the row attends to).
@@ -199,6 +200,7 @@ struct EpiDecQKV {
     T* v;   // self V cache of this layer: [S][H][TS][64]
     const int* list;
     const int* pos;
+    const int* rowpos;
     int* rowlen;
     int d, H;
     __device__ EpiPre pre(int i, int r, int) const {
@@ -206,7 +208,7 @@ struct EpiDecQKV {
         if (i < d) {
             p.a = ld4(bq + i);
         } else {
-            p.s = pos[list[r]];
+            p.s = rowpos ? rowpos[r] : pos[list[r]];
             if (i >= 2 * d) p.a = ld4(bv + (i - 2 * d));
         }
         return p;

@@ -42,31 +42,45 @@ __global__ void prep_audio_kernel(const SegSrc* __restrict__ src, float* __restr
     xpad[(long long)z * 480400 + i] = s < n ? a[s] : 0.f;
 }
 
-// One workgroup per segment: max over valid frames of the log-mel, clamp to
-// max - 8, (L + 4) / 4, zero the frames beyond the segment in pad mode 1.
-// Writes fp32 in place (frame-major [3000][n_mels]) and the conv input
-// Ypad[z][1 + f][c] in T.
-template <class T>
-__global__ __launch_bounds__(1024) void mel_norm_kernel(float* __restrict__ logmel, T* __restrict__ ypad,
-                                                        const int* __restrict__ nvalid, int n_mels) {
-    const int z = blockIdx.x;
-    float* L = logmel + (long long)z * 3000 * n_mels;
+// Log-mel normalisation in two launches over many workgroups: the max over
+// each segment's valid frames (MEL_CHUNKS partial maxima per segment, no
+// atomics), then clamp to max - 8, (L + 4) / 4, zero the frames beyond the
+// segment (pad mode 1). Writes fp32 in place (frame-major [3000][n_mels])
+// and the conv input Ypad[z][1 + f][c] in T.
+constexpr int MEL_CHUNKS = 16;
+
+// grid (MEL_CHUNKS, segments), 256 threads: part[z][chunk] = max of chunk
+__global__ __launch_bounds__(256) void mel_max_kernel(const float* __restrict__ logmel, const int* __restrict__ nvalid,
+                                                      int n_mels, float* __restrict__ part) {
+    const int z = blockIdx.y, ch = blockIdx.x;
+    const float* L = logmel + (long long)z * 3000 * n_mels;
     const int nv = nvalid[z] * n_mels;
+    const int per = (3000 * n_mels / MEL_CHUNKS + 255) / 256 * 256;
+    const int e0 = ch * per, e1 = min(nv, e0 + per);
     float m = -INFINITY;
-    for (int e = threadIdx.x; e < nv; e += blockDim.x) m = fmaxf(m, L[e]);
+    for (int e = e0 + threadIdx.x; e < e1; e += 256) m = fmaxf(m, L[e]);
     m = wave_max(m);
-    __shared__ float red[16];
+    __shared__ float red[4];
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
     __syncthreads();
-    if (threadIdx.x < 64) {
-        float v = threadIdx.x < (blockDim.x >> 6) ? red[threadIdx.x] : -INFINITY;
-        v = wave_max(v);
-        if (threadIdx.x == 0) red[0] = v;
-    }
-    __syncthreads();
-    const float floor_ = red[0] - 8.0f;
+    if (threadIdx.x == 0)
+        part[z * MEL_CHUNKS + ch] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// grid (blocks, segments), 256 threads, each thread a run of elements
+template <class T>
+__global__ __launch_bounds__(256) void mel_norm_kernel(float* __restrict__ logmel, T* __restrict__ ypad,
+                                                       const int* __restrict__ nvalid, int n_mels,
+                                                       const float* __restrict__ part) {
+    const int z = blockIdx.y;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < MEL_CHUNKS; ++c) mx = fmaxf(mx, part[z * MEL_CHUNKS + c]);
+    const float floor_ = mx - 8.0f;
+    float* L = logmel + (long long)z * 3000 * n_mels;
+    const int nv = nvalid[z] * n_mels;
     T* Y = ypad + (long long)z * 3002 * CP;
-    for (int e = threadIdx.x; e < 3000 * n_mels; e += blockDim.x) {
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < 3000 * n_mels; e += gridDim.x * 256) {
         const int f = e / n_mels, c = e - f * n_mels;
         const float y = e < nv ? (fmaxf(L[e], floor_) + 4.0f) * 0.25f : 0.0f;
         L[e] = y;
@@ -139,14 +153,16 @@ __global__ __launch_bounds__(256) void layer_norm_kernel(const float* __restrict
 // Decoder input: x = token embedding + position embedding (fp32), then the
 // first layer's layer norm. The token embedding (shared with the output
 // head) and z use the decoder layout (dec_off); x and pos_emb are row-major.
+// Row r is slot list[r] at position rowpos[r], or at the slot's current
+// position pos[list[r]] when rowpos is null.
 template <class T, int E>
 __global__ __launch_bounds__(64) void embed_ln_kernel(const T* __restrict__ tok_emb, const T* __restrict__ pos_emb,
                                                       const int* __restrict__ list, const int* __restrict__ pos,
-                                                      const int* __restrict__ seq, float* __restrict__ x,
-                                                      T* __restrict__ z, const float* __restrict__ g,
-                                                      const float* __restrict__ b) {
+                                                      const int* __restrict__ rowpos, const int* __restrict__ seq,
+                                                      float* __restrict__ x, T* __restrict__ z,
+                                                      const float* __restrict__ g, const float* __restrict__ b) {
     constexpr int d = 64 * E;
-    const int r = blockIdx.x, lane = threadIdx.x, s = list[r], p = pos[s];
+    const int r = blockIdx.x, lane = threadIdx.x, s = list[r], p = rowpos ? rowpos[r] : pos[s];
     const int tok = seq[s * 448 + p];
     float v[E];
 #pragma unroll
@@ -1469,12 +1485,18 @@ __global__ void argmax_step_kernel(unsigned long long* __restrict__ best, int n,
 
 // Seat prompts: for entry e, slot slots[e] gets tokens prompts[e * 448 ...]
 // (position 0, no end of text seen).
+// prefilled = 1: positions 0 .. n_prompt - 2 are run at encode time, so the
+// slot's first decode step is at its last prompt position.
 __global__ void seat_kernel(const int* __restrict__ slots, const int* __restrict__ np_in,
                             const int* __restrict__ prompts, int* __restrict__ seq, int* __restrict__ pos,
-                            int* __restrict__ n_prompt, int* __restrict__ stop_at) {
+                            int* __restrict__ n_prompt, int* __restrict__ stop_at, int prefilled) {
     const int e = blockIdx.x, s = slots[e];
     for (int i = threadIdx.x; i < 448; i += blockDim.x) seq[s * 448 + i] = i < np_in[e] ? prompts[e * 448 + i] : 0;
-    if (threadIdx.x == 0) { pos[s] = 0; n_prompt[s] = np_in[e]; stop_at[s] = -1; }
+    if (threadIdx.x == 0) {
+        pos[s] = prefilled ? np_in[e] - 1 : 0;
+        n_prompt[s] = np_in[e];
+        stop_at[s] = -1;
+    }
 }
 
 }  // namespace wmi

@@ -77,7 +77,7 @@ def test_params_from_blob(lib):
 
 
 @pytest.mark.parametrize("field,value", [("max_slots", 0), ("max_slots", 129), ("pad_mode", 2),
-                                         ("max_encode_batch", 99), ("refill_min", -1)])
+                                         ("max_encode_batch", 99), ("refill_min", -1), ("prefill", 2)])
 def test_create_rejects_bad_params_before_device(lib, field, value):
     s = synth.TINY.with_(n_vocab=300, n_enc=1, n_dec=1)
     blob = synth.pack_blob(synth.make_weights(s, 0))
