@@ -122,7 +122,7 @@ def cpu_baseline(shape, W, segs):
     t = time.perf_counter()
     x = M.conv_stem(W, mel[None]) + M.sinusoid_pe(1500, shape.d)[None]
     t_stem = time.perf_counter() - t
-    NL = min(12, shape.n_enc, shape.n_dec)
+    NL = min(16, shape.n_enc, shape.n_dec)
     shl = shape.with_(n_enc=NL, n_dec=NL)
     t = time.perf_counter()
     E = M.encoder(W, shl, mel[None])
