@@ -139,14 +139,16 @@ int parse_blob_header(const void* blob, size_t bytes, whisper_params* out, const
 
 constexpr double kPi = 3.14159265358979323846;
 
-static std::vector<float> dft_basis() {  // [404][400]: rows 2k, 2k+1 = w cos, w sin of bin k
-    std::vector<float> b(404 * 400, 0.f);
+// k-major [400][DFT_ROWS]: column 2k, 2k+1 = w cos, w sin of bin k at sample n
+// (periodic Hann w), columns 402 .. DFT_ROWS-1 zero
+static std::vector<float> dft_basis() {
+    std::vector<float> b(400 * DFT_ROWS, 0.f);
     for (int k = 0; k <= 200; ++k)
         for (int n = 0; n < 400; ++n) {
             const double w = 0.5 - 0.5 * cos(2.0 * kPi * n / 400.0);
             const double ang = 2.0 * kPi * (double)((k * n) % 400) / 400.0;
-            b[(2 * k) * 400 + n] = (float)(w * cos(ang));
-            b[(2 * k + 1) * 400 + n] = (float)(w * sin(ang));
+            b[n * DFT_ROWS + 2 * k] = (float)(w * cos(ang));
+            b[n * DFT_ROWS + 2 * k + 1] = (float)(w * sin(ang));
         }
     return b;
 }
@@ -928,7 +930,8 @@ class EngineT final : public Engine {
         prof_begin(WHISPER_K_FRONT_END, st_);
         hipLaunchKernelGGL(prep_audio_kernel, dim3((480400 + 255) / 256, nb), dim3(256), 0, st_, segsrc_, xpad_,
                            P_.pad_mode);
-        gemm_simt(basis_, 400, 0, xpad_, 160, 480400, 404, 3000, 400, nb, EpiPower{power_}, st_);
+        hipLaunchKernelGGL(dft_power_kernel, dim3((3000 + DFT_FB - 1) / DFT_FB, 2, nb), dim3(256), 0, st_, basis_,
+                           xpad_, power_);
         gemm_simt(melfb_, 201, 0, power_, 201, 0, nm_, nb * 3000, 201, 1, EpiLogMel{logmel_, nm_}, st_);
         hipLaunchKernelGGL(mel_max_kernel, dim3(MEL_CHUNKS, nb), dim3(256), 0, st_, logmel_, nvalid_, nm_, melmax_);
         hipLaunchKernelGGL(mel_norm_kernel<T>, dim3(64, nb), dim3(256), 0, st_, logmel_, ypad_, nvalid_, nm_, melmax_);

@@ -32,18 +32,6 @@ struct EpiPre {
     int s;
 };
 
-// DFT -> power: rows (2k, 2k+1) are the cosine and sine parts of bin k.
-struct EpiPower {
-    float* power;  // [batch * 3000][201]
-    __device__ EpiPre pre(int, int, int) const { return EpiPre{}; }
-    __device__ void operator()(int i, int j, int z, float a, float b, float c, float d, const EpiPre&) const {
-        const int k = i >> 1;
-        float* p = power + ((long long)z * 3000 + j) * 201 + k;
-        p[0] = a * a + b * b;
-        if (k + 1 < 201) p[1] = c * c + d * d;
-    }
-};
-
 // Mel projection -> log10 with floor 1e-10. out [rows][n_mels].
 struct EpiLogMel {
     float* out;

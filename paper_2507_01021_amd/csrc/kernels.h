@@ -42,6 +42,100 @@ __global__ void prep_audio_kernel(const SegSrc* __restrict__ src, float* __restr
     xpad[(long long)z * 480400 + i] = s < n ? a[s] : 0.f;
 }
 
+// STFT power of the 3000 frames of each segment on the fp32 matrix cores:
+// C[i][f] = sum_n basis[i][n] xpad[160 f + n] over n < 400, where basis rows
+// 2k and 2k+1 are the Hann-windowed cosine and sine of bin k, then
+// power[z][f][k] = C[2k][f]^2 + C[2k+1][f]^2.
+// basisT is k-major: basisT[n][i] for i < DFT_ROWS (rows 402 .. 415 zero).
+// Workgroup: DFT_RH basis rows (13 tiles of 16) x 64 frames, 4 waves, wave w
+// takes frames 16 w .. 16 w + 15 against all 13 row tiles with
+// v_mfma_f32_16x16x4_f32. K runs in chunks of 16 through LDS (k-major
+// tiles, rows padded so the two half-waves of a read hit distinct banks),
+// the next chunk's loads held in registers while the current one is used.
+constexpr int DFT_ROWS = 416;        // 402 basis rows padded to 26 tiles of 16
+constexpr int DFT_RH = DFT_ROWS / 2; // rows per workgroup
+constexpr int DFT_FB = 64;           // frames per workgroup
+constexpr int DFT_BLD = DFT_FB + 16; // LDS row length of the frame tile
+
+typedef float mfma_f32x4_t __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void dft_power_kernel(const float* __restrict__ basisT,
+                                                        const float* __restrict__ xpad,
+                                                        float* __restrict__ power) {
+    __shared__ float As[2][16 * DFT_RH];
+    __shared__ float Bs[2][16 * DFT_BLD];
+    const int f0 = blockIdx.x * DFT_FB, half = blockIdx.y, z = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int fr = lane & 15, fc = lane >> 4;
+    const float* x = xpad + (long long)z * 480400;
+    // staging: A chunk = 16 k x 208 rows = 832 float4; B chunk = 64 frames x
+    // 16 k = 256 float4 (thread: frame tid / 4, k 4 (tid % 4) .. +3)
+    const int bj = tid >> 2, bq = tid & 3;
+    const float* xb = x + (long long)min(f0 + bj, 2999) * 160 + 4 * bq;
+    // A chunk element e = tid + 256 q (q < 3, and q = 3 for tid < 64): k row e / 52, float4 e % 52
+    int aoff[4], loff[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = min(tid + 256 * q, 831), kk = e / 52, c = e - kk * 52;
+        aoff[q] = kk * DFT_ROWS + half * DFT_RH + 4 * c;
+        loff[q] = kk * DFT_RH + 4 * c;
+    }
+    const bool a3 = tid + 768 < 832;
+#define WMI_DFT_GLOAD(K0)                                                                               \
+    do {                                                                                                \
+        a0 = *reinterpret_cast<const float4*>(basisT + (long long)(K0) * DFT_ROWS + aoff[0]);           \
+        a1 = *reinterpret_cast<const float4*>(basisT + (long long)(K0) * DFT_ROWS + aoff[1]);           \
+        a2 = *reinterpret_cast<const float4*>(basisT + (long long)(K0) * DFT_ROWS + aoff[2]);           \
+        if (a3) a3v = *reinterpret_cast<const float4*>(basisT + (long long)(K0) * DFT_ROWS + aoff[3]);  \
+        bv = *reinterpret_cast<const float4*>(xb + (K0));                                               \
+    } while (0)
+#define WMI_DFT_LSTORE(BUF)                                                                             \
+    do {                                                                                                \
+        *reinterpret_cast<float4*>(&As[BUF][loff[0]]) = a0;                                             \
+        *reinterpret_cast<float4*>(&As[BUF][loff[1]]) = a1;                                             \
+        *reinterpret_cast<float4*>(&As[BUF][loff[2]]) = a2;                                             \
+        if (a3) *reinterpret_cast<float4*>(&As[BUF][loff[3]]) = a3v;                                    \
+        Bs[BUF][(4 * bq + 0) * DFT_BLD + bj] = bv.x;                                                    \
+        Bs[BUF][(4 * bq + 1) * DFT_BLD + bj] = bv.y;                                                    \
+        Bs[BUF][(4 * bq + 2) * DFT_BLD + bj] = bv.z;                                                    \
+        Bs[BUF][(4 * bq + 3) * DFT_BLD + bj] = bv.w;                                                    \
+    } while (0)
+    float4 a0, a1, a2, a3v = float4{0.f, 0.f, 0.f, 0.f}, bv;
+    mfma_f32x4_t acc[13];
+#pragma unroll
+    for (int t = 0; t < 13; ++t) acc[t] = mfma_f32x4_t{0.f, 0.f, 0.f, 0.f};
+    constexpr int NCH = 400 / 16;
+    WMI_DFT_GLOAD(0);
+    WMI_DFT_LSTORE(0);
+    __syncthreads();
+    for (int ch = 0; ch < NCH; ++ch) {
+        const int buf = ch & 1;
+        if (ch + 1 < NCH) WMI_DFT_GLOAD((ch + 1) * 16);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const int k = 4 * kk + fc;
+            const float b = Bs[buf][k * DFT_BLD + 16 * w + fr];
+#pragma unroll
+            for (int t = 0; t < 13; ++t)
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(As[buf][k * DFT_RH + 16 * t + fr], b, acc[t], 0, 0, 0);
+        }
+        if (ch + 1 < NCH) WMI_DFT_LSTORE(buf ^ 1);
+        __syncthreads();
+    }
+#undef WMI_DFT_GLOAD
+#undef WMI_DFT_LSTORE
+    // lane: rows 16 t + 4 fc + r (bins (half * 208 + 16 t + 4 fc) / 2 + 0, 1), frame 16 w + fr
+    const int f = f0 + 16 * w + fr;
+    if (f >= 3000) return;
+    float* prow = power + ((long long)z * 3000 + f) * 201;
+#pragma unroll
+    for (int t = 0; t < 13; ++t) {
+        const int k = (half * DFT_RH + 16 * t + 4 * fc) >> 1;
+        if (k < 201) prow[k] = acc[t][0] * acc[t][0] + acc[t][1] * acc[t][1];
+        if (k + 1 < 201) prow[k + 1] = acc[t][2] * acc[t][2] + acc[t][3] * acc[t][3];
+    }
+}
+
 // Log-mel normalisation in two launches over many workgroups: the max over
 // each segment's valid frames (MEL_CHUNKS partial maxima per segment, no
 // atomics), then clamp to max - 8, (L + 4) / 4, zero the frames beyond the
