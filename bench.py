@@ -189,6 +189,8 @@ def main():
     ap.add_argument("--pad-mode", type=int, default=0, choices=(0, 1),
                     help="0: pad the audio to 30 s, then the front end (default); 1: front end on the "
                          "segment alone, features padded to 3000 frames")
+    ap.add_argument("--encode-batch", type=int, default=0,
+                    help="segments per encoder pass (0: min(slots, 32))")
     ap.add_argument("--prefill", type=int, default=0, choices=(0, 1),
                     help="decoder workloads: 1 runs each segment's prompt through the decoder in one pass at "
                          "encode time instead of one position per decode step")
@@ -214,7 +216,8 @@ def main():
     blob = synth.pack_blob(W)
     dev_audio = [torch.from_numpy(s.audio).to("cuda:0") for s in segs]
     ptrs = [t.data_ptr() for t in dev_audio]
-    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=min(slots, 32), pad_mode=a.pad_mode,
+    eb = a.encode_batch or min(slots, 32)
+    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=eb, pad_mode=a.pad_mode,
                           ctc_beam=a.ctc_beam, prefill=a.prefill if shape.n_dec else 0)
     del blob
     audio_s = sum(s.seconds for s in segs)
@@ -311,7 +314,7 @@ def main():
         "config": {"workload": a.workload, "segments": len(segs), "slots": slots,
                    "new_tokens": [int(min(s.max_new_tokens for s in segs)), int(max(s.max_new_tokens for s in segs))],
                    "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1,
-                   "pad_mode": a.pad_mode, "prefill": a.prefill},
+                   "pad_mode": a.pad_mode, "prefill": a.prefill, "encode_batch": eb},
         "roofline": roof, "encoder": enc, "decode": dec, "batcher": batcher,
     }
     if not a.no_cpu_baseline:
@@ -359,7 +362,7 @@ def bench_ctc(a, ctx, shape, W, segs, slots, ptrs, audio_s, wall, st_timed):
         "value": round(value, 2), "unit": "audio-s/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": round(wall / a.steps * 1e3, 2), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
-        "config": {"workload": a.workload, "segments": len(segs), "encode_batch": slots,
+        "config": {"workload": a.workload, "segments": len(segs), "encode_batch": a.encode_batch or min(slots, 32),
                    "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1, "pad_mode": a.pad_mode,
                    "decoding": "CTC best path" if a.ctc_beam < 2 else f"CTC prefix beam search, beam {a.ctc_beam}"},
         "roofline": roof, "encoder": enc, "batcher": batcher,
