@@ -1427,36 +1427,66 @@ __global__ __launch_bounds__(64) void ctc_beam_kernel(const float* __restrict__ 
         __syncthreads();
         // the B best candidates, in order (ties: lower candidate index)
         const int nxt = cur ^ 1;
-        int kept = 0;
-        for (int r = 0; r < B; ++r) {
-            float best = -INFINITY;
-            int bi = CMAX;
-            for (int j = lane; j < nc; j += 64)
-                if (cscore[j] > best || (cscore[j] == best && j < bi && cscore[j] > -INFINITY)) {
-                    best = cscore[j];
-                    bi = j;
+        if (nc <= 128) {
+            // one pass: a candidate's rank is the number of candidates ahead
+            // of it, and the first B ranks become the next beams
+            for (int j = lane; j < nc; j += 64) {
+                const float sj = cscore[j];
+                int rank = 0;
+#pragma unroll 8
+                for (int q = 0; q < nc; ++q) {
+                    const float sq = cscore[q];
+                    rank += (sq > sj || (sq == sj && q < j)) ? 1 : 0;
                 }
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) {
-                const float ob = __shfl_xor(best, o, 64);
-                const int oi = __shfl_xor(bi, o, 64);
-                if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+                if (sj > -INFINITY && rank < B) {
+                    bh[nxt][rank] = ch[j];
+                    blen[nxt][rank] = clen[j];
+                    blast[nxt][rank] = clast[j];
+                    bpb[nxt][rank] = cpb[j];
+                    bpnb[nxt][rank] = cpnb[j];
+                    bpe[(long long)t * KMAX + rank] = (cpar[j] << 20) | capp[j];
+                }
             }
-            if (bi >= CMAX || best == -INFINITY) break;
-            if (lane == 0) {
-                bh[nxt][r] = ch[bi];
-                blen[nxt][r] = clen[bi];
-                blast[nxt][r] = clast[bi];
-                bpb[nxt][r] = cpb[bi];
-                bpnb[nxt][r] = cpnb[bi];
-                bpe[(long long)t * KMAX + r] = (cpar[bi] << 20) | capp[bi];
-                cscore[bi] = -INFINITY;
+            int finite = 0;
+            for (int j0 = 0; j0 < nc; j0 += 64) {
+                const int j = j0 + lane;
+                finite += __popcll(__ballot(j < nc && cscore[j] > -INFINITY));
             }
+            if (lane == 0) nbeam = min(B, finite);
             __syncthreads();
-            ++kept;
+        } else {
+            // B rounds of a wave-wide maximum
+            int kept = 0;
+            for (int r = 0; r < B; ++r) {
+                float best = -INFINITY;
+                int bi = CMAX;
+                for (int j = lane; j < nc; j += 64)
+                    if (cscore[j] > best || (cscore[j] == best && j < bi && cscore[j] > -INFINITY)) {
+                        best = cscore[j];
+                        bi = j;
+                    }
+#pragma unroll
+                for (int o = 32; o >= 1; o >>= 1) {
+                    const float ob = __shfl_xor(best, o, 64);
+                    const int oi = __shfl_xor(bi, o, 64);
+                    if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+                }
+                if (bi >= CMAX || best == -INFINITY) break;
+                if (lane == 0) {
+                    bh[nxt][r] = ch[bi];
+                    blen[nxt][r] = clen[bi];
+                    blast[nxt][r] = clast[bi];
+                    bpb[nxt][r] = cpb[bi];
+                    bpnb[nxt][r] = cpnb[bi];
+                    bpe[(long long)t * KMAX + r] = (cpar[bi] << 20) | capp[bi];
+                    cscore[bi] = -INFINITY;
+                }
+                __syncthreads();
+                ++kept;
+            }
+            if (lane == 0) nbeam = kept;
+            __syncthreads();
         }
-        if (lane == 0) nbeam = kept;
-        __syncthreads();
         cur = nxt;
     }
     if (lane == 0) {  // trace the best final beam back to frame 0
