@@ -870,6 +870,19 @@ class EngineT final : public Engine {
                                                 s, part, n, bias, dx, dz, g, b));
         }
     }
+    // log-mel of `frames` power rows on the matrix cores (mel tiles of 16)
+    void mel_log(int frames) {
+        const dim3 grid((frames + 63) / 64);
+        switch ((nm_ + 15) / 16) {
+#define WMI_MEL_CASE(MT) \
+    case MT: hipLaunchKernelGGL(mel_log_kernel<MT>, grid, dim3(256), 0, st_, melfb_, power_, logmel_, frames, nm_); break;
+            WMI_MEL_CASE(1) WMI_MEL_CASE(2) WMI_MEL_CASE(3) WMI_MEL_CASE(4)
+            WMI_MEL_CASE(5) WMI_MEL_CASE(6) WMI_MEL_CASE(7) WMI_MEL_CASE(8)
+#undef WMI_MEL_CASE
+            default: throw ArgError(WHISPER_E_INVAL, "n_mels above 128");
+        }
+    }
+
     // split factor of a decode projection with reduction length K
     static int split_k(int K) { return (K / 32) % 4 == 0 ? 4 : 1; }
 
@@ -932,7 +945,7 @@ class EngineT final : public Engine {
                            P_.pad_mode);
         hipLaunchKernelGGL(dft_power_kernel, dim3((3000 + DFT_FB - 1) / DFT_FB, 2, nb), dim3(256), 0, st_, basis_,
                            xpad_, power_);
-        gemm_simt(melfb_, 201, 0, power_, 201, 0, nm_, nb * 3000, 201, 1, EpiLogMel{logmel_, nm_}, st_);
+        mel_log(nb * 3000);
         hipLaunchKernelGGL(mel_max_kernel, dim3(MEL_CHUNKS, nb), dim3(256), 0, st_, logmel_, nvalid_, nm_, melmax_);
         hipLaunchKernelGGL(mel_norm_kernel<T>, dim3(64, nb), dim3(256), 0, st_, logmel_, ypad_, nvalid_, nm_, melmax_);
         prof_end(WHISPER_K_FRONT_END, st_);
@@ -1083,7 +1096,14 @@ class EngineT final : public Engine {
         lnpg_ = vecf("enc.ln_post.g");
         lnpb_ = vecf("enc.ln_post.b");
         basis_ = upload_new(dft_basis());
-        melfb_ = upload_new(mel_bank(nm_));
+        {  // k-major [DFT_PS][mel tiles x 16], zero beyond bin 200 and mel nm_ - 1
+            const int mp = (nm_ + 15) / 16 * 16;
+            const std::vector<float> fb = mel_bank(nm_);
+            std::vector<float> t((size_t)DFT_PS * mp, 0.f);
+            for (int m = 0; m < nm_; ++m)
+                for (int k = 0; k < 201; ++k) t[(size_t)k * mp + m] = fb[(size_t)m * 201 + k];
+            melfb_ = upload_new(t);
+        }
         pe_ = upload_new(sinusoids(N_CTX, d));
         if (ctc_) {
             Wctc_ = mat("ctc.w");
@@ -1129,7 +1149,7 @@ class EngineT final : public Engine {
         seat_np_ = slot_of_ + EB;
         seat_prompts_ = seat_np_ + EB;
         xpad_ = dalloc<float>(EB * 480400);
-        power_ = dalloc<float>(EB * 3000 * 201);
+        power_ = dalloc<float>(EB * 3000 * DFT_PS);
         logmel_ = dalloc<float>(EB * 3000 * nm_);
         melmax_ = dalloc<float>(EB * MEL_CHUNKS);
         ypad_ = dalloc<T>(EB * 3002 * CP);

@@ -32,17 +32,6 @@ struct EpiPre {
     int s;
 };
 
-// Mel projection -> log10 with floor 1e-10. out [rows][n_mels].
-struct EpiLogMel {
-    float* out;
-    int n_mels;
-    __device__ EpiPre pre(int, int, int) const { return EpiPre{}; }
-    __device__ void operator()(int i, int j, int, float a, float b, float c, float d, const EpiPre&) const {
-        st4(out + (long long)j * n_mels + i, log10f(fmaxf(a, 1e-10f)), log10f(fmaxf(b, 1e-10f)),
-            log10f(fmaxf(c, 1e-10f)), log10f(fmaxf(d, 1e-10f)));
-    }
-};
-
 template <class T>
 struct EpiConv1 {  // i = channel, j = frame
     const float* bias;

@@ -45,7 +45,8 @@ __global__ void prep_audio_kernel(const SegSrc* __restrict__ src, float* __restr
 // STFT power of the 3000 frames of each segment on the fp32 matrix cores:
 // C[i][f] = sum_n basis[i][n] xpad[160 f + n] over n < 400, where basis rows
 // 2k and 2k+1 are the Hann-windowed cosine and sine of bin k, then
-// power[z][f][k] = C[2k][f]^2 + C[2k+1][f]^2.
+// power[z][f][k] = C[2k][f]^2 + C[2k+1][f]^2 (row stride DFT_PS; bins
+// 201 .. 207 come from the zero basis rows and are 0).
 // basisT is k-major: basisT[n][i] for i < DFT_ROWS (rows 402 .. 415 zero).
 // Workgroup: DFT_RH basis rows (13 tiles of 16) x 64 frames, 4 waves, wave w
 // takes frames 16 w .. 16 w + 15 against all 13 row tiles with
@@ -56,6 +57,7 @@ constexpr int DFT_ROWS = 416;        // 402 basis rows padded to 26 tiles of 16
 constexpr int DFT_RH = DFT_ROWS / 2; // rows per workgroup
 constexpr int DFT_FB = 64;           // frames per workgroup
 constexpr int DFT_BLD = DFT_FB + 16; // LDS row length of the frame tile
+constexpr int DFT_PS = DFT_RH;       // power row stride: bins 0..200, then zeros to 207
 
 typedef float mfma_f32x4_t __attribute__((ext_vector_type(4)));
 
@@ -127,12 +129,84 @@ __global__ __launch_bounds__(256) void dft_power_kernel(const float* __restrict_
     // lane: rows 16 t + 4 fc + r (bins (half * 208 + 16 t + 4 fc) / 2 + 0, 1), frame 16 w + fr
     const int f = f0 + 16 * w + fr;
     if (f >= 3000) return;
-    float* prow = power + ((long long)z * 3000 + f) * 201;
+    float* prow = power + ((long long)z * 3000 + f) * DFT_PS;
 #pragma unroll
     for (int t = 0; t < 13; ++t) {
         const int k = (half * DFT_RH + 16 * t + 4 * fc) >> 1;
-        if (k < 201) prow[k] = acc[t][0] * acc[t][0] + acc[t][1] * acc[t][1];
-        if (k + 1 < 201) prow[k + 1] = acc[t][2] * acc[t][2] + acc[t][3] * acc[t][3];
+        prow[k] = acc[t][0] * acc[t][0] + acc[t][1] * acc[t][1];
+        prow[k + 1] = acc[t][2] * acc[t][2] + acc[t][3] * acc[t][3];
+    }
+}
+
+// Mel projection and log on the fp32 matrix cores: logmel[f][m] =
+// log10(max(sum_k fb[m][k] power[f][k], 1e-10)) over the 208 power bins of
+// a frame (fb is zero beyond bin 200). fbT is k-major [208][16 MT] (mels
+// padded to MT tiles of 16 with zero rows). Workgroup: 64 frames, 4 waves,
+// wave w takes frames 16 w .. 16 w + 15 against every mel tile; K in LDS
+// chunks of 16, the next chunk's loads held in registers.
+template <int MT>
+__global__ __launch_bounds__(256) void mel_log_kernel(const float* __restrict__ fbT, const float* __restrict__ power,
+                                                      float* __restrict__ logmel, int frames, int n_mels) {
+    constexpr int MP = 16 * MT, ALD = MP % 32 == 0 ? MP + 16 : MP, AQ = 16 * MP / 4;
+    __shared__ float As[2][16 * ALD];
+    __shared__ float Bs[2][16 * DFT_BLD];
+    const int f0 = blockIdx.x * 64;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int fr = lane & 15, fc = lane >> 4;
+    const int bj = tid >> 2, bq = tid & 3;
+    const float* pb = power + (long long)min(f0 + bj, frames - 1) * DFT_PS + 4 * bq;
+    float4 a0, a1 = float4{0.f, 0.f, 0.f, 0.f}, bv;
+    const bool has1 = tid + 256 < AQ;
+    const int e0 = tid, e1 = min(tid + 256, AQ - 1);
+    const int k0r = e0 / (MP / 4), c0 = e0 - k0r * (MP / 4), k1r = e1 / (MP / 4), c1 = e1 - k1r * (MP / 4);
+#define WMI_MEL_GLOAD(K0)                                                                              \
+    do {                                                                                               \
+        if (e0 < AQ) a0 = *reinterpret_cast<const float4*>(fbT + (long long)((K0) + k0r) * MP + 4 * c0); \
+        if (has1) a1 = *reinterpret_cast<const float4*>(fbT + (long long)((K0) + k1r) * MP + 4 * c1);    \
+        bv = *reinterpret_cast<const float4*>(pb + (K0));                                              \
+    } while (0)
+#define WMI_MEL_LSTORE(BUF)                                                                            \
+    do {                                                                                               \
+        if (e0 < AQ) *reinterpret_cast<float4*>(&As[BUF][k0r * ALD + 4 * c0]) = a0;                    \
+        if (has1) *reinterpret_cast<float4*>(&As[BUF][k1r * ALD + 4 * c1]) = a1;                       \
+        Bs[BUF][(4 * bq + 0) * DFT_BLD + bj] = bv.x;                                                   \
+        Bs[BUF][(4 * bq + 1) * DFT_BLD + bj] = bv.y;                                                   \
+        Bs[BUF][(4 * bq + 2) * DFT_BLD + bj] = bv.z;                                                   \
+        Bs[BUF][(4 * bq + 3) * DFT_BLD + bj] = bv.w;                                                   \
+    } while (0)
+    mfma_f32x4_t acc[MT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[t] = mfma_f32x4_t{0.f, 0.f, 0.f, 0.f};
+    constexpr int NCH = DFT_PS / 16;
+    WMI_MEL_GLOAD(0);
+    WMI_MEL_LSTORE(0);
+    __syncthreads();
+    for (int ch = 0; ch < NCH; ++ch) {
+        const int buf = ch & 1;
+        if (ch + 1 < NCH) WMI_MEL_GLOAD((ch + 1) * 16);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const int k = 4 * kk + fc;
+            const float b = Bs[buf][k * DFT_BLD + 16 * w + fr];
+#pragma unroll
+            for (int t = 0; t < MT; ++t)
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(As[buf][k * ALD + 16 * t + fr], b, acc[t], 0, 0, 0);
+        }
+        if (ch + 1 < NCH) WMI_MEL_LSTORE(buf ^ 1);
+        __syncthreads();
+    }
+#undef WMI_MEL_GLOAD
+#undef WMI_MEL_LSTORE
+    // lane: mels 16 t + 4 fc .. +3 of frame 16 w + fr
+    const int f = f0 + 16 * w + fr;
+    if (f >= frames) return;
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+        const int m = 16 * t + 4 * fc;
+        if (m < n_mels)
+            *reinterpret_cast<float4*>(logmel + (long long)f * n_mels + m) =
+                float4{log10f(fmaxf(acc[t][0], 1e-10f)), log10f(fmaxf(acc[t][1], 1e-10f)),
+                       log10f(fmaxf(acc[t][2], 1e-10f)), log10f(fmaxf(acc[t][3], 1e-10f))};
     }
 }
 
