@@ -120,3 +120,17 @@ def test_params_from_ctc_blob(lib):
     p = binding.whisper_params()
     assert lib.whisper_params_from_blob(hdr.ctypes.data, hdr.size, C.byref(p)) == 0
     assert (p.n_text_layer, p.n_vocab, p.n_audio_layer) == (0, 256, 1)
+
+
+def test_prefill_rejected_for_ctc_models(lib):
+    """prefill = 1 needs a decoder: a CTC blob's context is refused before any device work."""
+    shape = synth.CTC_TINY.with_(n_enc=1)
+    lay, total = synth.blob_layout(shape)
+    blob = np.zeros(total, dtype=np.uint8)
+    blob[:256] = synth.pack_blob(synth.make_weights(shape, 0))[:256]
+    p = binding.params_from_blob(blob)
+    p.prefill = 1
+    h = C.c_void_p()
+    st = lib.whisper_ctx_create(C.byref(p), blob.ctypes.data, blob.nbytes, 0, C.byref(h))
+    assert st == binding.E_INVAL and not h.value
+    assert b"prefill" in lib.whisper_last_error(None)
