@@ -346,7 +346,8 @@ def bench_ctc(a, ctx, shape, W, segs, slots, ptrs, audio_s, wall, st_timed):
     fc1_tf = fc1_flops / (g_ms / 1e3) / 1e12
     roof = {"bound": "mfma", "achieved": round(fc1_tf, 1), "peak": peak_f / 1e12, "unit": "TFLOP/s",
             "frac": round(fc1_tf * 1e12 / peak_f, 4), "traffic": None,
-            "kernel": "gemm_bf16_kernel<EpiGelu> (encoder fc1 + GELU)",
+            "kernel": ("gemm_bf16_h_kernel" if shape.d <= 1024 else "gemm_bf16_kernel")
+                      + "<EpiGelu> (encoder fc1 + GELU)",
             "flops_per_launch": fc1_flops / max(g_n, 1), "avg_launch_us": round(g_ms * 1e3 / max(g_n, 1), 2),
             "launches": g_n}
     fe_ms, fe_n = prof[binding.K_FRONT_END]

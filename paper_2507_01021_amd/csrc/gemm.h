@@ -10,12 +10,15 @@
 // is A so that the four consecutive i are the contiguous output dimension.
 //
 // gemm_bf16: bf16 inputs, v_mfma_f32_16x16x32_bf16 with fp32 accumulation,
-//   256x256 workgroup tile, 4 waves of 128x128, K tiles of 32 streamed into a
-//   4-stage LDS ring with direct global->LDS loads (three tiles in flight, no
-//   staging registers), 16-byte chunks XOR-swizzled against bank conflicts.
+//   K tiles of 32 streamed into an LDS ring with direct global->LDS loads
+//   (no staging registers), 16-byte chunks XOR-swizzled against bank
+//   conflicts. Two tilings: 256x256 tiles, 8 waves of 128x64, a 4-stage ring
+//   (one workgroup per CU), for K > 1024; 256x128 tiles, 8 waves of 64x64, a
+//   3-stage ring (two workgroups per CU), for K <= 1024. Tiles are mapped to
+//   the XCDs so that workgroups sharing an L2 share operand tiles.
 //   Requires K % 64 == 0, MA % 4 == 0, 16-byte aligned rows (lda, ldb % 8 == 0).
-// gemm_simt: fp32 (or bf16 storage) SIMT kernel for the fp32 model and the
-//   front end: 64x64x16 tile, 4x4 outputs per thread, any K, any lda.
+// gemm_simt: fp32 (or bf16 storage) SIMT kernel for the fp32 model: 64x64x16
+//   tile, 4x4 outputs per thread, any K, any lda.
 #pragma once
 
 #include "common.h"
@@ -163,6 +166,98 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_kernel(
     }
 }
 
+// Two-workgroups-per-CU variant: a 256 x 128 tile, 8 waves of 64 x 64
+// (64 accumulator registers), a 3-stage ring of 24 KiB stages (72 KiB), so
+// two workgroups share a CU and one's prologue and epilogue overlap the
+// other's main loop.
+namespace gh {
+constexpr int BM = 256, BN = 128, BK = 32, NS = 3, THREADS = 512;
+constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;  // 16 KiB, 8 KiB
+constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+constexpr int LDS_BYTES = NS * STAGE_BYTES;  // 72 KiB
+}  // namespace gh
+
+template <class Epi>
+__global__ __launch_bounds__(512, 2) void gemm_bf16_h_kernel(
+    const bf16* __restrict__ A, int lda, long long sA, const bf16* __restrict__ B, int ldb,
+    long long sB, int MA, int MB, int K, int tilesA, Epi epi) {
+    extern __shared__ __align__(16) unsigned char lds[];
+    const int z = blockIdx.z;
+    A += (long long)z * sA;
+    B += (long long)z * sB;
+    int ta, tb;
+    xcd_tile(blockIdx.x, tilesA, (int)(gridDim.x / tilesA), ta, tb);
+    const int a0 = ta * gh::BM, b0 = tb * gh::BN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wa = (wave & 3) * 64, wb = (wave >> 2) * 64;
+    const int fr = lane & 15, fc = lane >> 4;
+
+    // Direct loads: wave w fills A rows 32 w .. 32 w + 31 (2 instructions of
+    // 16 rows x 64 B) and B rows 16 w .. 16 w + 15 (1 instruction).
+    const int dr = lane >> 2;
+    const int dc = (lane & 3) ^ ((dr >> 1) & 3);
+    const bf16* ga[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) ga[s] = A + (long long)min(a0 + wave * 32 + s * 16 + dr, MA - 1) * lda + dc * 8;
+    const bf16* gp = B + (long long)min(b0 + wave * 16 + dr, MB - 1) * ldb + dc * 8;
+
+    mfma_f32x4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_f32x4{0.f, 0.f, 0.f, 0.f};
+
+#define WMI_ISSUE3(KT)                                                                                  \
+    do {                                                                                                \
+        const int st_ = ((KT) % gh::NS) * gh::STAGE_BYTES;                                              \
+        const int k_ = (KT) * gh::BK;                                                                   \
+        _Pragma("unroll") for (int s = 0; s < 2; ++s)                                                  \
+            __builtin_amdgcn_global_load_lds(ga[s] + k_, lds + st_ + wave * 2048 + s * 1024, 16, 0, 0); \
+        __builtin_amdgcn_global_load_lds(gp + k_, lds + st_ + gh::A_BYTES + wave * 1024, 16, 0, 0);     \
+    } while (0)
+
+    const int nk = K / gh::BK;
+    WMI_ISSUE3(0);
+    if (nk > 1) WMI_ISSUE3(1);
+    for (int kt = 0; kt < nk; ++kt) {
+        // tile kt has landed once only the 3-load group of the next tile is pending
+        if (kt + 1 < nk) __builtin_amdgcn_s_waitcnt(WMI_VMCNT(3));
+        else __builtin_amdgcn_s_waitcnt(WMI_VMCNT(0));
+        __builtin_amdgcn_s_barrier();
+        if (kt + gh::NS - 1 < nk) WMI_ISSUE3(kt + gh::NS - 1);
+        const unsigned char* stage = lds + (kt % gh::NS) * gh::STAGE_BYTES;
+        mfma_bf16x8 fa[4], fb[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fa[i] = *reinterpret_cast<const mfma_bf16x8*>(stage + swz32(wa + i * 16 + fr, fc));
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            fb[j] = *reinterpret_cast<const mfma_bf16x8*>(stage + gh::A_BYTES + swz32(wb + j * 16 + fr, fc));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+#undef WMI_ISSUE3
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int jj = b0 + wb + j * 16 + fr;
+        const bool jok = jj < MB;
+        EpiPre pre[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int ii = a0 + wa + i * 16 + fc * 4;
+            if (jok && ii < MA) pre[i] = epi.pre(ii, jj, z);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int ii = a0 + wa + i * 16 + fc * 4;
+            if (jok && ii < MA) epi(ii, jj, z, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], pre[i]);
+        }
+    }
+}
+
 template <class Epi>
 inline void gemm_bf16(const bf16* A, int lda, long long sA, const bf16* B, int ldb, long long sB,
                       int MA, int MB, int K, int batch, const Epi& epi, hipStream_t st) {
@@ -174,6 +269,26 @@ inline void gemm_bf16(const bf16* A, int lda, long long sA, const bf16* B, int l
         WMI_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<Epi>),
                                     hipFuncAttributeMaxDynamicSharedMemorySize, gb::LDS_BYTES));
         attr_set = true;
+    }
+    // Short reductions (K <= 1024) take the 256 x 128 tiles, two workgroups
+    // per CU, whose prologues and epilogues overlap; longer ones the
+    // 256 x 256 tiles. WHISPER_GEMM_H=0/1 forces one.
+    static const int force = [] {
+        const char* g = getenv("WHISPER_GEMM_H");
+        return g ? (g[0] == '1' ? 1 : 0) : -1;
+    }();
+    if (force == 1 || (force < 0 && K <= 1024)) {
+        static bool attr_h = false;
+        if (!attr_h) {
+            WMI_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_h_kernel<Epi>),
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, gh::LDS_BYTES));
+            attr_h = true;
+        }
+        const int tb2 = (MB + gh::BN - 1) / gh::BN;
+        dim3 grid(tilesA * tb2, 1, batch);
+        hipLaunchKernelGGL((gemm_bf16_h_kernel<Epi>), grid, dim3(gh::THREADS), gh::LDS_BYTES, st, A, lda, sA, B,
+                           ldb, sB, MA, MB, K, tilesA, epi);
+        return;
     }
     dim3 grid(tilesA * tilesB, 1, batch);
     hipLaunchKernelGGL((gemm_bf16_kernel<Epi>), grid, dim3(gb::THREADS), gb::LDS_BYTES, st, A, lda,
