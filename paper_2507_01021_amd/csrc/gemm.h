@@ -21,6 +21,8 @@
 //   tile, 4x4 outputs per thread, any K, any lda.
 #pragma once
 
+#include <atomic>
+
 #include "common.h"
 
 namespace wmi {
@@ -258,18 +260,23 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_h_kernel(
     }
 }
 
+// Raises kernel f's dynamic LDS limit to `bytes` on the current device, once
+// per device (the attribute is per device; `done` holds one bit per device).
+inline void lds_limit(const void* f, int bytes, std::atomic<uint64_t>& done) {
+    int dev = 0;
+    WMI_HIP(hipGetDevice(&dev));
+    const uint64_t bit = 1ull << (dev & 63);
+    if (done.load() & bit) return;
+    WMI_HIP(hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes));
+    done.fetch_or(bit);
+}
+
 template <class Epi>
 inline void gemm_bf16(const bf16* A, int lda, long long sA, const bf16* B, int ldb, long long sB,
                       int MA, int MB, int K, int batch, const Epi& epi, hipStream_t st) {
     if (K % 64 || MA % 4 || lda % 8 || ldb % 8 || MA <= 0 || MB <= 0 || batch <= 0)
         throw ArgError(-1, "gemm_bf16: unsupported shape");
     const int tilesA = (MA + gb::BM - 1) / gb::BM, tilesB = (MB + gb::BN - 1) / gb::BN;
-    static bool attr_set = false;  // one per epilogue instantiation
-    if (!attr_set) {
-        WMI_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<Epi>),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, gb::LDS_BYTES));
-        attr_set = true;
-    }
     // Short reductions (K <= 1024) take the 256 x 128 tiles, two workgroups
     // per CU, whose prologues and epilogues overlap; longer ones the
     // 256 x 256 tiles. WHISPER_GEMM_H=0/1 forces one.
@@ -278,18 +285,16 @@ inline void gemm_bf16(const bf16* A, int lda, long long sA, const bf16* B, int l
         return g ? (g[0] == '1' ? 1 : 0) : -1;
     }();
     if (force == 1 || (force < 0 && K <= 1024)) {
-        static bool attr_h = false;
-        if (!attr_h) {
-            WMI_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_h_kernel<Epi>),
-                                        hipFuncAttributeMaxDynamicSharedMemorySize, gh::LDS_BYTES));
-            attr_h = true;
-        }
+        static std::atomic<uint64_t> done_h{0};  // one per epilogue instantiation
+        lds_limit(reinterpret_cast<const void*>(&gemm_bf16_h_kernel<Epi>), gh::LDS_BYTES, done_h);
         const int tb2 = (MB + gh::BN - 1) / gh::BN;
         dim3 grid(tilesA * tb2, 1, batch);
         hipLaunchKernelGGL((gemm_bf16_h_kernel<Epi>), grid, dim3(gh::THREADS), gh::LDS_BYTES, st, A, lda, sA, B,
                            ldb, sB, MA, MB, K, tilesA, epi);
         return;
     }
+    static std::atomic<uint64_t> done{0};
+    lds_limit(reinterpret_cast<const void*>(&gemm_bf16_kernel<Epi>), gb::LDS_BYTES, done);
     dim3 grid(tilesA * tilesB, 1, batch);
     hipLaunchKernelGGL((gemm_bf16_kernel<Epi>), grid, dim3(gb::THREADS), gb::LDS_BYTES, st, A, lda,
                        sA, B, ldb, sB, MA, MB, K, tilesA, epi);
