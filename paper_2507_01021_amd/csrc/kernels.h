@@ -653,11 +653,11 @@ __global__ __launch_bounds__(64) void enc_attn_f32_kernel(const float* __restric
 
 // ------------------------------------------------------------- decode attention
 //
-// One wavefront per (row r, head h, chunk c) over the slot's cache: scores
-// with K^T rows (lane owns PPL consecutive positions), softmax in fp32 with
-// wavefront reductions, then P V with V rows (8 lanes per 128-byte row, 8
-// rows per load). With one chunk the normalised output is written directly;
-// otherwise (m, l, o[64]) partials go to `part` for the combine kernel.
+// Attention of one decode position per (row, head) over the slot's caches:
+// keys stored transposed (K^T [64][positions]) so a lane owns consecutive
+// positions and scores need no cross-lane reduction, values row-major so
+// eight lanes read one 128-byte row; softmax in fp32. self_attn_kernel and
+// cross_attn_kernel below describe their work split.
 template <class T>
 __device__ inline void load_vec(const T* p, float* out, int n);
 template <>
