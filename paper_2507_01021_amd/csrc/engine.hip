@@ -2,18 +2,20 @@
 // encode pass / decode step that drive the kernels on the context's stream.
 //
 // Encode pass (Listing 1: features per segment, pad to 30 s, stack, encode):
-//   audio -> reflect-padded window -> DFT power (SIMT GEMM, window folded
-//   into the basis) -> mel projection + log10 -> per-segment max and
-//   normalisation -> conv stem (two implicit-im2col GEMMs over overlapping
-//   rows) -> encoder layers (LN, QK and V projections, attention, output
-//   projection + residual, LN, fc1 + GELU, fc2 + residual) -> final LN ->
-//   cross-attention keys and values of every decoder layer written straight
-//   into the slots' caches -> prompts seated.
+//   audio -> reflect-padded window -> DFT power (fp32 matrix cores, window
+//   folded into the basis) -> mel projection + log10 (fp32 matrix cores) ->
+//   per-segment max and normalisation -> conv stem (two implicit-im2col
+//   GEMMs over overlapping rows) -> encoder layers (LN, QK and V
+//   projections, attention, output projection + residual, LN, fc1 + GELU,
+//   fc2 + residual) -> final LN -> cross-attention keys and values of every
+//   decoder layer written straight into the slots' caches -> prompts seated
+//   (and, with prefill, prompt positions 0..n_prompt-2 run through the
+//   decoder layers).
 // Decode step (greedy generate, one token per active slot):
 //   embedding -> per layer: LN, fused QKV projection appending this position
 //   to the self-attention cache, self-attention over the slot's positions,
 //   output projection + residual, LN, cross query, cross-attention over the
-//   1500 cached encoder positions (chunked + combine), output projection +
+//   1500 cached encoder positions, output projection +
 //   residual, LN, fc1 + GELU, fc2 + residual -> final LN -> logits against
 //   the token embedding -> argmax, next input, position advance.
 //   In bf16 the projection weights and the activations they multiply are
