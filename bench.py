@@ -316,6 +316,8 @@ def main():
                    "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1,
                    "pad_mode": a.pad_mode, "prefill": a.prefill, "encode_batch": eb},
         "roofline": roof, "encoder": enc, "decode": dec, "batcher": batcher,
+        # every segment is encoded as a full 30 s window: RTFx over padded seconds
+        "padded_rtfx": round(30.0 * len(segs) * a.steps / wall, 2),
     }
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, W, segs)
@@ -367,6 +369,7 @@ def bench_ctc(a, ctx, shape, W, segs, slots, ptrs, audio_s, wall, st_timed):
                    "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1, "pad_mode": a.pad_mode,
                    "decoding": "CTC best path" if a.ctc_beam < 2 else f"CTC prefix beam search, beam {a.ctc_beam}"},
         "roofline": roof, "encoder": enc, "batcher": batcher,
+        "padded_rtfx": round(30.0 * len(segs) * a.steps / wall, 2),
     }
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_ctc(shape, W, segs)
