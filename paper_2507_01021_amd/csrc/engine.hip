@@ -23,8 +23,10 @@
 //   split in two halves (the first a whole number of 16-row tiles) that run
 //   the complete step on two streams, each as its own captured graph (the
 //   halves touch disjoint slots), so the two chains of small latency-bound
-//   kernels overlap. Steps with kernel timing on run unsplit, so each timed
-//   launch has the device to itself.
+//   kernels overlap. While the slot list stays the same the chains are not
+//   joined between steps (one may run a step ahead of the other); any other
+//   call joins them first. Steps with kernel timing on run unsplit, so each
+//   timed launch has the device to itself.
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
@@ -233,6 +235,7 @@ class EngineT final : public Engine {
         if (const char* g = getenv("WHISPER_STEP_SPLIT")) split_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_STEP_CHAINS")) chains_ = std::max(1, std::min(MAXC, atoi(g)));
         if (const char* g = getenv("WHISPER_FUSED_LN")) fused_ln_ = g[0] != '0';
+        if (const char* g = getenv("WHISPER_FREE_CHAINS")) free_run_ = g[0] != '0';
         load_weights(blob, bytes);
         alloc_state();
         WMI_HIP(hipDeviceSynchronize());
@@ -276,28 +279,57 @@ class EngineT final : public Engine {
     }
 
     void set_stream(void* s) override {
+        join_chains();
         WMI_HIP(hipStreamSynchronize(st_));
         st_ = s ? static_cast<hipStream_t>(s) : own_stream_;
     }
 
     void sync() override {
+        join_chains();
         WMI_HIP(hipStreamSynchronize(st_));
         if (ctc_st_) WMI_HIP(hipStreamSynchronize(ctc_st_));
     }
 
     // -------------------------------------------------------------- encode
     void encode(const SegmentDesc* segs, int n, const int* slots, bool sync_) override {
+        join_chains();
         WMI_HIP(hipSetDevice(dev_));
         for (int s0 = 0; s0 < n; s0 += EB_) encode_pass(segs + s0, std::min(EB_, n - s0), slots + s0);
         WMI_HIP(hipGetLastError());
         if (sync_) WMI_HIP(hipStreamSynchronize(st_));
     }
 
+    // Steps of an unchanged slot list may leave the chains running apart
+    // (each on its own stream, ahead or behind the others); everything else
+    // first joins them into the context's stream.
+    void join_chains() {
+        if (!chains_apart_) return;
+        for (int c = 1; c < apart_nc_; ++c) {
+            WMI_HIP(hipEventRecord(join_ev_[c], cst_[c]));
+            WMI_HIP(hipStreamWaitEvent(st_, join_ev_[c], 0));
+        }
+        chains_apart_ = false;
+    }
+
     // -------------------------------------------------------------- decode step
     void decode_step(const int* slots, int n, const int* forced, int* out_tok, float* out_logits,
                      bool sync_) override {
         WMI_HIP(hipSetDevice(dev_));
-        if (n != (int)list_host_.size() || !std::equal(slots, slots + n, list_host_.begin())) {
+        const bool same_list = n == (int)list_host_.size() && std::equal(slots, slots + n, list_host_.begin());
+        bool timed = false;
+        for (auto& pr : prof_) timed = timed || pr.on;
+        const bool plain = graphs_ && !forced && !out_tok && !out_logits && !timed && !sync_;
+        if (free_run_ && plain && same_list && chains_apart_) {
+            // the chains keep running on their own streams: no fork, no join
+            auto it = step_graphs_.find(n);
+            if (it != step_graphs_.end()) {
+                for (int c = 0; c < apart_nc_; ++c) WMI_HIP(hipGraphLaunch(it->second[c], c == 0 ? st_ : cst_[c]));
+                WMI_HIP(hipGetLastError());
+                return;
+            }
+        }
+        join_chains();
+        if (!same_list) {
             list_host_.assign(slots, slots + n);
             upload(0, list_, slots, n * sizeof(int));
         }
@@ -305,8 +337,6 @@ class EngineT final : public Engine {
         // Plain steps (no teacher forcing, no per-step outputs, no kernel
         // timing) replay captured graphs of the whole step; a graph only
         // depends on the row count because the slot list lives in device memory.
-        bool timed = false;
-        for (auto& pr : prof_) timed = timed || pr.on;
         int r0[MAXC + 1];
         const int nc = timed ? (r0[0] = 0, r0[1] = n, 1) : chain_rows(n, r0);
         auto stream = [&](int c) { return c == 0 ? st_ : cst_[c]; };
@@ -327,9 +357,14 @@ class EngineT final : public Engine {
         } else {
             for (int c = 0; c < nc; ++c) launch_rows(r0[c], r0[c + 1] - r0[c], forced != nullptr, stream(c), c);
         }
-        for (int c = 1; c < nc; ++c) {  // join
-            WMI_HIP(hipEventRecord(join_ev_[c], cst_[c]));
-            WMI_HIP(hipStreamWaitEvent(st_, join_ev_[c], 0));
+        if (free_run_ && plain && nc > 1) {  // stay apart until something needs the results
+            chains_apart_ = true;
+            apart_nc_ = nc;
+        } else {
+            for (int c = 1; c < nc; ++c) {  // join
+                WMI_HIP(hipEventRecord(join_ev_[c], cst_[c]));
+                WMI_HIP(hipStreamWaitEvent(st_, join_ev_[c], 0));
+            }
         }
         prof_end(WHISPER_K_DEC_STEP, st_);
         WMI_HIP(hipGetLastError());
@@ -486,6 +521,7 @@ class EngineT final : public Engine {
     }
 
     void read_tokens(int slot, int count, int32_t* dst) override {
+        join_chains();
         WMI_HIP(hipSetDevice(dev_));
         if (count <= 0) return;
         WMI_HIP(hipMemcpyAsync(dst, gen_ + (size_t)slot * 448, count * sizeof(int), hipMemcpyDeviceToHost, st_));
@@ -493,9 +529,13 @@ class EngineT final : public Engine {
     }
 
     void read_tokens_async(int slot, int count, int32_t* dst) override {
+        join_chains();
         queue_read(gen_ + (size_t)slot * 448, count, dst);
     }
-    void read_stop_async(int slot, int32_t* dst) override { queue_read(stop_at_ + slot, 1, dst); }
+    void read_stop_async(int slot, int32_t* dst) override {
+        join_chains();
+        queue_read(stop_at_ + slot, 1, dst);
+    }
 
     // Queues a copy of count ints from device memory into the pinned area,
     // delivered to dst by finish_reads().
@@ -516,6 +556,7 @@ class EngineT final : public Engine {
     }
 
     void finish_reads() override {
+        join_chains();
         WMI_HIP(hipStreamSynchronize(st_));
         for (auto& r : pending_) memcpy(r.dst, tokpin_ + r.off, r.count * sizeof(int));
         pending_.clear();
@@ -524,6 +565,7 @@ class EngineT final : public Engine {
 
     // -------------------------------------------------------------- decoding options
     void set_decoding(int eot, const int* never, int n_never, const int* first, int n_first) override {
+        join_chains();
         WMI_HIP(hipStreamSynchronize(st_));
         const size_t words = (size_t)V_ / 32 + 1;
         std::vector<unsigned> a(words, 0u), b(words, 0u);
@@ -545,6 +587,7 @@ class EngineT final : public Engine {
     // returns the snapshot taken before the latest one (its copy has long
     // completed when the caller keeps one step ahead), or null.
     void stop_snapshot() override {
+        join_chains();
         const int b = (int)(snapshots_ & 1);
         if (!stop_pin_[b]) {
             WMI_HIP(hipHostMalloc(reinterpret_cast<void**>(&stop_pin_[b]), (size_t)S_ * sizeof(int)));
@@ -564,6 +607,7 @@ class EngineT final : public Engine {
 
     // -------------------------------------------------------------- debug
     void debug_copy(int tensor, int index, void* dst, size_t bytes) override {
+        join_chains();
         WMI_HIP(hipSetDevice(dev_));
         WMI_HIP(hipStreamSynchronize(st_));
         float* out = static_cast<float*>(dst);
@@ -606,18 +650,21 @@ class EngineT final : public Engine {
 
     // -------------------------------------------------------------- completion marks
     void mark_reset() override {
+        join_chains();
         for (auto e : marks_) event_pool_.push_back(e);
         marks_.clear();
         if (!mark_start_) mark_start_ = get_event();
         WMI_HIP(hipEventRecord(mark_start_, st_));
     }
     int mark() override {
+        join_chains();
         hipEvent_t e = get_event();
         WMI_HIP(hipEventRecord(e, st_));
         marks_.push_back(e);
         return (int)marks_.size() - 1;
     }
     std::vector<double> mark_times_us() override {
+        join_chains();
         WMI_HIP(hipStreamSynchronize(st_));
         if (ctc_st_) WMI_HIP(hipStreamSynchronize(ctc_st_));
         std::vector<double> t(marks_.size());
@@ -631,6 +678,7 @@ class EngineT final : public Engine {
 
     // -------------------------------------------------------------- profiling
     void profile_enable(int k, bool on) override {
+        join_chains();
         WMI_HIP(hipStreamSynchronize(st_));
         recycle(k);
         prof_[k].on = on;
@@ -638,6 +686,7 @@ class EngineT final : public Engine {
         prof_[k].launches = 0;
     }
     int encode_ctc(const SegmentDesc* segs, int n, int* mark_out) override {
+        join_chains();
         WMI_HIP(hipSetDevice(dev_));
         if (!ctc_) throw ArgError(WHISPER_E_STATE, "not a CTC model");
         if (n < 1 || n > EB_) throw ArgError(WHISPER_E_INVAL, "encode_ctc: 1..max_encode_batch segments");
@@ -655,6 +704,7 @@ class EngineT final : public Engine {
     }
 
     void read_ctc(int ticket, int n, int32_t* tokens, int32_t* counts) override {
+        join_chains();
         WMI_HIP(hipSetDevice(dev_));
         if (!ctc_ || n < 1 || n > EB_ || ticket < 0 || ticket < ctc_ticket_ - 2 || ticket >= ctc_ticket_)
             throw ArgError(WHISPER_E_INVAL, "read_ctc: one of the last two batches of a CTC model, 1..max_encode_batch entries");
@@ -665,6 +715,7 @@ class EngineT final : public Engine {
     }
 
     double time_cross_attn(int n, int reps) override {
+        join_chains();
         WMI_HIP(hipSetDevice(dev_));
         if (n < 1 || n > S_ || reps < 1) throw ArgError(WHISPER_E_INVAL, "time_cross_attn: n in 1..max_slots, reps >= 1");
         std::vector<int> rows(n);
@@ -691,6 +742,7 @@ class EngineT final : public Engine {
     }
 
     void profile_read(int k, double* ms, int64_t* launches) override {
+        join_chains();
         WMI_HIP(hipStreamSynchronize(st_));
         recycle(k);
         *ms = prof_[k].total_ms;
@@ -748,6 +800,8 @@ class EngineT final : public Engine {
     unsigned long long* best_;
     std::vector<int> list_host_;
     bool graphs_ = true, split_ = true, fused_ln_ = true;
+    bool free_run_ = true, chains_apart_ = false;
+    int apart_nc_ = 0;
     // prompt prefill: rows per chunk (the skinny projections take up to 128)
     // and the chunk's buffers; the list block is followed by the positions
     bool prefill_ = false;
