@@ -236,6 +236,7 @@ class EngineT final : public Engine {
         if (const char* g = getenv("WHISPER_STEP_CHAINS")) chains_ = std::max(1, std::min(MAXC, atoi(g)));
         if (const char* g = getenv("WHISPER_FUSED_LN")) fused_ln_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_FREE_CHAINS")) free_run_ = g[0] != '0';
+        if (const char* g = getenv("WHISPER_FC2_SPLIT")) fc2_split_ = atoi(g);
         load_weights(blob, bytes);
         alloc_state();
         WMI_HIP(hipDeviceSynchronize());
@@ -420,7 +421,8 @@ class EngineT final : public Engine {
     // norm of each row in b.dz.
     void decoder_layers(const RowBufs& b, int n, hipStream_t s) {
         const int d = d_;
-        const int ks1 = split_k(d), ks4 = split_k(4 * d);
+        const int ks1 = split_k(d);
+        const int ks4 = fc2_split_ == 8 && (4 * d / 32) % 8 == 0 ? 8 : split_k(4 * d);
         WMI_SWITCH_E(d, hipLaunchKernelGGL((embed_ln_kernel<T, E>), dim3(n), dim3(64), 0, s, tok_emb_, pos_emb_,
                                            b.list, pos_, b.rowpos, seq_, b.dx, b.dz, dec_[0].ln1g, dec_[0].ln1b));
         for (int l = 0; l < Ld_; ++l) {
@@ -461,7 +463,7 @@ class EngineT final : public Engine {
                         datt_ + (size_t)r0 * d,
                         dh_ + (size_t)r0 * 4 * d,
                         rowlen_ + r0,
-                        gpart_ + (size_t)c * 4 * S_ * d};
+                        gpart_ + (size_t)c * KSMAX * S_ * d};
         decoder_layers(b, n, s);
         const int* list = list_ + r0;
         float* logits = logits_ + (size_t)r0 * V_;
@@ -801,6 +803,8 @@ class EngineT final : public Engine {
     std::vector<int> list_host_;
     bool graphs_ = true, split_ = true, fused_ln_ = true;
     bool free_run_ = true, chains_apart_ = false;
+    static constexpr int KSMAX = 8;  // most split-K partials of a decode projection
+    int fc2_split_ = 8;  // split-K of fc2 (K = 4d) where 4d / 32 is a multiple of 8
     int apart_nc_ = 0;
     // prompt prefill: rows per chunk (the skinny projections take up to 128)
     // and the chunk's buffers; the list block is followed by the positions
@@ -918,7 +922,10 @@ class EngineT final : public Engine {
     // decoder: x += split-K partials + bias, then z = LN(x)
     void resid_ln(int KS, int n, const float* bias, const float* g, const float* b, float* part, float* dx, T* dz,
                   hipStream_t s) {
-        if (KS == 4) {
+        if (KS == 8) {
+            WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 8>), dim3(n), dim3(resid_ln_threads<E>()), 0,
+                                                s, part, n, bias, dx, dz, g, b));
+        } else if (KS == 4) {
             WMI_SWITCH_E(d_, hipLaunchKernelGGL((resid_ln_kernel<T, E, 4>), dim3(n), dim3(resid_ln_threads<E>()), 0,
                                                 s, part, n, bias, dx, dz, g, b));
         } else {
@@ -1240,7 +1247,7 @@ class EngineT final : public Engine {
         datt_ = dalloc<T>(S16 * d);
         dh_ = dalloc<T>(S16 * 4 * d);
         logits_ = dalloc<float>(S * (size_t)V_);
-        gpart_ = dalloc<float>((size_t)MAXC * 4 * S * d);  // split-K partials [chain][4][rows][d]
+        gpart_ = dalloc<float>((size_t)MAXC * KSMAX * S * d);  // split-K partials [chain][KS][rows][d]
         best_ = dalloc<unsigned long long>(S);
         if (prefill_) {
             pf_cap_ = 128;
@@ -1251,7 +1258,7 @@ class EngineT final : public Engine {
             pf_dq_ = dalloc<T>((size_t)pf_cap_ * d);
             pf_datt_ = dalloc<T>((size_t)pf_cap_ * d);
             pf_dh_ = dalloc<T>((size_t)pf_cap_ * 4 * d);
-            pf_part_ = dalloc<float>((size_t)4 * pf_cap_ * d);
+            pf_part_ = dalloc<float>((size_t)KSMAX * pf_cap_ * d);
         }
         if (ctc_) {
             ctc_logits_ = dalloc<float>(EB * N_CTX * (size_t)V_);
