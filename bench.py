@@ -102,7 +102,7 @@ def counter_traffic(workload):
 
 
 def cpu_baseline(shape, W, segs):
-    """The oracle, as is, on a bounded sample (about 10 s of CPU work on
+    """The oracle, as is, on a bounded sample (about 11 s of CPU work on
     large-v3 shapes on a 16-thread host): one segment's front end, conv stem, NL encoder layers,
     NL layers of cross-attention keys/values and three decode steps of an
     NL-layer decoder (plus the output head alone), extrapolated per layer to
@@ -122,7 +122,7 @@ def cpu_baseline(shape, W, segs):
     t = time.perf_counter()
     x = M.conv_stem(W, mel[None]) + M.sinusoid_pe(1500, shape.d)[None]
     t_stem = time.perf_counter() - t
-    NL = min(16, shape.n_enc, shape.n_dec)
+    NL = min(20, shape.n_enc, shape.n_dec)
     shl = shape.with_(n_enc=NL, n_dec=NL)
     t = time.perf_counter()
     E = M.encoder(W, shl, mel[None])
