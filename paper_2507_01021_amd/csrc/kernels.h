@@ -1029,8 +1029,8 @@ struct EpiResidX {
 // residual stream x (row-major, width d = 64 E; fp32 mean, then biased
 // variance about it, eps 1e-5, gain and bias), rounds them to bf16 and keeps
 // them in LDS in the MFMA's B-operand fragment layout. Its weight loads (W
-// fragment-major, one batch covering each wave's k-steps) are issued first,
-// so they overlap the normalisation. The NW waves take interleaved 32-wide
+// fragment-major, one batch covering each wave's k-steps) are issued right
+// after the row loads, so they are in flight during the normalisation. The NW waves take interleaved 32-wide
 // k-steps and are summed in LDS in a fixed order: a row's result depends on
 // that row alone. Rows past n are zero and dropped.
 namespace sln {
@@ -1050,24 +1050,26 @@ __global__ __launch_bounds__(64 * sln::NW) void skinny_ln_kernel(const bf16* __r
     const int fr = lane & 15, fc = lane >> 4;
     const int i0 = blockIdx.x * 16 * RT, r0 = blockIdx.y * 16;
     EpiPre pre[RT];
-    if (wave == 0) {
+    mfma_bf16x8 a[U][RT];
+    float v[RPW][CH][8], gg[CH][8], bb[CH][8];
+    // Loads in the order they are needed (the vector-memory counter retires
+    // them in issue order): this wave's rows (lane holds 8-column chunks
+    // lane, lane + 64, ...), then gain and bias, so the normalisation starts
+    // while the weights are still in flight; then the weights, then the
+    // epilogue's operands.
 #pragma unroll
-        for (int t = 0; t < RT; ++t) {
-            const int i = i0 + t * 16 + fc * 4, r = r0 + fr;
-            if (i < MA && r < n) pre[t] = epi.pre(i, r, 0);
+    for (int rr = 0; rr < RPW; ++rr) {
+        const int R = r0 + wave * RPW + rr;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int c8 = lane + 64 * c;
+            const bool ok = R < n && c8 < NC;
+            const float* xp = x + (long long)R * d + 8 * c8;
+            const float4 x0 = ok ? ld4(xp) : float4{}, x1 = ok ? ld4(xp + 4) : float4{};
+            v[rr][c][0] = x0.x; v[rr][c][1] = x0.y; v[rr][c][2] = x0.z; v[rr][c][3] = x0.w;
+            v[rr][c][4] = x1.x; v[rr][c][5] = x1.y; v[rr][c][6] = x1.z; v[rr][c][7] = x1.w;
         }
     }
-    mfma_bf16x8 a[U][RT];
-#pragma unroll
-    for (int q = 0; q < U; ++q) {
-        const int st = min(wave + NW * q, nks - 1);
-#pragma unroll
-        for (int t = 0; t < RT; ++t)
-            a[q][t] = *reinterpret_cast<const mfma_bf16x8*>(
-                W + (((long long)(blockIdx.x * RT + t) * nks + st) * 64 + lane) * 8);
-    }
-    // This wave's rows: lane holds 8-column chunks lane, lane + 64, ...
-    float v[RPW][CH][8], gg[CH][8], bb[CH][8];
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
         const int c8 = lane + 64 * c;
@@ -1080,16 +1082,18 @@ __global__ __launch_bounds__(64 * sln::NW) void skinny_ln_kernel(const bf16* __r
         bb[c][4] = b1.x; bb[c][5] = b1.y; bb[c][6] = b1.z; bb[c][7] = b1.w;
     }
 #pragma unroll
-    for (int rr = 0; rr < RPW; ++rr) {
-        const int R = r0 + wave * RPW + rr;
+    for (int q = 0; q < U; ++q) {
+        const int st = min(wave + NW * q, nks - 1);
 #pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int c8 = lane + 64 * c;
-            const bool ok = R < n && c8 < NC;
-            const float* xp = x + (long long)R * d + 8 * c8;
-            const float4 x0 = ok ? ld4(xp) : float4{}, x1 = ok ? ld4(xp + 4) : float4{};
-            v[rr][c][0] = x0.x; v[rr][c][1] = x0.y; v[rr][c][2] = x0.z; v[rr][c][3] = x0.w;
-            v[rr][c][4] = x1.x; v[rr][c][5] = x1.y; v[rr][c][6] = x1.z; v[rr][c][7] = x1.w;
+        for (int t = 0; t < RT; ++t)
+            a[q][t] = *reinterpret_cast<const mfma_bf16x8*>(
+                W + (((long long)(blockIdx.x * RT + t) * nks + st) * 64 + lane) * 8);
+    }
+    if (wave == 0) {
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+            const int i = i0 + t * 16 + fc * 4, r = r0 + fr;
+            if (i < MA && r < n) pre[t] = epi.pre(i, r, 0);
         }
     }
 #pragma unroll
