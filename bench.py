@@ -177,12 +177,97 @@ def cpu_baseline_ctc(shape, W, segs):
             "sample": f"the first {done} segments, each through the whole CTC oracle ({spent:.1f} s of CPU work)"}
 
 
+def run_decoder_workload(binding, torch, name, steps, warmup, pad_mode=0, encode_batch=0, prefill=0, max_new=0,
+                         per_kernel=True):
+    """Times `steps` whisper_batch_transcribe calls over the workload (after
+    `warmup` calls), with HIP events around every encode pass in the same
+    calls; the decode steps are the rest of the calls' wall time. Returns
+    (result dict, context, model shape, weights, segments, slots, device
+    audio pointers, audio seconds)."""
+    from paper_2507_01021_amd import synth
+
+    shape, segs, slots = synth.workload(name)
+    if max_new:
+        for s in segs:
+            s.max_new_tokens = max_new
+    W = synth.make_weights(shape, 0)
+    blob = synth.pack_blob(W)
+    dev_audio = [torch.from_numpy(s.audio).to("cuda:0") for s in segs]
+    ptrs = [t.data_ptr() for t in dev_audio]
+    eb = encode_batch or min(slots, 32)
+    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=eb, pad_mode=pad_mode,
+                          prefill=prefill if shape.n_dec else 0)
+    del blob
+    ctx._keep = dev_audio
+    audio_s = sum(s.seconds for s in segs)
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        ctx.transcribe(segs, device_audio=ptrs)
+    torch.cuda.synchronize()
+    ctx.stats(reset=True)
+    ctx.profile_enable(binding.K_ENC_PASS, True)        # events around each encode pass, decode steps unchanged
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        res = ctx.transcribe(segs, device_audio=ptrs)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st = ctx.stats(reset=True)
+    enc_ms, enc_n = ctx.profile_read(binding.K_ENC_PASS)
+    ctx.profile_enable(binding.K_ENC_PASS, False)
+    assert enc_n == st["encode_passes"]
+    assert all(r["status"] == 0 and r["tokens"].size == s.max_new_tokens for r, s in zip(res, segs))
+    fl = encoder_flops(shape) * len(segs) * steps
+    peak_f = PEAK_BF16 if shape.dtype == "bf16" else PEAK_F32
+    enc = {"ms_per_pass": round(enc_ms / max(enc_n, 1), 3), "passes": enc_n,
+           "tflops": round(fl / (enc_ms / 1e3) / 1e12, 1), "mfma_frac": round(fl / (enc_ms / 1e3) / peak_f, 4)}
+    # decode: the timed calls' wall time minus their encode passes (same calls)
+    dec_wall_ms = wall * 1e3 - enc_ms
+    db = decode_bytes(shape, st)
+    dec = {"ms_per_step": round(dec_wall_ms / max(st["decode_steps"], 1), 3), "steps": st["decode_steps"],
+           "gbps": round(db / (dec_wall_ms / 1e3) / 1e9, 1), "hbm_frac": round(db / (dec_wall_ms / 1e3) / PEAK_HBM, 4),
+           "bytes_per_step": round(db / max(st["decode_steps"], 1)),
+           "avg_active_slots": round(st["rows_decoded"] / max(st["decode_steps"], 1), 2)}
+    batcher = {"refill_batches_per_call": st["refill_batches"] // steps,
+               "host_ms_per_refill": round(st["batcher_host_ms"] / max(st["refill_batches"], 1), 4),
+               "host_ms_per_call": round(st["batcher_host_ms"] / steps, 3),
+               "engine_host_ms_per_call": round(st["engine_host_ms"] / steps, 2)}
+    out = {"value": round(audio_s * steps / wall, 2), "ms_per_call": round(wall / steps * 1e3, 2),
+           "encoder": enc, "decode": dec, "batcher": batcher,
+           "padded_rtfx": round(30.0 * len(segs) * steps / wall, 2)}
+    if per_kernel:
+        # Per-kernel timing: the same calls again with HIP events around every
+        # launch of the named kernels (decode steps then run as individual
+        # launches, unsplit, instead of captured graphs)
+        kinds = (binding.K_DEC_STEP, binding.K_ENC_GEMM, binding.K_FRONT_END)
+        for k in kinds:
+            ctx.profile_enable(k, True)
+        t1 = time.perf_counter()
+        for _ in range(steps):
+            ctx.transcribe(segs, device_audio=ptrs)
+        torch.cuda.synchronize()
+        wall_timed = time.perf_counter() - t1
+        prof = {k: ctx.profile_read(k) for k in kinds}
+        for k in kinds:
+            ctx.profile_enable(k, False)
+        fe_ms, fe_n = prof[binding.K_FRONT_END]
+        enc["front_end_ms_per_pass"] = round(fe_ms / max(fe_n, 1), 3)
+        g_ms, g_n = prof[binding.K_ENC_GEMM]
+        fc1_flops = 2 * 1500 * shape.d * 4 * shape.d * len(segs) * shape.n_enc * steps
+        enc["fc1_gemm_tflops"] = round(fc1_flops / (g_ms / 1e3) / 1e12, 1) if g_ms > 0 else None
+        d_ms, d_n = prof[binding.K_DEC_STEP]
+        dec["ms_per_step_kernel_timed"] = round(d_ms / max(d_n, 1), 3)
+        dec["ms_per_call_kernel_timed"] = round(wall_timed / steps * 1e3, 2)
+    return out, ctx, shape, W, segs, slots, ptrs, audio_s
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="large-v3-b32")
+    ap.add_argument("--secondary", default="turbo-u64-q512",
+                    help="refill workload measured after the headline one in the same run ('' to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
@@ -208,48 +293,10 @@ def main():
 
     from paper_2507_01021_amd import binding, synth
 
-    shape, segs, slots = synth.workload(a.workload)
-    if a.max_new:
-        for s in segs:
-            s.max_new_tokens = a.max_new
-    W = synth.make_weights(shape, 0)
-    blob = synth.pack_blob(W)
-    dev_audio = [torch.from_numpy(s.audio).to("cuda:0") for s in segs]
-    ptrs = [t.data_ptr() for t in dev_audio]
-    eb = a.encode_batch or min(slots, 32)
-    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=eb, pad_mode=a.pad_mode,
-                          ctc_beam=a.ctc_beam, prefill=a.prefill if shape.n_dec else 0)
-    del blob
-    audio_s = sum(s.seconds for s in segs)
-    torch.cuda.synchronize()
-    for _ in range(a.warmup):
-        ctx.transcribe(segs, device_audio=ptrs)
-    torch.cuda.synchronize()
-    ctx.stats(reset=True)
-    t0 = time.perf_counter()
-    for _ in range(a.steps):
-        res = ctx.transcribe(segs, device_audio=ptrs)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    st_timed = ctx.stats(reset=True)
-    ctc = shape.n_dec == 0
-    assert all(r["status"] == 0 and (r["tokens"].size <= s.max_new_tokens if ctc else r["tokens"].size == s.max_new_tokens)
-               for r, s in zip(res, segs))
-    if ctc:
-        return bench_ctc(a, ctx, shape, W, segs, slots, ptrs, audio_s, wall, st_timed)
-    # Per-kernel timing: the same steps again with HIP events around every
-    # launch of the named kernels on the library's stream (decode steps then
-    # run as individual launches instead of one captured graph per step).
-    kinds = (binding.K_ENC_PASS, binding.K_DEC_STEP, binding.K_ENC_GEMM, binding.K_FRONT_END)
-    for k in kinds:
-        ctx.profile_enable(k, True)
-    t1 = time.perf_counter()
-    for _ in range(a.steps):
-        ctx.transcribe(segs, device_audio=ptrs)
-    torch.cuda.synchronize()
-    wall_timed = time.perf_counter() - t1
-    prof = {k: ctx.profile_read(k) for k in kinds}
-    st = ctx.stats(reset=True)
+    if synth.workload(a.workload)[0].n_dec == 0:
+        return bench_ctc(a, binding, torch)
+    r, ctx, shape, W, segs, slots, ptrs, audio_s = run_decoder_workload(
+        binding, torch, a.workload, a.steps, a.warmup, a.pad_mode, a.encode_batch, a.prefill, a.max_new)
     copy_gbps = copy_ceiling_gbps(torch)
 
     if a.calib_copy_mib:
@@ -263,7 +310,6 @@ def main():
     # back-to-back launches over all of the workload's slots (their caches
     # hold the last pass's encoder output), two events on the library's
     # stream around 4 launches per decoder layer
-    n_active_avg = st["rows_decoded"] / max(st["decode_steps"], 1)
     ca_rows, ca_n = slots, 4 * shape.n_dec
     ca_avg_s = ctx.time_kernel(binding.K_CROSS_ATTN, ca_rows, ca_n) / 1e6
     ca_bytes = ca_rows * shape.d * 1500 * 2 * (2 if shape.dtype == "bf16" else 4)
@@ -274,65 +320,62 @@ def main():
             "bytes_per_launch": ca_bytes, "avg_launch_us": round(ca_avg_s * 1e6, 2), "launches": ca_n,
             "rows_per_launch": ca_rows,
             "measured_copy_gbps": copy_gbps}
+    ctx.close()
 
-    enc_ms, enc_n = prof[binding.K_ENC_PASS]
-    dec_ms, dec_n = prof[binding.K_DEC_STEP]
-    fl = encoder_flops(shape) * len(segs) * a.steps
-    peak_f = PEAK_BF16 if shape.dtype == "bf16" else PEAK_F32
-    fe_ms, fe_n = prof[binding.K_FRONT_END]
-    enc = {"ms_per_pass": round(enc_ms / max(enc_n, 1), 3), "passes": enc_n,
-           "tflops": round(fl / (enc_ms / 1e3) / 1e12, 1), "mfma_frac": round(fl / (enc_ms / 1e3) / peak_f, 4),
-           "front_end_ms_per_pass": round(fe_ms / max(fe_n, 1), 3)}
-    g_ms, g_n = prof[binding.K_ENC_GEMM]
-    fc1_flops = 2 * 1500 * shape.d * 4 * shape.d * len(segs) * shape.n_enc * a.steps
-    enc["fc1_gemm_tflops"] = round(fc1_flops / (g_ms / 1e3) / 1e12, 1) if g_ms > 0 else None
-    # decode in the timed configuration (captured graphs, split steps): the
-    # call's wall time minus its encode passes (timed separately below)
-    enc_pass_ms = enc_ms / max(enc_n, 1)
-    dec_wall_ms = wall * 1e3 - st_timed["encode_passes"] * enc_pass_ms
-    db = decode_bytes(shape, st_timed)
-    dec = {"ms_per_step": round(dec_wall_ms / max(st_timed["decode_steps"], 1), 3),
-           "steps": st_timed["decode_steps"],
-           "gbps": round(db / (dec_wall_ms / 1e3) / 1e9, 1),
-           "hbm_frac": round(db / (dec_wall_ms / 1e3) / PEAK_HBM, 4),
-           "avg_active_slots": round(n_active_avg, 2),
-           # the same steps launched one kernel at a time, unsplit, with HIP
-           # events around every timed kernel (the per-kernel timing pass)
-           "ms_per_step_kernel_timed": round(dec_ms / max(dec_n, 1), 3),
-           "ms_per_call_kernel_timed": round(wall_timed / a.steps * 1e3, 2)}
-    batcher = {"refill_batches_per_call": st_timed["refill_batches"] // a.steps,
-               "host_ms_per_refill": round(st_timed["batcher_host_ms"] / max(st_timed["refill_batches"], 1), 4),
-               "host_ms_per_call": round(st_timed["batcher_host_ms"] / a.steps, 3),
-               "engine_host_ms_per_call": round(st_timed["engine_host_ms"] / a.steps, 2)}
-
-    value = audio_s * a.steps / wall
     out = {
         "metric": "audio-sec transcribed/sec (RTFx) at batch B; encoder MFMA util; decode HBM GB/s",
-        "value": round(value, 2), "unit": "audio-s/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
-        "ms_per_step": round(wall / a.steps * 1e3, 2), "higher_is_better": True, "scaling": "weak",
+        "value": r["value"], "unit": "audio-s/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": r["ms_per_call"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": shape.dtype, "data": "synthetic",
         "config": {"workload": a.workload, "segments": len(segs), "slots": slots,
                    "new_tokens": [int(min(s.max_new_tokens for s in segs)), int(max(s.max_new_tokens for s in segs))],
                    "audio_s": round(audio_s, 2), "weights_seed": 0, "workload_seed": 1,
-                   "pad_mode": a.pad_mode, "prefill": a.prefill, "encode_batch": eb},
-        "roofline": roof, "encoder": enc, "decode": dec, "batcher": batcher,
+                   "pad_mode": a.pad_mode, "prefill": a.prefill, "encode_batch": a.encode_batch or min(slots, 32)},
+        "roofline": roof, "encoder": r["encoder"], "decode": r["decode"], "batcher": r["batcher"],
         # every segment is encoded as a full 30 s window: RTFx over padded seconds
-        "padded_rtfx": round(30.0 * len(segs) * a.steps / wall, 2),
+        "padded_rtfx": r["padded_rtfx"],
     }
+    if a.secondary and a.secondary != a.workload and not a.max_new:
+        # the refill workload (continuous batching with slot refill), one
+        # timed call after one warm-up call, same accounting
+        r2, ctx2, shape2, _, segs2, slots2, _, audio2 = run_decoder_workload(
+            binding, torch, a.secondary, 1, 1, a.pad_mode, 0, a.prefill, 0, per_kernel=False)
+        ctx2.close()
+        out["secondary"] = {"workload": a.secondary, "segments": len(segs2), "slots": slots2,
+                            "audio_s": round(audio2, 2), "value": r2["value"], "unit": "audio-s/s",
+                            "ms_per_call": r2["ms_per_call"], "encoder": r2["encoder"], "decode": r2["decode"]}
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, W, segs)
-    ctx.close()
     print(json.dumps(out), flush=True)
 
 
-def bench_ctc(a, ctx, shape, W, segs, slots, ptrs, audio_s, wall, st_timed):
+def bench_ctc(a, binding, torch):
     """Encoder-only CTC workload: the queue in encoder passes; its roofline is
     the encoder's fc1 GEMM (MFMA-bound), timed with HIP events around every
     launch in a second run of the same calls."""
-    import torch
+    from paper_2507_01021_amd import synth
 
-    from paper_2507_01021_amd import binding
-
+    shape, segs, slots = synth.workload(a.workload)
+    W = synth.make_weights(shape, 0)
+    blob = synth.pack_blob(W)
+    dev_audio = [torch.from_numpy(s.audio).to("cuda:0") for s in segs]
+    ptrs = [t.data_ptr() for t in dev_audio]
+    ctx = binding.Context(blob, max_slots=slots, max_encode_batch=a.encode_batch or min(slots, 32),
+                          pad_mode=a.pad_mode, ctc_beam=a.ctc_beam)
+    del blob
+    audio_s = sum(s.seconds for s in segs)
+    torch.cuda.synchronize()
+    for _ in range(a.warmup):
+        ctx.transcribe(segs, device_audio=ptrs)
+    torch.cuda.synchronize()
+    ctx.stats(reset=True)
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        res = ctx.transcribe(segs, device_audio=ptrs)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st_timed = ctx.stats(reset=True)
+    assert all(r["status"] == 0 and r["tokens"].size <= s.max_new_tokens for r, s in zip(res, segs))
     kinds = (binding.K_ENC_PASS, binding.K_ENC_GEMM, binding.K_FRONT_END)
     for k in kinds:
         ctx.profile_enable(k, True)

@@ -400,6 +400,20 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
                                     int64_t encode_us, int64_t step_us, int32_t eot,
                                     int32_t batch_policy, int64_t step_cost_us, int64_t max_wait_us);
 
+/*
+ * Host-only check of the greedy choice's arithmetic (no device work): the
+ * same 64-bit keys the decode step's kernels compare (value bits mapped to
+ * an order-preserving integer, then the complement of the id, so the largest
+ * key is the largest logit and, among equal logits, the lowest id; Listing
+ * 1's generate read as greedy search). For each of `rows` rows of n_vocab
+ * fp32 logits (host, row-major), ids whose bit is set in `excluded` (host,
+ * n_vocab / 32 + 1 words, or NULL) are skipped; tokens[r] receives the
+ * chosen id, or 0 with no_token[r] = 1 when no id is admissible (the decode
+ * step then fails with WHISPER_E_DEVICE). Errors: WHISPER_E_INVAL.
+ */
+whisper_status whisper_test_greedy_keys(const float* logits, int32_t rows, int32_t n_vocab,
+                                        const uint32_t* excluded, int32_t* tokens, int32_t* no_token);
+
 #ifdef __cplusplus
 }
 #endif

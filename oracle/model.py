@@ -224,14 +224,16 @@ def pick_token(logits, step, suppress=(), suppress_begin=()):
 
 
 def greedy(W, shape, ckv_seg, prompt, n_new, forced=None, cached=True, eot=None, suppress=(),
-           suppress_begin=()):
+           suppress_begin=(), progress=None):
     """Greedy decode of up to n_new tokens after the prompt.
 
     Token 1 is the choice (pick_token) at the prompt's last position; token
     i+1 the choice after feeding token i (or forced[i-1] when teacher
     forcing). Decoding stops early when the choice is `eot` (end of text,
     not returned). Returns (tokens int64, logits float64): one logits row
-    per choice made, i.e. one more row than tokens when stopped by eot."""
+    per choice made, i.e. one more row than tokens when stopped by eot.
+    progress, if given, is called with the number of choices made so far
+    after each one (it takes no part in the computation)."""
     prompt = [int(t) for t in prompt]
     if len(prompt) < 1 or len(prompt) + n_new > shape.n_text_ctx:
         raise ValueError("prompt length + n_new must fit the text context")
@@ -245,6 +247,8 @@ def greedy(W, shape, ckv_seg, prompt, n_new, forced=None, cached=True, eot=None,
             lg = decoder_step(W, shape, nxt, cache, ckv_seg)
             g = pick_token(lg, i, suppress, suppress_begin)
             logits.append(lg)
+            if progress:
+                progress(i + 1)
             if eot is not None and g == eot:
                 break
             toks.append(g)

@@ -23,7 +23,7 @@ EXPORTS = (
     "whisper_ctx_set_stream", "whisper_batch_encode", "whisper_batch_decode_step",
     "whisper_slot_tokens", "whisper_batch_transcribe", "whisper_batch_serve", "whisper_debug_copy",
     "whisper_profile_enable", "whisper_profile_read", "whisper_time_kernel", "whisper_stats_read",
-    "whisper_set_decoding", "whisper_test_batcher",
+    "whisper_set_decoding", "whisper_test_batcher", "whisper_test_greedy_keys",
 )
 
 
@@ -89,6 +89,7 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "whisper_test_batcher": (i32, [i32, C.POINTER(i64), pi32, C.POINTER(i64), pi32, i32, i32, i32,
                                       pi32, i64, C.POINTER(whisper_result), pi32, i32, pi32, i32, i64, i64, i32,
                                       i32, i64, i64]),
+        "whisper_test_greedy_keys": (i32, [C.POINTER(C.c_float), i32, i32, C.POINTER(C.c_uint32), pi32, pi32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -288,3 +289,24 @@ def test_batcher(arrival_us, user_id, segment_id, max_new_tokens, slots, encode_
         return buf[:total], results, ev[: 3 * min(ne.value, events_cap)].reshape(-1, 3), \
             [res[i].finish_us for i in range(n)]
     return buf[:total], results, ev[: 3 * min(ne.value, events_cap)].reshape(-1, 3)
+
+
+def test_greedy_keys(logits, excluded_ids=()):
+    """The greedy choice of every row of `logits` [rows, n_vocab] computed on
+    the host with the decode step's key arithmetic; ids in excluded_ids are
+    skipped. Returns (tokens, no_token flags)."""
+    lib = load()
+    lg = np.ascontiguousarray(logits, dtype=np.float32)
+    rows, V = lg.shape
+    mask = None
+    if len(excluded_ids):
+        m = np.zeros(V // 32 + 1, dtype=np.uint32)
+        for i in excluded_ids:
+            m[i >> 5] |= np.uint32(1 << (i & 31))
+        mask = m
+    tok = np.zeros(max(1, rows), dtype=np.int32)
+    bad = np.zeros(max(1, rows), dtype=np.int32)
+    _check(lib.whisper_test_greedy_keys(_ptr(lg, C.c_float), rows, V,
+                                        None if mask is None else _ptr(mask, C.c_uint32),
+                                        _ptr(tok, C.c_int32), _ptr(bad, C.c_int32)))
+    return tok[:rows], bad[:rows]

@@ -717,4 +717,12 @@ whisper_status whisper_test_batcher(int32_t n, const int64_t* arrival_us, const 
     return WHISPER_OK;
 }
 
+whisper_status whisper_test_greedy_keys(const float* logits, int32_t rows, int32_t n_vocab,
+                                        const uint32_t* excluded, int32_t* tokens, int32_t* no_token) {
+    if (rows < 0 || n_vocab < 1 || (rows > 0 && (!logits || !tokens || !no_token)))
+        return fail(nullptr, WHISPER_E_INVAL, "bad arguments");
+    wmi::greedy_keys_host(logits, rows, n_vocab, excluded, tokens, no_token);
+    return WHISPER_OK;
+}
+
 }  // extern "C"

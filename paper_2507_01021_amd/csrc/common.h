@@ -128,14 +128,16 @@ __device__ inline float wave_max(float v) {
     return v;
 }
 
-// Order-preserving map of fp32 to uint32 (for atomic max of floats).
-__device__ inline uint32_t f2ord(float f) {
-    uint32_t u = __float_as_uint(f);
+// Order-preserving map of fp32 to uint32: a < b as floats (not NaN) iff
+// f2ord(a) < f2ord(b) as integers. Host and device (the greedy-choice keys
+// are checked on the host too).
+__host__ __device__ inline uint32_t f2ord(float f) {
+    const uint32_t u = __builtin_bit_cast(uint32_t, f);
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
-__device__ inline float ord2f(uint32_t o) {
-    uint32_t u = (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o;
-    return __uint_as_float(u);
+__host__ __device__ inline float ord2f(uint32_t o) {
+    const uint32_t u = (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o;
+    return __builtin_bit_cast(float, u);
 }
 
 // MFMA operand vectors.

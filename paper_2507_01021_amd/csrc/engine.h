@@ -81,6 +81,10 @@ class Engine {
 // Throws ArgError (code = whisper_status) or DeviceError.
 std::unique_ptr<Engine> make_engine(const whisper_params& p, const void* blob, size_t bytes, int device);
 
+// Host run of the device's greedy-choice keys (largest logit, lowest id on
+// ties, excluded ids skipped, token 0 and bad[r] = 1 for a row with none).
+void greedy_keys_host(const float* logits, int rows, int V, const unsigned* excluded, int* tokens, int* bad);
+
 // Blob header check; fills the model fields of *out. Returns a whisper_status.
 int parse_blob_header(const void* blob, size_t bytes, whisper_params* out, const char** why);
 

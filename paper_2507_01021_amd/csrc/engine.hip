@@ -25,8 +25,8 @@
 //   halves touch disjoint slots), so the two chains of small latency-bound
 //   kernels overlap. While the slot list stays the same the chains are not
 //   joined between steps (one may run a step ahead of the other); any other
-//   call joins them first. Steps with kernel timing on run unsplit, so each
-//   timed launch has the device to itself.
+//   call joins them first. Steps with decode-kernel timing on run unsplit, so
+//   each timed launch has the device to itself.
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
@@ -317,8 +317,10 @@ class EngineT final : public Engine {
                      bool sync_) override {
         WMI_HIP(hipSetDevice(dev_));
         const bool same_list = n == (int)list_host_.size() && std::equal(slots, slots + n, list_host_.begin());
-        bool timed = false;
-        for (auto& pr : prof_) timed = timed || pr.on;
+        // timing of a decode kernel (or of the whole step) brackets each launch
+        // with events: such steps run as plain launches, unsplit; encoder
+        // timings leave the steps as they are
+        const bool timed = prof_[WHISPER_K_CROSS_ATTN].on || prof_[WHISPER_K_SELF_ATTN].on || prof_[WHISPER_K_DEC_STEP].on;
         const bool plain = graphs_ && !forced && !out_tok && !out_logits && !timed && !sync_;
         if (free_run_ && plain && same_list && chains_apart_) {
             // the chains keep running on their own streams: no fork, no join
@@ -351,12 +353,13 @@ class EngineT final : public Engine {
             if (it == step_graphs_.end()) {
                 std::array<hipGraphExec_t, MAXC> ge{};
                 for (int c = 0; c < nc; ++c)
-                    ge[c] = capture(stream(c), [&] { launch_rows(r0[c], r0[c + 1] - r0[c], false, stream(c), c); });
+                    ge[c] = capture(stream(c), [&] { launch_rows(r0[c], r0[c + 1] - r0[c], false, false, stream(c), c); });
                 it = step_graphs_.emplace(n, ge).first;
             }
             for (int c = 0; c < nc; ++c) WMI_HIP(hipGraphLaunch(it->second[c], stream(c)));
         } else {
-            for (int c = 0; c < nc; ++c) launch_rows(r0[c], r0[c + 1] - r0[c], forced != nullptr, stream(c), c);
+            for (int c = 0; c < nc; ++c)
+                launch_rows(r0[c], r0[c + 1] - r0[c], forced != nullptr, out_logits != nullptr, stream(c), c);
         }
         if (free_run_ && plain && nc > 1) {  // stay apart until something needs the results
             chains_apart_ = true;
@@ -372,7 +375,10 @@ class EngineT final : public Engine {
         if (out_tok) WMI_HIP(hipMemcpyAsync(out_tok, outtok_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
         if (out_logits)
             WMI_HIP(hipMemcpyAsync(out_logits, logits_, (size_t)n * V_ * sizeof(float), hipMemcpyDeviceToHost, st_));
-        if (sync_ || out_tok || out_logits || forced) WMI_HIP(hipStreamSynchronize(st_));
+        if (sync_ || out_tok || out_logits || forced) {
+            WMI_HIP(hipStreamSynchronize(st_));
+            check_decode_error();
+        }
     }
 
     // Rows of a step of n rows cut into chains (independent launch
@@ -453,26 +459,57 @@ class EngineT final : public Engine {
     // on stream s, with chain c's split-K partial buffer. r0 is a multiple
     // of 16, so the fragment-major activations of these rows start at
     // element r0 * K.
-    void launch_rows(int r0, int n, bool forced, hipStream_t s, int c) {
+    void launch_rows(int r0, int n, bool forced, bool want_logits, hipStream_t s, int c) {
         const int d = d_;
-        const RowBufs b{list_ + r0,
-                        nullptr,
-                        dx_ + (size_t)r0 * d,
-                        dz_ + (size_t)r0 * d,
-                        dq_ + (size_t)r0 * d,
-                        datt_ + (size_t)r0 * d,
-                        dh_ + (size_t)r0 * 4 * d,
-                        rowlen_ + r0,
-                        gpart_ + (size_t)c * KSMAX * S_ * d};
+        const StepBufs b{RowBufs{list_ + r0, nullptr, dx_ + (size_t)r0 * d, dz_ + (size_t)r0 * d,
+                                 dq_ + (size_t)r0 * d, datt_ + (size_t)r0 * d, dh_ + (size_t)r0 * 4 * d,
+                                 rowlen_ + r0, gpart_ + (size_t)c * KSMAX * S_ * d},
+                         logits_ + (size_t)r0 * V_, keys_ + (size_t)r0 * nkeys_, outtok_ + r0,
+                         forced ? forced_ + r0 : nullptr};
+        run_step(b, n, want_logits, s);
+    }
+
+    // Buffers of one step's rows: the decoder rows, the logits (fp32 model:
+    // always written; bf16: when asked for), greedy-choice keys, tokens out
+    // and forced tokens in (or null).
+    struct StepBufs {
+        RowBufs rows;
+        float* logits;
+        unsigned long long* keys;
+        int* outtok;
+        const int* forced;
+    };
+
+    // Every kernel of one decode step for n rows, on stream s.
+    void run_step(const StepBufs& sb, int n, bool want_logits, hipStream_t s) {
+        const int d = d_;
+        const RowBufs& b = sb.rows;
         decoder_layers(b, n, s);
-        const int* list = list_ + r0;
-        float* logits = logits_ + (size_t)r0 * V_;
-        unsigned long long* best = best_ + r0;
-        proj(tok_emb_, V_, b.dz, n, d, 1, EpiLogits{logits, V_}, s);
+        const int* list = b.list;
+        float* logits = sb.logits;
+        unsigned long long* keys = sb.keys;
         const TokenFilter tf{use_never_ ? never_mask_ : nullptr, use_first_ ? first_mask_ : nullptr, list, pos_, npr_};
-        hipLaunchKernelGGL(argmax_partial_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, s, logits, V_, best, tf);
-        hipLaunchKernelGGL(argmax_step_kernel, dim3((n + 63) / 64), dim3(64), 0, s, best, n, list, pos_, npr_, seq_,
-                           gen_, forced ? forced_ + r0 : nullptr, outtok_ + r0, eot_, stop_at_);
+        int nk = ARGMAX_CHUNKS;
+        if constexpr (std::is_same<T, bf16>::value) {
+            // the head kernel keeps one key per row and workgroup; logits only when asked for
+            nk = head_argmax(tok_emb_, V_, b.dz, n, d, HeadArgs{want_logits ? logits : nullptr, keys, V_, tf}, s);
+        } else {
+            proj(tok_emb_, V_, b.dz, n, d, 1, EpiLogits{logits, V_}, s);
+            hipLaunchKernelGGL(argmax_keys_kernel, dim3(ARGMAX_CHUNKS, n), dim3(256), 0, s, logits, V_, keys, tf);
+        }
+        hipLaunchKernelGGL(argmax_step_kernel, dim3(n), dim3(64), 0, s, keys, nk, list, pos_, npr_, seq_, gen_,
+                           sb.forced, sb.outtok, eot_, stop_at_, dec_err_);
+    }
+
+    // Raises the device-side decode error flag (a row without an admissible
+    // token) as an error of the call that synchronised; clears it.
+    void check_decode_error() {
+        int e = 0;
+        WMI_HIP(hipMemcpy(&e, dec_err_, sizeof(int), hipMemcpyDeviceToHost));
+        if (e) {
+            WMI_HIP(hipMemset(dec_err_, 0, sizeof(int)));
+            throw DeviceError("decode step: a row had no admissible token (non-finite logits); token 0 was recorded");
+        }
     }
 
     // Prompt prefill of one encoder pass (prefill_ on): every seated slot's
@@ -563,6 +600,7 @@ class EngineT final : public Engine {
         for (auto& r : pending_) memcpy(r.dst, tokpin_ + r.off, r.count * sizeof(int));
         pending_.clear();
         tokpin_used_ = 0;
+        check_decode_error();
     }
 
     // -------------------------------------------------------------- decoding options
@@ -799,7 +837,9 @@ class EngineT final : public Engine {
     int64_t snapshots_ = 0;
     T *kts_, *vs_, *ktc_, *vc_, *dz_, *dq_, *datt_, *dh_;
     float *dx_, *logits_, *gpart_;
-    unsigned long long* best_;
+    unsigned long long* keys_;  // greedy-choice keys [S][nkeys_]
+    int nkeys_ = ARGMAX_CHUNKS;
+    int* dec_err_;              // set by a decode step that found no admissible token
     std::vector<int> list_host_;
     bool graphs_ = true, split_ = true, fused_ln_ = true;
     bool free_run_ = true, chains_apart_ = false;
@@ -1248,7 +1288,9 @@ class EngineT final : public Engine {
         dh_ = dalloc<T>(S16 * 4 * d);
         logits_ = dalloc<float>(S * (size_t)V_);
         gpart_ = dalloc<float>((size_t)MAXC * KSMAX * S * d);  // split-K partials [chain][KS][rows][d]
-        best_ = dalloc<unsigned long long>(S);
+        nkeys_ = std::max(ARGMAX_CHUNKS, (V_ + 31) / 32);
+        keys_ = dalloc<unsigned long long>(S * (size_t)nkeys_);
+        dec_err_ = dalloc<int>(1);
         if (prefill_) {
             pf_cap_ = 128;
             pf_list_ = dalloc<int>(2 * pf_cap_);
@@ -1281,6 +1323,22 @@ class EngineT final : public Engine {
         }
     }
 };
+
+// Host run of the greedy choice's key arithmetic (amax_key, key_token): the
+// admissible ids of each row (bit clear in `excluded`, [V / 32 + 1] words,
+// or null) become keys, the largest key per row is decoded.
+void greedy_keys_host(const float* logits, int rows, int V, const unsigned* excluded, int* tokens, int* bad) {
+    for (int r = 0; r < rows; ++r) {
+        unsigned long long k = 0;
+        for (int i = 0; i < V; ++i) {
+            if (excluded && ((excluded[i >> 5] >> (i & 31)) & 1u)) continue;
+            const unsigned long long c = amax_key(logits[(size_t)r * V + i], i);
+            k = c > k ? c : k;
+        }
+        bad[r] = 0;
+        tokens[r] = key_token(k, &bad[r]);
+    }
+}
 
 std::unique_ptr<Engine> make_engine(const whisper_params& p, const void* blob, size_t bytes, int device) {
     if (p.dtype == WHISPER_DTYPE_BF16) return std::unique_ptr<Engine>(new EngineT<bf16>(p, blob, bytes, device));

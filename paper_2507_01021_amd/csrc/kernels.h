@@ -1588,16 +1588,22 @@ __global__ __launch_bounds__(64) void ctc_beam_kernel(const float* __restrict__ 
 
 // ------------------------------------------------------------- greedy step
 //
-// argmax over the logits in two kernels: (1) grid (chunks, rows), each
-// workgroup reduces a chunk of one row and folds it into best[r] with a
-// 64-bit atomic max of (order-preserving value bits << 32 | ~index), which
-// picks the largest value and, among equal values, the lowest index, in any
-// order of arrival; (2) one thread per row reads best[r], resets it, records
-// the token, feeds it (or the forced token) as the next input once the
-// prompt is consumed, and advances the slot's position.
+// The greedy choice (largest logit, lowest id on ties) in two stages. Every
+// candidate id i with logit v becomes the 64-bit key (order-preserving bits
+// of v << 32 | ~i): the largest key has the largest value and, among equal
+// values, the lowest id, whatever order keys are compared in. (1) Partial
+// maxima: in the bf16 model the output head's own kernel reduces its
+// workgroup's 32 ids per row and writes one key per (row, workgroup)
+// (head_argmax_kernel, below the decode projections); the fp32 model writes
+// its logits and argmax_keys_kernel reduces ARGMAX_CHUNKS chunks per row.
+// (2) argmax_step_kernel: one wave per row takes the largest of the row's
+// keys, records the token, feeds it (or the forced token) as the next input
+// once the prompt is consumed, and advances the slot's position.
 // Logit filters (optional): ids whose bit is set in `never` cannot be
 // chosen, ids set in `first` not as a row's first generated token (the row
 // is at its first generated token when its input is the prompt's last).
+// A row with no admissible key (every id filtered, which the API refuses,
+// or keys lost to non-numbers) records token 0 and raises *err.
 constexpr int ARGMAX_CHUNKS = 16;
 
 struct TokenFilter {
@@ -1608,12 +1614,22 @@ struct TokenFilter {
     const int* n_prompt;    // slot -> prompt length
 };
 
-__device__ inline unsigned long long amax_key(float v, int i) {
+__host__ __device__ inline unsigned long long amax_key(float v, int i) {
     return ((unsigned long long)f2ord(v) << 32) | (unsigned long long)(0xffffffffu - (unsigned)i);
 }
+// The token of a row's largest key; a row without any key (k = 0) gets
+// token 0 and sets *bad.
+__host__ __device__ inline int key_token(unsigned long long k, int* bad) {
+    if (k == 0ull) {
+        *bad = 1;
+        return 0;
+    }
+    return (int)(0xffffffffu - (unsigned)(k & 0xffffffffull));
+}
 
-__global__ __launch_bounds__(256) void argmax_partial_kernel(const float* __restrict__ logits, int V,
-                                                             unsigned long long* __restrict__ best, TokenFilter f) {
+// fp32 model: keys[r][chunk] = the largest key of chunk `chunk` of row r's logits.
+__global__ __launch_bounds__(256) void argmax_keys_kernel(const float* __restrict__ logits, int V,
+                                                          unsigned long long* __restrict__ keys, TokenFilter f) {
     const int r = blockIdx.y, t = threadIdx.x;
     const int per = (V + ARGMAX_CHUNKS - 1) / ARGMAX_CHUNKS;
     const int lo = blockIdx.x * per, hi = min(V, lo + per);
@@ -1628,23 +1644,16 @@ __global__ __launch_bounds__(256) void argmax_partial_kernel(const float* __rest
     for (int i = lo + t; i < hi; i += 256 * 4) {
         float v[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = (i + 256 * q < hi) ? lg[i + 256 * q] : -INFINITY;
-        if (never || first) {
+        for (int q = 0; q < 4; ++q) v[q] = (i + 256 * q < hi) ? lg[i + 256 * q] : 0.f;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int j = i + 256 * q;
-                if (j < hi) {
-                    const unsigned bit = 1u << (j & 31);
-                    if ((never && (never[j >> 5] & bit)) || (first && (first[j >> 5] & bit))) v[q] = -INFINITY;
-                }
-            }
+        for (int q = 0; q < 4; ++q) {
+            const int j = i + 256 * q;
+            if (j >= hi) continue;
+            const unsigned bit = 1u << (j & 31);
+            if ((never && (never[j >> 5] & bit)) || (first && (first[j >> 5] & bit))) continue;
+            const unsigned long long c = amax_key(v[q], j);
+            k = c > k ? c : k;
         }
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            if (i + 256 * q < hi && v[q] != -INFINITY) {
-                const unsigned long long c = amax_key(v[q], i + 256 * q);
-                k = c > k ? c : k;
-            }
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -1657,21 +1666,35 @@ __global__ __launch_bounds__(256) void argmax_partial_kernel(const float* __rest
     if (t == 0) {
         unsigned long long m = sk[0];
         for (int w = 1; w < 4; ++w) m = sk[w] > m ? sk[w] : m;
-        atomicMax(best + r, m);
+        keys[(long long)r * ARGMAX_CHUNKS + blockIdx.x] = m;
     }
 }
 
 // eot >= 0: the first time a slot's generated token is eot, stop_at[slot]
-// becomes the number of tokens generated before it.
-__global__ void argmax_step_kernel(unsigned long long* __restrict__ best, int n, const int* __restrict__ list,
-                                   int* __restrict__ pos, const int* __restrict__ n_prompt, int* __restrict__ seq,
-                                   int* __restrict__ gen, const int* __restrict__ forced, int* __restrict__ out_tok,
-                                   int eot, int* __restrict__ stop_at) {
-    const int r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= n) return;
-    const unsigned long long k = best[r];
-    best[r] = 0ull;
-    const int tok = (int)(0xffffffffu - (unsigned)(k & 0xffffffffull));
+// becomes the number of tokens generated before it. One wave per row over
+// its nk keys.
+__global__ __launch_bounds__(64) void argmax_step_kernel(const unsigned long long* __restrict__ keys, int nk,
+                                                         const int* __restrict__ list, int* __restrict__ pos,
+                                                         const int* __restrict__ n_prompt, int* __restrict__ seq,
+                                                         int* __restrict__ gen, const int* __restrict__ forced,
+                                                         int* __restrict__ out_tok, int eot,
+                                                         int* __restrict__ stop_at, int* __restrict__ err) {
+    const int r = blockIdx.x, lane = threadIdx.x;
+    const unsigned long long* kr = keys + (long long)r * nk;
+    unsigned long long k = 0;
+    for (int j = lane; j < nk; j += 64) {
+        const unsigned long long c = kr[j];
+        k = c > k ? c : k;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long c = __shfl_xor(k, o, 64);
+        k = c > k ? c : k;
+    }
+    if (lane != 0) return;
+    int bad = 0;
+    const int tok = key_token(k, &bad);
+    if (bad) atomicOr(err, 1);
     const int s = list[r], p = pos[s], np = n_prompt[s];
     if (p >= np - 1) {
         const int g = p - (np - 1);
@@ -1683,6 +1706,94 @@ __global__ void argmax_step_kernel(unsigned long long* __restrict__ best, int n,
         out_tok[r] = -1;
     }
     pos[s] = p + 1;
+}
+
+// Output head with the first stage of the greedy choice (bf16 model): the
+// decode projection of the tied token embedding (RT = 2: 32 vocabulary rows
+// per workgroup), then, per activation row, the largest key (amax_key) over
+// the workgroup's admissible ids, written to keys[row][blockIdx.x]; the
+// logits themselves are stored only when `logits` is set (fp32, [n][V]).
+// Filter bits and the rows' first-token flags are loaded before the main
+// loop.
+struct HeadArgs {
+    float* logits;              // [n][V] or null
+    unsigned long long* keys;   // [n][gridDim.x]
+    int V;
+    TokenFilter f;
+};
+
+template <int NT, int U>
+__global__ __launch_bounds__(256) void head_argmax_kernel(const bf16* __restrict__ W, const bf16* __restrict__ X,
+                                                          int nks_tot, int n, int Kc, HeadArgs h) {
+    constexpr int RT = 2;
+    __shared__ float red[3 * RT * NT * 4 * 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int fr = lane & 15, fc = lane >> 4;
+    const int i0 = blockIdx.x * 16 * RT;
+    unsigned excl[RT][NT];  // bit q: id i + q is not admissible for this row
+    if (wave == 0) {
+#pragma unroll
+        for (int u = 0; u < NT; ++u) {
+            const int r = u * 16 + fr;
+            bool first = false;
+            if (h.f.first && r < n) {
+                const int sl = h.f.list[r];
+                first = h.f.pos[sl] == h.f.n_prompt[sl] - 1;
+            }
+#pragma unroll
+            for (int t = 0; t < RT; ++t) {
+                const int i = i0 + t * 16 + fc * 4;
+                unsigned m = 0;
+                if (r < n && i < h.V) {
+                    if (h.f.never) m |= (h.f.never[i >> 5] >> (i & 31)) & 0xfu;
+                    if (first) m |= (h.f.first[i >> 5] >> (i & 31)) & 0xfu;
+                }
+                excl[t][u] = m;
+            }
+        }
+    }
+    float v[RT][NT][4];
+    skinny_core<RT, NT, U>(W, X, nks_tot, n, Kc, red, v);
+    if (wave > 0) return;
+#pragma unroll
+    for (int u = 0; u < NT; ++u) {
+        const int r = u * 16 + fr;
+        unsigned long long k = 0;
+#pragma unroll
+        for (int t = 0; t < RT; ++t) {
+            const int i = i0 + t * 16 + fc * 4;
+            if (r >= n) continue;
+            if (h.logits) {
+                float* p = h.logits + (long long)r * h.V + i;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (i + q < h.V) p[q] = v[t][u][q];
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if (i + q >= h.V || ((excl[t][u] >> q) & 1u)) continue;
+                const unsigned long long c = amax_key(v[t][u][q], i + q);
+                k = c > k ? c : k;
+            }
+        }
+        // ids i0 .. i0 + 31 of row r are spread over lanes fr, fr + 16, fr + 32, fr + 48
+        unsigned long long c = __shfl_xor(k, 16, 64);
+        k = c > k ? c : k;
+        c = __shfl_xor(k, 32, 64);
+        k = c > k ? c : k;
+        if (fc == 0 && r < n) h.keys[(long long)r * gridDim.x + blockIdx.x] = k;
+    }
+}
+
+// Output head + per-workgroup keys for n rows (W: fragment-major [V rounded
+// up to 32][K], X fragment-major [n rounded up to 16][K]); returns the number
+// of keys per row.
+inline int head_argmax(const bf16* W, int V, const bf16* X, int n, int K, const HeadArgs& h, hipStream_t st) {
+    if (K % 32 || n <= 0 || n > 128 || V <= 0) throw ArgError(-1, "head_argmax: unsupported shape");
+    const int nks = K / 32, tiles = (V + 31) / 32;
+    WMI_SKINNY_NT(n, WMI_SKINNY_U(K, NT, hipLaunchKernelGGL((head_argmax_kernel<NT, U>), dim3(tiles), dim3(256), 0,
+                                                             st, W, X, nks, n, K, h)));
+    return tiles;
 }
 
 // Seat prompts: for entry e, slot slots[e] gets tokens prompts[e * 448 ...]

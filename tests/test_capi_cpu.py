@@ -134,3 +134,26 @@ def test_prefill_rejected_for_ctc_models(lib):
     st = lib.whisper_ctx_create(C.byref(p), blob.ctypes.data, blob.nbytes, 0, C.byref(h))
     assert st == binding.E_INVAL and not h.value
     assert b"prefill" in lib.whisper_last_error(None)
+
+
+def test_greedy_keys_on_host(lib):
+    """The decode step's greedy-choice keys, run on the host: the largest
+    logit wins, the lowest id among equal logits, negative values and -inf
+    order correctly, excluded ids are skipped, and a row with every id
+    excluded yields token 0 with its flag raised (the step's error)."""
+    V = 70
+    rng = np.random.default_rng(3)
+    lg = rng.normal(size=(6, V)).astype(np.float32)
+    lg[1, 5] = lg[1, 40] = lg[1].max() + 1.0           # tie: the lower id
+    lg[2] = -np.abs(lg[2]) - 1.0                        # all negative
+    lg[2, 66] = -0.5
+    lg[3] = -np.inf
+    lg[3, 69] = -1e30                                   # the only finite value
+    lg[4, 33] = 1e30
+    tok, bad = binding.test_greedy_keys(lg)
+    assert tok.tolist() == [int(np.argmax(r)) for r in lg]
+    assert tok[1] == 5 and tok[2] == 66 and tok[3] == 69 and not bad.any()
+    tok, bad = binding.test_greedy_keys(lg, excluded_ids=[33, 5])
+    assert tok[4] != 33 and tok[1] == 40 and not bad.any()
+    tok, bad = binding.test_greedy_keys(lg[:1], excluded_ids=range(V))
+    assert tok.tolist() == [0] and bad.tolist() == [1]

@@ -1,12 +1,15 @@
-"""GPU parity of the encoder-only CTC variant (greedy best-path decoding)
-against the float64 oracle (oracle/ctc.py), through the C ABI.
+"""GPU parity of the encoder-only CTC variant (greedy best-path decoding
+and prefix beam search) against the float64 oracle (oracle/ctc.py), through
+the C ABI.
 
 Tolerances: head logits per frame relative to the frame's largest
 magnitude, 1e-3 for the fp32 model and 2e-2 for bf16 (the decoder logits'
-bar). The device's per-frame ids equal the argmax of its own logits exactly;
-they equal the oracle's on every frame whose top-1 - top-2 margin exceeds
-twice that tolerance, and otherwise lie within that band. Labels are
-compared exactly when no frame of the segment is that close to a tie."""
+bar). The device's per-frame ids equal the argmax of its own logits
+exactly; they equal the oracle's on every frame whose top-1 - top-2 margin
+exceeds twice the frame's measured logit error, and otherwise lie within
+that band (tests/parity.py). The device's labels equal the oracle's CTC
+collapse of the device's ids, always; so they equal the oracle's labels
+whenever no frame is a near tie."""
 import copy
 import sys
 
@@ -18,9 +21,9 @@ from oracle import ctc as OC
 from oracle import model as M
 from paper_2507_01021_amd import binding, synth
 
-pytestmark = pytest.mark.gpu
+from parity import TOL, check_ctc_entry
 
-TOL = {"f32": 1e-3, "bf16": 2e-2}
+pytestmark = pytest.mark.gpu
 
 
 def log(*a):
@@ -32,26 +35,12 @@ def _oracle(W, shape, segs, pad_mode=0):
     return OC.transcribe_ctc(W, shape, segs, pad_mode=pad_mode, return_logits=True)
 
 
-def _check_entry(ctx, shape, b, seg, ref, tol):
-    """Logits, per-frame ids and labels of batch entry b against the oracle;
-    returns True when the labels were compared exactly."""
-    V = shape.n_vocab
-    lg = ctx.debug_copy(binding.T_CTC_LOGITS, b, (1500, V))
-    ids = ctx.debug_copy(binding.T_CTC_IDS, b, (1500,), np.int32)
-    want = ref["logits"]
-    err = (np.abs(lg - want).max(axis=1) / np.abs(want).max(axis=1)).max()
-    log(f"entry {b}: logits rel err {err:.2e}")
-    assert err < tol
-    assert np.array_equal(ids, np.argmax(lg, axis=1))       # the device argmax is exact on its own logits
-    T = OC.valid_frames(seg.audio.size)
-    top2 = np.sort(want[:T], axis=1)[:, -2:]
-    clear = (top2[:, 1] - top2[:, 0]) > 2 * tol * np.abs(want[:T]).max(axis=1)
-    assert np.array_equal(ids[:T][clear], np.asarray(ref["ids"])[clear])
-    for t in np.nonzero(~clear)[0]:
-        assert want[t, ids[t]] >= want[t].max() - 2 * tol * np.abs(want[t]).max()
-    same = np.array_equal(ids[:T], np.asarray(ref["ids"]))
-    log(f"entry {b}: {T} frames, {int((~clear).sum())} near ties, ids identical: {same}")
-    return same
+def _check_labels(seg, ref, ids, near, labels):
+    """Labels: the oracle's collapse of the device's ids; with no near-tie
+    frame, the oracle's own labels."""
+    assert labels == OC.collapse(ids.tolist())[:seg.max_new_tokens]
+    if near == 0:
+        assert labels == ref["tokens"]
 
 
 @pytest.fixture(scope="module")
@@ -67,25 +56,24 @@ def test_ctc_tiny_logits_ids_labels(tiny):
     shape, W, segs, ref, ctx = tiny
     log("ctc-tiny: encode 2 segments")
     ctx.encode(segs, [0, 1])
-    same = []
+    got = []
     for b, (s, r) in enumerate(zip(segs, ref)):
         mel = ctx.debug_copy(binding.T_MEL, b, (shape.n_mels, 3000))
         assert np.abs(mel - oracle.log_mel_segment(s.audio, shape.n_mels)).max() < 2e-5
-        same.append(_check_entry(ctx, shape, b, s, r, TOL["f32"]))
+        got.append(check_ctc_entry(ctx, shape, b, s, r, TOL["f32"], log))
     res = ctx.transcribe(segs)
-    for s, r, g, ok in zip(segs, ref, res, same):
+    for s, r, g, (ids, near) in zip(segs, ref, res, got):
         log(f"segment {s.segment_id}: {len(r['tokens'])} labels (oracle), {g['tokens'].size} (device)")
         assert g["status"] == 0 and g["tokens"].size <= s.max_new_tokens
-        if ok:  # identical frame ids collapse to identical labels
-            assert g["tokens"].tolist() == r["tokens"]
-    assert any(same)
+        _check_labels(s, r, ids, near, g["tokens"].tolist())
+    assert any(near == 0 for _, near in got)     # the exact-label case occurs
 
 
 def test_ctc_base_bf16_and_queue():
-    """bf16 model: per-entry parity on a pass of 3 segments, then a queue of
-    40 segments in passes of 16: every result maps back to its segment and
-    equals the segment's labels from the solo pass (bit-exact); a small
-    max_new_tokens truncates."""
+    """bf16 model: per-entry parity on a pass of 3 segments (logits, ids, and
+    labels as the collapse of the ids), then a queue of 40 segments in passes
+    of 16: every result maps back to its segment and equals the segment's
+    labels from the solo pass (bit-exact); a small max_new_tokens truncates."""
     shape = synth.CTC_BASE
     W = synth.make_weights(shape, 0)
     segs = synth.uniform_batch(shape, 3, 1500, seed=3)
@@ -93,11 +81,10 @@ def test_ctc_base_bf16_and_queue():
     with binding.Context(synth.pack_blob(W), max_slots=16, max_encode_batch=16) as ctx:
         log("ctc-base: encode 3 segments")
         ctx.encode(segs, list(range(3)))
-        same = [_check_entry(ctx, shape, b, s, r, TOL["bf16"]) for b, (s, r) in enumerate(zip(segs, ref))]
+        got = [check_ctc_entry(ctx, shape, b, s, r, TOL["bf16"], log) for b, (s, r) in enumerate(zip(segs, ref))]
         solo = [ctx.transcribe([s])[0]["tokens"] for s in segs]
-        for t, r, ok in zip(solo, ref, same):
-            if ok:
-                assert t.tolist() == r["tokens"]
+        for s, t, r, (ids, near) in zip(segs, solo, ref, got):
+            _check_labels(s, r, ids, near, t.tolist())
         q = []
         for k in range(40):
             t = copy.copy(segs[k % 3])
@@ -155,6 +142,45 @@ def test_ctc_prefix_beam_search_matches_oracle(beam, scale):
         same += eq
     if scale > 1:
         assert same == len(segs)
+
+
+def test_ctc_beam_base_bf16_matches_oracle_under_margin_rule():
+    """bf16 prefix beam search (beam 4) against the oracle's search on its
+    float64 logits. A segment's device labels must equal the oracle's unless
+    the oracle's smallest pruning margin is within the error budget of the
+    device's scores: a prefix's score is a sum over frames of log-softmax
+    terms, each off by at most twice the frame's largest logit error, so two
+    prefixes' difference moves by at most 4 times the sum of those errors
+    (plus 5e-3 nats for fp32 summation). Also batch = solo, valid ids."""
+    shape = synth.CTC_BASE
+    W = synth.make_weights(shape, 0)
+    W.values["ctc.w"] = (W.values["ctc.w"] * np.float32(30.0)).astype(np.float32)
+    W.bits["ctc.w"] = synth.round_to_bf16(W.values["ctc.w"])
+    W.values["ctc.w"] = synth.bf16_to_f32(W.bits["ctc.w"]).reshape(W.values["ctc.w"].shape)
+    segs = synth.fixed_batch(shape, [16000, 24000, 48000, 64000], 1500, seed=5)
+    ref = OC.transcribe_ctc(W, shape, segs, beam=4, return_logits=True)
+    blob = synth.pack_blob(W)
+    with binding.Context(blob, max_slots=4) as greedy_ctx:       # the device's logits of each entry
+        greedy_ctx.encode(segs, list(range(4)))
+        lgs = [greedy_ctx.debug_copy(binding.T_CTC_LOGITS, b, (1500, shape.n_vocab)) for b in range(4)]
+    with binding.Context(blob, max_slots=4, ctc_beam=4) as ctx:
+        res = ctx.transcribe(segs)
+        solo = [ctx.transcribe([s])[0] for s in segs]
+    checked = 0
+    for s, r, g, g1, lg in zip(segs, ref, res, solo, lgs):
+        T = OC.valid_frames(s.audio.size)
+        err = np.abs(lg[:T] - r["logits"][:T]).max(axis=1)
+        assert (err / np.abs(r["logits"][:T]).max(axis=1)).max() < TOL["bf16"]
+        budget = 4.0 * float(err.sum()) + 5e-3
+        eq = g["tokens"].tolist() == r["tokens"]
+        log(f"bf16 beam 4, segment {s.segment_id}: {T} frames, {len(r['tokens'])} labels (oracle), "
+            f"{g['tokens'].size} (device), margin {r['margin']:.3g}, budget {budget:.3g}, identical {eq}")
+        assert np.array_equal(g["tokens"], g1["tokens"])          # batch = solo
+        assert g["status"] == 0 and all(1 <= c < shape.n_vocab for c in g["tokens"])
+        if r["margin"] > budget:
+            assert eq
+            checked += 1
+    log(f"bf16 beam: {checked} of {len(segs)} segments beyond the error budget")
 
 
 def test_ctc_beam_base_bf16_runs_and_is_batch_independent():

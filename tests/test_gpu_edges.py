@@ -1,7 +1,8 @@
 """GPU edge cases against the oracle, through the C ABI: the empty call, the
 shortest and longest segments (1 and 480000 samples), and a decode that
 fills the text context to its last position (4 prompt tokens + 444 new =
-448). Tolerances as in test_gpu_parity (fp32 model)."""
+448), for the encoder-decoder and the CTC variant (1 and 1500 frames).
+Tolerances as in test_gpu_parity (fp32 model)."""
 import sys
 
 import numpy as np
@@ -11,7 +12,7 @@ import oracle
 from oracle import ctc as OC
 from paper_2507_01021_amd import binding, synth
 
-from parity import TOL, check_tokens, drive_teacher_forced, oracle_run, rel_row_err
+from parity import TOL, check_ctc_entry, check_tokens, drive_teacher_forced, oracle_run, rel_row_err
 
 pytestmark = pytest.mark.gpu
 
@@ -49,7 +50,7 @@ def test_shortest_and_longest_segments(tiny):
     toks, lgs = drive_teacher_forced(ctx, [0, 1], segs, ref, 8)
     for k in range(2):
         assert rel_row_err(lgs[k], ref[k]["logits"]).max() < TOL["f32"]
-        check_tokens(toks[k], ref[k]["logits"], TOL["f32"])
+        check_tokens(toks[k], ref[k]["logits"], gpu_logits=lgs[k], min_strict=4)
 
 
 def test_decode_to_the_last_text_position(tiny):
@@ -65,7 +66,7 @@ def test_decode_to_the_last_text_position(tiny):
         e = rel_row_err(lgs[k], ref[k]["logits"])
         log(f"slot {k}: logits rel err max {e.max():.2e} (last position {e[-1]:.2e})")
         assert e.max() < TOL["f32"]
-        check_tokens(toks[k], ref[k]["logits"], TOL["f32"])
+        check_tokens(toks[k], ref[k]["logits"], gpu_logits=lgs[k], min_strict=n_new // 2)
     with pytest.raises(binding.WhisperError):  # the slots retired with their last token
         ctx.decode_step([2])
     res = ctx.transcribe(segs)
@@ -74,18 +75,21 @@ def test_decode_to_the_last_text_position(tiny):
 
 
 def test_ctc_shortest_and_longest_segments():
+    """CTC segments of 1 sample (one frame) and 30 s (all 1500 frames):
+    logits, per-frame ids and labels against the oracle."""
     shape = synth.CTC_TINY
     W = synth.make_weights(shape, 0)
     segs = synth.fixed_batch(shape, [1, 480000], 1500, seed=13)
-    ref = OC.transcribe_ctc(W, shape, segs)
+    ref = OC.transcribe_ctc(W, shape, segs, return_logits=True)
     with binding.Context(synth.pack_blob(W), max_slots=2) as ctx:
         ctx.encode(segs, [0, 1])
-        ids = [ctx.debug_copy(binding.T_CTC_IDS, b, (1500,), np.int32) for b in range(2)]
-        res = ctx.transcribe(segs)
-        for s, r, i, g in zip(segs, ref, ids, res):
+        ids = []
+        for b, (s, r) in enumerate(zip(segs, ref)):
             T = OC.valid_frames(s.audio.size)
-            log(f"ctc-tiny: {s.audio.size} samples, {T} frames, {g['tokens'].size} labels")
             assert T == (1 if s.audio.size == 1 else 1500)
-            assert g["tokens"].size <= T
-            if np.array_equal(i[:T], np.asarray(r["ids"])):
-                assert g["tokens"].tolist() == r["tokens"]
+            ids.append(check_ctc_entry(ctx, shape, b, s, r, TOL["f32"], log)[0])
+        res = ctx.transcribe(segs)
+        for s, r, g, i in zip(segs, ref, res, ids):
+            log(f"ctc-tiny: {s.audio.size} samples, {i.size} frames, {g['tokens'].size} labels")
+            assert g["status"] == 0
+            assert g["tokens"].tolist() == OC.collapse(i.tolist())[:s.max_new_tokens]

@@ -1,11 +1,14 @@
 """GPU parity: the HIP path against the float64 oracle on the same seeded
 weights and audio, through the C ABI.
 
-Tolerances: normalised log-mel absolute 2e-5 (fp32 front end); encoder
-output, cross-attention keys/values and logits per row relative to the
-row's largest magnitude, 1e-3 for the fp32 model and 2e-2 for bf16; greedy
-tokens under teacher forcing by the near-tie rule of tests/parity.py;
-segment ids and token placement exactly."""
+Tolerances: normalised log-mel absolute 2e-5 (the front end is fp32 in
+both models, and the GPU's DFT sums 400 fp32 products per bin, so bins far
+below their frame's energy carry relative errors of ~1e-4, i.e. ~2e-5 after
+log10 and the division by 4); encoder output, cross-attention keys/values
+and logits per row relative to the row's largest magnitude, 1e-3 for the fp32 model and 2e-2 for bf16; greedy
+tokens under teacher forcing by the measured-error rule of tests/parity.py,
+free-running tokens up to their first difference from the oracle's free run
+(which must be a near tie); segment ids and token placement exactly."""
 import sys
 
 import numpy as np
@@ -14,7 +17,7 @@ import pytest
 from oracle import model as M
 from paper_2507_01021_amd import binding, synth
 
-from parity import TOL, check_tokens, drain, drive_teacher_forced, oracle_run, rel_row_err
+from parity import TOL, bands, check_free_run, check_tokens, drain, drive_teacher_forced, oracle_run, rel_row_err
 
 pytestmark = pytest.mark.gpu
 
@@ -77,8 +80,8 @@ def test_tiny_teacher_forced_logits_and_tokens(tiny):
         e = rel_row_err(lgs[k], ref[k]["logits"])
         log(f"seg {k} teacher-forced logits rel err max {e.max():.3e}")
         assert e.max() < TOL["f32"]
-        near = check_tokens(toks[k], ref[k]["logits"], TOL["f32"])
-        log(f"seg {k} near-ties {near}")
+        strict, near = check_tokens(toks[k], ref[k]["logits"], gpu_logits=lgs[k], min_strict=8)
+        log(f"seg {k} tokens strict {strict} near-tie {near}")
     # the slots are idle now and hold the generated tokens
     for k in range(2):
         assert np.array_equal(ctx.slot_tokens(k), np.array(toks[k], dtype=np.int32))
@@ -90,8 +93,8 @@ def test_tiny_transcribe_maps_ids_and_matches_oracle(tiny):
     for s, r, o in zip(segs, res, ref):
         assert (r["user_id"], r["segment_id"], r["status"]) == (s.user_id, s.segment_id, 0)
         assert r["tokens"].size == s.max_new_tokens
-        # free-running tokens equal the oracle's where no near-tie occurred on the way
-        check_tokens(r["tokens"], o["logits"], TOL["f32"])
+        # free-running tokens equal the oracle's free run up to a near tie
+        check_free_run(r["tokens"], o["tokens"], o["logits"], bands(o["logits"], tol=TOL["f32"]))
 
 
 def test_time_kernel_cross_attention(tiny):
@@ -107,7 +110,7 @@ def test_time_kernel_cross_attention(tiny):
             ctx.time_kernel(kernel, rows, reps)
     res = ctx.transcribe(segs)
     for s, r, o in zip(segs, res, ref):
-        check_tokens(r["tokens"], o["logits"], TOL["f32"])
+        check_free_run(r["tokens"], o["tokens"], o["logits"], bands(o["logits"], tol=TOL["f32"]))
 
 
 def test_base_bf16_teacher_forced(base):
@@ -126,8 +129,8 @@ def test_base_bf16_teacher_forced(base):
         e = rel_row_err(lgs[k], ref[k]["logits"])
         log(f"seg {k} bf16 logits rel err max {e.max():.3e}")
         assert e.max() < TOL["bf16"]
-        near = check_tokens(toks[k], ref[k]["logits"], TOL["bf16"])
-        log(f"seg {k} near-ties {near}")
+        strict, near = check_tokens(toks[k], ref[k]["logits"], gpu_logits=lgs[k], min_strict=2)
+        log(f"seg {k} tokens strict {strict} near-tie {near}")
 
 
 def test_base_batch_equals_solo_on_gpu(base):
@@ -183,8 +186,9 @@ def test_base_split_step_equals_unsplit(monkeypatch):
 
 
 def test_serve_realtime_admission_tokens_and_times(tiny):
-    """Real-time admission: segments arriving 0-150 ms apart get the same
-    tokens as the offline call, and none finishes before it arrived."""
+    """Real-time admission: segments arriving 0-150 ms apart get the oracle's
+    free-run tokens (up to a near tie) and the offline call's tokens, and none
+    finishes before it arrived."""
     shape, W, segs, ref, ctx = tiny
     import copy
     late = []
@@ -195,7 +199,9 @@ def test_serve_realtime_admission_tokens_and_times(tiny):
         late.append(t)
     offline = ctx.transcribe(late)
     served = ctx.transcribe(late, realtime=True)
-    for s, a, b in zip(late, offline, served):
+    for k, (s, a, b) in enumerate(zip(late, offline, served)):
+        o = ref[k % 2]
+        check_free_run(b["tokens"], o["tokens"], o["logits"], bands(o["logits"], tol=TOL["f32"]), min_agree=4)
         assert np.array_equal(a["tokens"], b["tokens"])
         assert b["finish_us"] >= s.arrival_us
     assert all(r["finish_us"] > 0 for r in offline)
@@ -204,8 +210,9 @@ def test_serve_realtime_admission_tokens_and_times(tiny):
 def test_dynamic_policy_same_tokens_as_continuous(tiny):
     """The dynamic queue policy (shortest-first with aging, refills held back
     for fuller encoder passes) changes only the schedule: 8 segments on 3
-    slots, arriving 0-140 ms apart, get the continuous batcher's tokens,
-    offline and with real-time admission."""
+    slots, arriving 0-140 ms apart, get the oracle's free-run tokens (up to
+    a near tie) and the continuous batcher's tokens, offline and with
+    real-time admission."""
     shape, W, segs, ref, ctx = tiny
     import copy
     late = []
@@ -223,8 +230,12 @@ def test_dynamic_policy_same_tokens_as_continuous(tiny):
         want = cont.transcribe(late)
         for realtime in (False, True):
             got = dyn.transcribe(late, realtime=realtime)
-            for s, a, b in zip(late, want, got):
-                assert b["segment_id"] == s.segment_id
+            for k, (s, a, b) in enumerate(zip(late, want, got)):
+                o = ref[k % 2]
+                n = s.max_new_tokens
+                assert b["segment_id"] == s.segment_id and b["tokens"].size == n
+                check_free_run(b["tokens"], o["tokens"][:n], o["logits"][:n],
+                               bands(o["logits"][:n], tol=TOL["f32"]), min_agree=4)
                 assert np.array_equal(a["tokens"], b["tokens"])
                 if realtime:
                     assert b["finish_us"] >= s.arrival_us

@@ -118,34 +118,49 @@ def test_prefix_beam_search_unpruned_is_exact_by_brute_force():
         assert tuple(labels) == best
 
 
-def test_prefix_beam_search_conserves_probability_when_unpruned():
-    """Unpruned, the final prefixes' probabilities sum to one (every path is
-    accounted for exactly once) and each equals its brute-force P(y)."""
-    rng = np.random.default_rng(12)
-    T, V = 4, 3
-    logits = rng.normal(size=(T, V))
-    probs = _label_probs_brute_force(logits)
-    # run the search keeping every prefix, then read the probabilities back
-    beams = [((), 0.0, -np.inf)]
-    import math
-    for t in range(T):
-        lpb, cands = ctc.frame_candidates(logits[t], V - 1)
-        nxt = {}
-        for prefix, pb, pnb in beams:
-            tot = np.logaddexp(pb, pnb)
-            e = nxt.setdefault(prefix, [-np.inf, -np.inf])
-            e[0] = np.logaddexp(e[0], tot + lpb)
-            if prefix:
-                e[1] = np.logaddexp(e[1], pnb + dict(cands)[prefix[-1]])
-            for c, lpc in cands:
-                src = pb if (prefix and c == prefix[-1]) else tot
-                f = nxt.setdefault(prefix + (c,), [-np.inf, -np.inf])
-                f[1] = np.logaddexp(f[1], src + lpc)
-        beams = [(p, e[0], e[1]) for p, e in nxt.items()]
-    got = {p: math.exp(np.logaddexp(pb, pnb)) for p, pb, pnb in beams}
-    assert abs(sum(got.values()) - 1.0) < 1e-12
-    for y, pr in probs.items():
-        assert abs(got.get(y, 0.0) - pr) < 1e-12
+def _restricted_label_probs(logits, per_frame):
+    """P(y) over the candidate-restricted lattice: frame t may emit only the
+    blank or one of its per_frame most probable non-blank labels (lowest id
+    on ties); every path through those choices that collapses to y adds the
+    product of its per-frame softmax probabilities (brute force)."""
+    T, V = logits.shape
+    p = np.exp(logits - logits.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    allowed = [[0] + sorted(range(1, V), key=lambda c: (-p[t, c], c))[:per_frame] for t in range(T)]
+    out = {}
+    for path in itertools.product(*allowed):
+        y = tuple(ctc.collapse(path))
+        out[y] = out.get(y, 0.0) + float(np.prod([p[t, path[t]] for t in range(T)]))
+    return out
+
+
+def test_prefix_beam_search_pruned_candidates_by_brute_force():
+    """With fewer candidates than labels per frame (per_frame < V - 1) and a
+    beam wider than the number of prefixes, the search returns the most
+    probable label sequence of the candidate-restricted lattice."""
+    rng = np.random.default_rng(14)
+    for _ in range(25):
+        T, V = int(rng.integers(1, 5)), int(rng.integers(4, 6))
+        per_frame = int(rng.integers(1, V - 2))
+        logits = rng.normal(size=(T, V)) * 2
+        probs = _restricted_label_probs(logits, per_frame)
+        best = max(probs, key=probs.get)
+        labels, _ = ctc.prefix_beam_search(logits, T, beam=10_000, per_frame=per_frame)
+        assert tuple(labels) == best
+
+
+def test_prefix_beam_search_tie_order_hand_worked():
+    """Two frames, blank and labels 1, 2, all logits equal (every id has
+    probability 1/3), beam 2, both labels candidates. Frame 0 yields (), (1)
+    and (2) at 1/3 each; the tie order (stays, then extensions in candidate
+    order) keeps () and (1). Frame 1 then gives (1) = 1/9 (blank after it) +
+    1/9 (its label repeated) + 1/9 (label 1 after the empty prefix) = 1/3,
+    and (), (2), (1, 2) 1/9 each: the output is [1], and the smallest margin
+    is 0 (the tie at frame 0). Keeping (2) instead would give [2]."""
+    labels, margin = ctc.prefix_beam_search(np.zeros((2, 3)), 2, beam=2, per_frame=2)
+    assert labels == [1] and margin == 0.0
+    # with a beam of one the empty prefix (the first stay) wins every tie
+    assert ctc.prefix_beam_search(np.zeros((2, 3)), 2, beam=1, per_frame=2) == ([], 0.0)
 
 
 def test_prefix_beam_search_pruned_properties():
