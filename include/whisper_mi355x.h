@@ -244,6 +244,38 @@ whisper_status whisper_batch_decode_step(whisper_ctx* ctx, const int32_t* slots,
                                          const int32_t* forced, int32_t* out_tokens,
                                          float* out_logits);
 
+/* Limits of whisper_batch_decode_step_noalloc: its static scratch array per
+ * GPU, and the most slots one call steps. */
+#define WHISPER_NOALLOC_SCRATCH_BYTES (8u << 20)
+#define WHISPER_NOALLOC_MAX_ROWS 64
+
+/*
+ * For callers that cannot allocate memory (code under HIP graph capture,
+ * tight serving loops, hosts that forbid hipMalloc): the greedy step of
+ * whisper_batch_decode_step (no teacher forcing, no logits) that allocates
+ * nothing. Its per-step temporaries (slot list, activations, split-K
+ * partial sums, greedy-choice keys) live in one static device array of
+ * WHISPER_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends,
+ * instead of the context's workspaces; the slot list reaches the device as
+ * a kernel argument. The call only enqueues kernels on the context's stream
+ * (see whisper_ctx_set_stream) and returns without waiting for them; the
+ * caller synchronises that stream. The slots' state (position, generated
+ * tokens, retirement) advances exactly as with whisper_batch_decode_step.
+ *   slots           host array of n distinct active slots,
+ *                   1 <= n <= WHISPER_NOALLOC_MAX_ROWS
+ *   out_tokens_dev  NULL or device memory of the context's GPU, n int32:
+ *                   this step's argmax per slot (-1 inside the prompt),
+ *                   written when the enqueued work runs
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * behind: calls whose work overlaps in time on one GPU (contexts on
+ * different streams) race on it. A row without an admissible token is
+ * reported by the next call that synchronises. Errors: E_INVAL, E_STATE
+ * (slot idle, or kernel timing on), E_CAPACITY (n above the maximum, or the
+ * model's rows need more than the array; the message states the size).
+ */
+whisper_status whisper_batch_decode_step_noalloc(whisper_ctx* ctx, const int32_t* slots, int32_t n,
+                                                 int32_t* out_tokens_dev);
+
 /* Copies the tokens generated so far in `slot` (at most cap) to dst (host)
  * and their count to *n_out. */
 whisper_status whisper_slot_tokens(whisper_ctx* ctx, int32_t slot, int32_t* dst, int32_t cap,

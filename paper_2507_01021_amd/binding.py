@@ -21,6 +21,7 @@ K_CROSS_ATTN, K_ENC_GEMM, K_SELF_ATTN, K_ENC_ATTN, K_ENC_PASS, K_DEC_STEP, K_FRO
 EXPORTS = (
     "whisper_params_from_blob", "whisper_ctx_create", "whisper_ctx_destroy", "whisper_last_error",
     "whisper_ctx_set_stream", "whisper_batch_encode", "whisper_batch_decode_step",
+    "whisper_batch_decode_step_noalloc",
     "whisper_slot_tokens", "whisper_batch_transcribe", "whisper_batch_serve", "whisper_debug_copy",
     "whisper_profile_enable", "whisper_profile_read", "whisper_time_kernel", "whisper_stats_read",
     "whisper_set_decoding", "whisper_test_batcher", "whisper_test_greedy_keys",
@@ -75,6 +76,7 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         "whisper_ctx_set_stream": (i32, [vp, vp]),
         "whisper_batch_encode": (i32, [vp, C.POINTER(whisper_segment), i32, pi32]),
         "whisper_batch_decode_step": (i32, [vp, pi32, i32, pi32, pi32, C.POINTER(C.c_float)]),
+        "whisper_batch_decode_step_noalloc": (i32, [vp, pi32, i32, vp]),
         "whisper_slot_tokens": (i32, [vp, i32, pi32, i32, pi32]),
         "whisper_batch_transcribe": (i32, [vp, C.POINTER(whisper_segment), i32, pi32, i64,
                                           C.POINTER(whisper_result)]),
@@ -204,6 +206,14 @@ class Context:
             self.h, _ptr(sl, C.c_int32), n, None if fo is None else _ptr(fo, C.c_int32),
             _ptr(toks, C.c_int32), None if lg is None else _ptr(lg, C.c_float)))
         return (toks, lg) if logits else toks
+
+    def decode_step_noalloc(self, slots, out_tokens_dev: int = 0):
+        """whisper_batch_decode_step_noalloc: enqueues one greedy step that
+        allocates nothing; out_tokens_dev is a device address of len(slots)
+        int32 (or 0). Returns without waiting for the device."""
+        sl = np.ascontiguousarray(slots, dtype=np.int32)
+        self._check(load().whisper_batch_decode_step_noalloc(self.h, _ptr(sl, C.c_int32), sl.size,
+                                                             C.c_void_p(out_tokens_dev or None)))
 
     def slot_tokens(self, slot: int, cap: int = 448):
         buf = np.empty(cap, dtype=np.int32)

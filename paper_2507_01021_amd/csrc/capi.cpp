@@ -484,6 +484,39 @@ whisper_status whisper_batch_decode_step(whisper_ctx* ctx, const int32_t* slots,
     });
 }
 
+whisper_status whisper_batch_decode_step_noalloc(whisper_ctx* ctx, const int32_t* slots, int32_t n,
+                                                 int32_t* out_tokens_dev) {
+    if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
+    if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");
+    if (ctx->p.n_text_layer == 0) return fail(ctx, WHISPER_E_STATE, "not available for an encoder-only CTC model");
+    if (n < 1 || n > WHISPER_NOALLOC_MAX_ROWS || n > ctx->p.max_slots)
+        return fail(ctx, WHISPER_E_CAPACITY, "n must be in 1.." + std::to_string(WHISPER_NOALLOC_MAX_ROWS) +
+                                                 " and at most max_slots");
+    if (!slots) return fail(ctx, WHISPER_E_INVAL, "slots must not be NULL");
+    bool seen[128] = {};
+    for (int i = 0; i < n; ++i) {
+        if (slots[i] < 0 || slots[i] >= ctx->p.max_slots)
+            return fail(ctx, WHISPER_E_CAPACITY, "slot " + std::to_string(slots[i]) + " outside 0..max_slots-1");
+        if (seen[slots[i]]) return fail(ctx, WHISPER_E_INVAL, "slots must be distinct");
+        seen[slots[i]] = true;
+        if (!ctx->slots[slots[i]].active)
+            return fail(ctx, WHISPER_E_STATE, "slot " + std::to_string(slots[i]) + " is idle");
+    }
+    return guarded(ctx, [&]() -> whisper_status {
+        ctx->eng->decode_step_noalloc(slots, n, out_tokens_dev);
+        ctx->stats.decode_steps += 1;
+        ctx->stats.rows_decoded += n;
+        for (int i = 0; i < n; ++i) {
+            SlotState& s = ctx->slots[slots[i]];
+            ctx->stats.positions_attended += s.steps + 1;
+            if (s.steps >= s.n_prompt - 1) s.generated++;
+            s.steps++;
+            if (s.generated == s.max_new) s.active = false;
+        }
+        return WHISPER_OK;
+    });
+}
+
 whisper_status whisper_slot_tokens(whisper_ctx* ctx, int32_t slot, int32_t* dst, int32_t cap, int32_t* n_out) {
     if (!ctx) return fail(nullptr, WHISPER_E_INVAL, "ctx is NULL");
     if (ctx->broken) return fail(ctx, WHISPER_E_DEVICE, "context unusable after a device error");

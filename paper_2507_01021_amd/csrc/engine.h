@@ -33,6 +33,11 @@ class Engine {
     // sync = false leaves the work queued (outputs must then be null).
     virtual void decode_step(const int* slots, int n, const int* forced, int* out_tok, float* out_logits,
                              bool sync) = 0;
+    // One greedy step (no teacher forcing, no logits) that allocates nothing:
+    // its per-step temporaries live in the library's static scratch array of
+    // this device; only kernels are enqueued on the context's stream and the
+    // call does not wait for them. out_tok_dev: device int32[n] or null.
+    virtual void decode_step_noalloc(const int* slots, int n, int* out_tok_dev) = 0;
     // Copies gen[slot][0..count) to host dst (synchronous).
     virtual void read_tokens(int slot, int count, int32_t* dst) = 0;
     // Queues a copy of gen[slot][0..count) into host memory owned by the

@@ -34,6 +34,7 @@
 #include <algorithm>
 #include <array>
 #include <map>
+#include <mutex>
 #include <type_traits>
 #include <string>
 #include <vector>
@@ -193,6 +194,44 @@ static std::vector<float> sinusoids(int T, int d) {  // [T][d]
     return pe;
 }
 
+// ------------------------------------------------------------------ scratch of the allocation-free step
+//
+// whisper_batch_decode_step_noalloc keeps its per-step temporaries (slot
+// list, row lengths, activations, split-K partial sums, greedy-choice keys,
+// tokens, and the fp32 model's logits) in this array instead of the
+// context's workspaces. Each GPU holds its own copy until the process ends.
+// In host code `scratch` only names the symbol: its device address on a
+// device comes from hipGetSymbolAddress with that device current, taken once
+// per device when an engine is created there and kept in g_scratch_dev.
+static __device__ __align__(256) unsigned char scratch[WHISPER_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+constexpr int MAX_DEVICES = 64;
+void* g_scratch_dev[MAX_DEVICES] = {};
+}  // namespace
+
+// Device address of `scratch` on device dev (the current device).
+static void* scratch_address(int dev) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (dev < 0 || dev >= MAX_DEVICES) throw ArgError(WHISPER_E_INVAL, "device index above 63");
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        WMI_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        g_scratch_dev[dev] = p;
+    }
+    return g_scratch_dev[dev];
+}
+
+// A slot list passed by value, so that staging it needs no copy from host memory.
+struct RowList {
+    int n;
+    int slot[WHISPER_NOALLOC_MAX_ROWS];
+};
+__global__ void put_list_kernel(RowList l, int* __restrict__ dst) {
+    if ((int)threadIdx.x < l.n) dst[threadIdx.x] = l.slot[threadIdx.x];
+}
+
 // ------------------------------------------------------------------ engine
 
 template <class T> struct HostElem;
@@ -239,6 +278,7 @@ class EngineT final : public Engine {
         if (const char* g = getenv("WHISPER_FC2_SPLIT")) fc2_split_ = atoi(g);
         load_weights(blob, bytes);
         alloc_state();
+        scratch_ = static_cast<unsigned char*>(scratch_address(dev_));
         WMI_HIP(hipDeviceSynchronize());
     }
 
@@ -499,6 +539,60 @@ class EngineT final : public Engine {
         }
         hipLaunchKernelGGL(argmax_step_kernel, dim3(n), dim3(64), 0, s, keys, nk, list, pos_, npr_, seq_, gen_,
                            sb.forced, sb.outtok, eot_, stop_at_, dec_err_);
+    }
+
+    // Scratch layout of an allocation-free step of n rows (byte offsets,
+    // each region 256-byte aligned); total() is what the array must hold.
+    struct NoallocLayout {
+        size_t list, rowlen, outtok, dx, dz, dq, datt, dh, part, keys, logits, end;
+    };
+    NoallocLayout noalloc_layout(int n) const {
+        const size_t d = d_, n16 = (size_t)(n + 15) / 16 * 16;
+        size_t o = 0;
+        auto take = [&](size_t bytes) { const size_t at = o; o += (bytes + 255) / 256 * 256; return at; };
+        NoallocLayout L;
+        L.list = take(WHISPER_NOALLOC_MAX_ROWS * sizeof(int));
+        L.rowlen = take(WHISPER_NOALLOC_MAX_ROWS * sizeof(int));
+        L.outtok = take(WHISPER_NOALLOC_MAX_ROWS * sizeof(int));
+        L.dx = take((size_t)n * d * sizeof(float));
+        L.dz = take(n16 * d * sizeof(T));
+        L.dq = take((size_t)n * d * sizeof(T));
+        L.datt = take(n16 * d * sizeof(T));
+        L.dh = take(n16 * 4 * d * sizeof(T));
+        L.part = take((size_t)KSMAX * n * d * sizeof(float));
+        L.keys = take((size_t)n * nkeys_ * sizeof(unsigned long long));
+        L.logits = std::is_same<T, bf16>::value ? o : take((size_t)n * V_ * sizeof(float));
+        L.end = o;
+        return L;
+    }
+
+    void decode_step_noalloc(const int* slots, int n, int* out_tok_dev) override {
+        if (n < 1 || n > WHISPER_NOALLOC_MAX_ROWS)
+            throw ArgError(WHISPER_E_CAPACITY, "decode_step_noalloc: n must be in 1.." +
+                                                   std::to_string(WHISPER_NOALLOC_MAX_ROWS));
+        const NoallocLayout L = noalloc_layout(n);
+        if (L.end > (size_t)WHISPER_NOALLOC_SCRATCH_BYTES)
+            throw ArgError(WHISPER_E_CAPACITY, "decode_step_noalloc: " + std::to_string(n) + " rows of this model need " +
+                                                   std::to_string(L.end) + " bytes of scratch, the array holds " +
+                                                   std::to_string((size_t)WHISPER_NOALLOC_SCRATCH_BYTES));
+        for (auto& pr : prof_)
+            if (pr.on) throw ArgError(WHISPER_E_STATE, "decode_step_noalloc: kernel timing is on");
+        WMI_HIP(hipSetDevice(dev_));
+        join_chains();
+        unsigned char* z = scratch_;  // this device's copy of the array
+        RowList rl;
+        rl.n = n;
+        for (int i = 0; i < n; ++i) rl.slot[i] = slots[i];
+        int* list = reinterpret_cast<int*>(z + L.list);
+        hipLaunchKernelGGL(put_list_kernel, dim3(1), dim3(WHISPER_NOALLOC_MAX_ROWS), 0, st_, rl, list);
+        const StepBufs b{RowBufs{list, nullptr, reinterpret_cast<float*>(z + L.dx), reinterpret_cast<T*>(z + L.dz),
+                                 reinterpret_cast<T*>(z + L.dq), reinterpret_cast<T*>(z + L.datt),
+                                 reinterpret_cast<T*>(z + L.dh), reinterpret_cast<int*>(z + L.rowlen),
+                                 reinterpret_cast<float*>(z + L.part)},
+                         reinterpret_cast<float*>(z + L.logits), reinterpret_cast<unsigned long long*>(z + L.keys),
+                         out_tok_dev ? out_tok_dev : reinterpret_cast<int*>(z + L.outtok), nullptr};
+        run_step(b, n, false, st_);
+        WMI_HIP(hipGetLastError());
     }
 
     // Raises the device-side decode error flag (a row without an admissible
@@ -814,6 +908,7 @@ class EngineT final : public Engine {
     hipStream_t own_stream_ = nullptr, st_ = nullptr;
     std::vector<void*> allocs_;
 
+    unsigned char* scratch_ = nullptr;  // device address of this device's scratch array
     // weights
     T *W1r_, *W2r_, *tok_emb_, *pos_emb_, *WcK_, *WcV_;
     float *cb1_, *cb2_, *lnpg_, *lnpb_, *lnfg_, *lnfb_, *bcV_;
