@@ -359,7 +359,12 @@ enum {
     WHISPER_K_ENC_PASS = 4,    /* a whole encode pass (front end to cross-KV) */
     WHISPER_K_DEC_STEP = 5,    /* a whole decode step (embedding to argmax) */
     WHISPER_K_FRONT_END = 6,   /* log-mel front end of an encode pass (audio to normalised mel) */
-    WHISPER_K_COUNT = 7
+    WHISPER_K_CROSS_ATTN_STEP = 7, /* decode-step cross-attention as the plain steps run it (captured
+                                      graphs, slots split into concurrent chains): each launch's span
+                                      from its first workgroup's start to its last one's end, stamped
+                                      by the kernel with the device's real-time counter and read after
+                                      each step (steps are joined and synchronised meanwhile) */
+    WHISPER_K_COUNT = 8
 };
 
 /* Starts (enable = 1) or stops (0) timing of `kernel`, clearing its totals. */

@@ -17,6 +17,7 @@ OK, E_INVAL, E_NOMEM, E_DEVICE, E_CAPACITY, E_STATE, E_BUFFER, E_FORMAT = 0, -1,
 DTYPE_F32, DTYPE_BF16 = 0, 1
 T_MEL, T_ENC_OUT, T_CROSS_K, T_CROSS_V, T_CTC_LOGITS, T_CTC_IDS = 0, 1, 2, 3, 4, 5
 K_CROSS_ATTN, K_ENC_GEMM, K_SELF_ATTN, K_ENC_ATTN, K_ENC_PASS, K_DEC_STEP, K_FRONT_END = 0, 1, 2, 3, 4, 5, 6
+K_CROSS_ATTN_STEP = 7
 
 EXPORTS = (
     "whisper_params_from_blob", "whisper_ctx_create", "whisper_ctx_destroy", "whisper_last_error",

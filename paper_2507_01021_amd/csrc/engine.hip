@@ -293,9 +293,10 @@ class EngineT final : public Engine {
         if (mark_start_) (void)hipEventDestroy(mark_start_);
         for (int c = 1; c < MAXC; ++c)
             if (cst_[c]) (void)hipStreamSynchronize(cst_[c]);
-        for (auto& g : step_graphs_)
-            for (auto ge : g.second)
-                if (ge) (void)hipGraphExecDestroy(ge);
+        for (auto* m : {&step_graphs_, &stamped_graphs_})
+            for (auto& g : *m)
+                for (auto ge : g.second)
+                    if (ge) (void)hipGraphExecDestroy(ge);
         for (auto& s : stage_) {
             if (s.ev) (void)hipEventDestroy(s.ev);
             if (s.host) (void)hipHostFree(s.host);
@@ -361,7 +362,10 @@ class EngineT final : public Engine {
         // with events: such steps run as plain launches, unsplit; encoder
         // timings leave the steps as they are
         const bool timed = prof_[WHISPER_K_CROSS_ATTN].on || prof_[WHISPER_K_SELF_ATTN].on || prof_[WHISPER_K_DEC_STEP].on;
-        const bool plain = graphs_ && !forced && !out_tok && !out_logits && !timed && !sync_;
+        // cross-attention spans stamped inside the plain steps' graphs: graphs and
+        // chains as usual, but the chains are joined and read after every step
+        const bool stamping = prof_[WHISPER_K_CROSS_ATTN_STEP].on;
+        const bool plain = graphs_ && !forced && !out_tok && !out_logits && !timed && !sync_ && !stamping;
         if (free_run_ && plain && same_list && chains_apart_) {
             // the chains keep running on their own streams: no fork, no join
             auto it = step_graphs_.find(n);
@@ -388,19 +392,22 @@ class EngineT final : public Engine {
             WMI_HIP(hipEventRecord(fork_ev_, st_));
             for (int c = 1; c < nc; ++c) WMI_HIP(hipStreamWaitEvent(cst_[c], fork_ev_, 0));
         }
+        stamp_on_ = stamping;
         if (graphs_ && !forced && !out_tok && !out_logits && !timed) {
-            auto it = step_graphs_.find(n);
-            if (it == step_graphs_.end()) {
+            auto& graphs = stamping ? stamped_graphs_ : step_graphs_;
+            auto it = graphs.find(n);
+            if (it == graphs.end()) {
                 std::array<hipGraphExec_t, MAXC> ge{};
                 for (int c = 0; c < nc; ++c)
                     ge[c] = capture(stream(c), [&] { launch_rows(r0[c], r0[c + 1] - r0[c], false, false, stream(c), c); });
-                it = step_graphs_.emplace(n, ge).first;
+                it = graphs.emplace(n, ge).first;
             }
             for (int c = 0; c < nc; ++c) WMI_HIP(hipGraphLaunch(it->second[c], stream(c)));
         } else {
             for (int c = 0; c < nc; ++c)
                 launch_rows(r0[c], r0[c + 1] - r0[c], forced != nullptr, out_logits != nullptr, stream(c), c);
         }
+        stamp_on_ = false;
         if (free_run_ && plain && nc > 1) {  // stay apart until something needs the results
             chains_apart_ = true;
             apart_nc_ = nc;
@@ -412,6 +419,7 @@ class EngineT final : public Engine {
         }
         prof_end(WHISPER_K_DEC_STEP, st_);
         WMI_HIP(hipGetLastError());
+        if (stamping) read_stamps(nc);
         if (out_tok) WMI_HIP(hipMemcpyAsync(out_tok, outtok_, n * sizeof(int), hipMemcpyDeviceToHost, st_));
         if (out_logits)
             WMI_HIP(hipMemcpyAsync(out_logits, logits_, (size_t)n * V_ * sizeof(float), hipMemcpyDeviceToHost, st_));
@@ -461,6 +469,7 @@ class EngineT final : public Engine {
         T* dh;
         int* rowlen;
         float* pbuf;
+        unsigned long long* stamps = nullptr;  // cross-attention timing slots [layer][2], or null
     };
 
     // Embedding and every decoder layer for n rows; leaves the final layer
@@ -483,7 +492,8 @@ class EngineT final : public Engine {
             hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, s, sa);
             prof_end(WHISPER_K_SELF_ATTN, s);
             self_out_cross_q(L, n, b.datt, b.dq, b.dx, b.dz, b.pbuf, s);
-            DecAttnArgs ca{b.dq, ktc_ + sl * TC, vc_ + sl * TC, b.datt, b.list, nullptr, TC, H_, d};
+            DecAttnArgs ca{b.dq, ktc_ + sl * TC, vc_ + sl * TC, b.datt, b.list, nullptr, TC, H_, d,
+                           b.stamps ? b.stamps + 2 * l : nullptr};
             prof_begin(WHISPER_K_CROSS_ATTN, s);
             hipLaunchKernelGGL(cross_attn_kernel<T>, dim3(H_, n), dim3(64 * CW), 0, s, ca);
             prof_end(WHISPER_K_CROSS_ATTN, s);
@@ -501,9 +511,14 @@ class EngineT final : public Engine {
     // element r0 * K.
     void launch_rows(int r0, int n, bool forced, bool want_logits, hipStream_t s, int c) {
         const int d = d_;
+        unsigned long long* stamps = nullptr;
+        if (stamp_on_) {  // this chain's slots: one (start, end) pair per layer, reset first
+            stamps = stamps_ + (size_t)c * Ld_ * 2;
+            hipLaunchKernelGGL(stamp_reset_kernel, dim3((Ld_ + 63) / 64), dim3(64), 0, s, stamps, Ld_);
+        }
         const StepBufs b{RowBufs{list_ + r0, nullptr, dx_ + (size_t)r0 * d, dz_ + (size_t)r0 * d,
                                  dq_ + (size_t)r0 * d, datt_ + (size_t)r0 * d, dh_ + (size_t)r0 * 4 * d,
-                                 rowlen_ + r0, gpart_ + (size_t)c * KSMAX * S_ * d},
+                                 rowlen_ + r0, gpart_ + (size_t)c * KSMAX * S_ * d, stamps},
                          logits_ + (size_t)r0 * V_, keys_ + (size_t)r0 * nkeys_, outtok_ + r0,
                          forced ? forced_ + r0 : nullptr};
         run_step(b, n, want_logits, s);
@@ -593,6 +608,22 @@ class EngineT final : public Engine {
                          out_tok_dev ? out_tok_dev : reinterpret_cast<int*>(z + L.outtok), nullptr};
         run_step(b, n, false, st_);
         WMI_HIP(hipGetLastError());
+    }
+
+    // Adds the stamped cross-attention spans of the last step's nc chains to
+    // the WHISPER_K_CROSS_ATTN_STEP totals (joins and waits for the step).
+    void read_stamps(int nc) {
+        join_chains();
+        for (int c = 1; c < nc; ++c) WMI_HIP(hipStreamSynchronize(cst_[c]));
+        WMI_HIP(hipStreamSynchronize(st_));
+        std::vector<unsigned long long> h((size_t)nc * Ld_ * 2);
+        WMI_HIP(hipMemcpy(h.data(), stamps_, h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+        Prof& pr = prof_[WHISPER_K_CROSS_ATTN_STEP];
+        for (size_t i = 0; i + 1 < h.size(); i += 2) {
+            if (h[i + 1] < h[i]) continue;  // a launch without rows
+            pr.total_ms += (double)(h[i + 1] - h[i]) / wall_khz_;
+            pr.launches += 1;
+        }
     }
 
     // Raises the device-side decode error flag (a row without an admissible
@@ -711,10 +742,12 @@ class EngineT final : public Engine {
         use_first_ = n_first > 0;
         eot_ = eot;
         // the options are launch arguments of the captured steps
-        for (auto& g : step_graphs_)
-            for (auto ge : g.second)
-                if (ge) WMI_HIP(hipGraphExecDestroy(ge));
-        step_graphs_.clear();
+        for (auto* m : {&step_graphs_, &stamped_graphs_}) {
+            for (auto& g : *m)
+                for (auto ge : g.second)
+                    if (ge) WMI_HIP(hipGraphExecDestroy(ge));
+            m->clear();
+        }
     }
 
     // Snapshot of every slot's stop_at after the work queued so far; poll
@@ -965,6 +998,10 @@ class EngineT final : public Engine {
     static constexpr int MAXC = 4;                                  // chains of a step (hardware queues)
     int chains_ = 2;
     std::map<int, std::array<hipGraphExec_t, MAXC>> step_graphs_;  // per row count: one graph per chain
+    std::map<int, std::array<hipGraphExec_t, MAXC>> stamped_graphs_;  // the same with cross-attention stamps
+    bool stamp_on_ = false;                 // launches being made carry cross-attention stamps
+    unsigned long long* stamps_ = nullptr;  // [chain][layer][2] stamp slots
+    double wall_khz_ = 100000.0;            // real-time counter ticks per millisecond
     hipStream_t cst_[MAXC] = {};                                   // streams of chains 1.. (chain 0: st_)
     hipEvent_t fork_ev_ = nullptr, join_ev_[MAXC] = {};
     // host staging
@@ -1383,6 +1420,12 @@ class EngineT final : public Engine {
         dh_ = dalloc<T>(S16 * 4 * d);
         logits_ = dalloc<float>(S * (size_t)V_);
         gpart_ = dalloc<float>((size_t)MAXC * KSMAX * S * d);  // split-K partials [chain][KS][rows][d]
+        stamps_ = dalloc<unsigned long long>((size_t)MAXC * std::max(Ld_, 1) * 2);
+        {
+            int khz = 0;
+            if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev_) == hipSuccess && khz > 0)
+                wall_khz_ = khz;
+        }
         nkeys_ = std::max(ARGMAX_CHUNKS, (V_ + 31) / 32);
         keys_ = dalloc<unsigned long long>(S * (size_t)nkeys_);
         dec_err_ = dalloc<int>(1);

@@ -658,15 +658,28 @@ __global__ __launch_bounds__(64) void enc_attn_f32_kernel(const float* __restric
 // positions and scores need no cross-lane reduction, values row-major so
 // eight lanes read one 128-byte row; softmax in fp32. self_attn_kernel and
 // cross_attn_kernel below describe their work split.
+// Cache reads are non-temporal: each step streams every cached byte once,
+// so they should not displace the weights and activations the projections
+// keep in L2 (and the stream itself runs faster that way).
 template <class T>
 __device__ inline void load_vec(const T* p, float* out, int n);
 template <>
 __device__ inline void load_vec<bf16>(const bf16* p, float* out, int n) {
-    for (int i = 0; i < n; i += 4) { const float4 v = ld4(p + i); out[i] = v.x; out[i + 1] = v.y; out[i + 2] = v.z; out[i + 3] = v.w; }
+    for (int i = 0; i < n; i += 4) {
+        const u32x2 u = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p + i));
+        out[i] = __uint_as_float(u.x << 16);
+        out[i + 1] = __uint_as_float(u.x & 0xffff0000u);
+        out[i + 2] = __uint_as_float(u.y << 16);
+        out[i + 3] = __uint_as_float(u.y & 0xffff0000u);
+    }
 }
 template <>
 __device__ inline void load_vec<float>(const float* p, float* out, int n) {
-    for (int i = 0; i < n; i += 4) { const float4 v = ld4(p + i); out[i] = v.x; out[i + 1] = v.y; out[i + 2] = v.z; out[i + 3] = v.w; }
+    for (int i = 0; i < n; i += 4) {
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + i));
+        out[i] = v.x; out[i + 1] = v.y; out[i + 2] = v.z; out[i + 3] = v.w;
+    }
 }
 
 struct DecAttnArgs {
@@ -677,6 +690,10 @@ struct DecAttnArgs {
     const int* list;    // row -> slot
     const int* rowlen;  // row -> cached positions incl. this one (self-attention)
     int TP, H, d;
+    // cross-attention timing (null normally): stamp[0] = earliest workgroup
+    // start, stamp[1] = latest workgroup end, in ticks of the device's
+    // real-time counter
+    unsigned long long* stamp;
 };
 
 // Self-attention of one decode position over the slot's cached positions
@@ -796,6 +813,7 @@ __global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {
     __shared__ float ml[CW][2];
     __shared__ float op[CW][64];
     const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    if (a.stamp && tid == 0) atomicMin(a.stamp, (unsigned long long)__builtin_amdgcn_s_memrealtime());
     const int slot = a.list[r];
     const T* q = reinterpret_cast<const T*>(a.q) + (long long)r * a.d + h * 64;
     if (tid < 64) qs[tid] = ldf(q + tid);
@@ -881,6 +899,19 @@ __global__ __launch_bounds__(64 * CW) void cross_attn_kernel(DecAttnArgs a) {
             acc += wgt * op[c][tid];
         }
         stf(reinterpret_cast<T*>(a.out) + dec_off<T>(r, h * 64 + tid, a.d), acc / L);
+    }
+    if (a.stamp) {
+        __syncthreads();
+        if (tid == 0) atomicMax(a.stamp + 1, (unsigned long long)__builtin_amdgcn_s_memrealtime());
+    }
+}
+
+// Timing slots of n launches: start = all ones (for a minimum), end = 0.
+__global__ void stamp_reset_kernel(unsigned long long* __restrict__ s, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) {
+        s[2 * i] = ~0ull;
+        s[2 * i + 1] = 0ull;
     }
 }
 

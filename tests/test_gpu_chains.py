@@ -36,3 +36,27 @@ def test_chains_apart_equal_joined():
         sys.stdout.flush()
     assert out["apart"] == out["joined"]
     assert all(len(t) == s.max_new_tokens for t, s in zip(out["apart"], segs))
+
+
+def test_stamped_cross_attention_steps():
+    """Cross-attention spans stamped inside the captured split steps
+    (WHISPER_K_CROSS_ATTN_STEP): the tokens equal an unstamped call's, every
+    launch (chain x layer x step) is counted, and the average span is
+    positive and below 5 ms."""
+    shape = synth.BASE
+    W = synth.make_weights(shape, 0)
+    segs = synth.uniform_batch(shape, 40, 6, seed=32)
+    with binding.Context(synth.pack_blob(W), max_slots=40) as ctx:
+        want = [r["tokens"].tolist() for r in ctx.transcribe(segs)]
+        ctx.stats(reset=True)
+        ctx.profile_enable(binding.K_CROSS_ATTN_STEP, True)
+        got = [r["tokens"].tolist() for r in ctx.transcribe(segs)]
+        ms, n = ctx.profile_read(binding.K_CROSS_ATTN_STEP)
+        ctx.profile_enable(binding.K_CROSS_ATTN_STEP, False)
+        st = ctx.stats()
+    print(f"stamped: {n} launches, {ms * 1e3 / max(n, 1):.2f} us each", flush=True)
+    assert got == want
+    steps = st["decode_steps"]
+    # one launch per chain and layer: two chains in steps of 32 or more rows, else one
+    assert steps > 0 and n % shape.n_dec == 0 and shape.n_dec * steps <= n <= 2 * shape.n_dec * steps
+    assert 0 < ms / n < 5.0
