@@ -489,7 +489,10 @@ class EngineT final : public Engine {
                  s);
             DecAttnArgs sa{b.dq, kts_ + sl * TS, vs_ + sl * TS, b.datt, b.list, b.rowlen, TS, H_, d};
             prof_begin(WHISPER_K_SELF_ATTN, s);
-            hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, s, sa);
+            if constexpr (std::is_same<T, bf16>::value)
+                hipLaunchKernelGGL(self_attn_bf16_kernel, dim3(H_, n), dim3(256), 0, s, sa);
+            else
+                hipLaunchKernelGGL(self_attn_kernel<T>, dim3(H_, n), dim3(256), 0, s, sa);
             prof_end(WHISPER_K_SELF_ATTN, s);
             self_out_cross_q(L, n, b.datt, b.dq, b.dx, b.dz, b.pbuf, s);
             DecAttnArgs ca{b.dq, ktc_ + sl * TC, vc_ + sl * TC, b.datt, b.list, nullptr, TC, H_, d,

@@ -704,7 +704,8 @@ struct DecAttnArgs {
 //   P V: wave w takes positions 128w..128w+127, 8 lanes per 128-byte V row,
 //     partial outputs added in LDS.
 // (Issuing the V loads together with the K loads measured slower: the K and
-// V phases are kept apart.)
+// V phases are kept apart.) The fp32 model uses this kernel; the bf16 model
+// uses self_attn_bf16_kernel below.
 template <class T>
 __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     __shared__ float qs[64];
@@ -795,6 +796,125 @@ __global__ __launch_bounds__(256) void self_attn_kernel(DecAttnArgs a) {
     if (tid < 64) {
         const float v = ((op[0][tid] + op[1][tid]) + op[2][tid]) + op[3][tid];
         stf(reinterpret_cast<T*>(a.out) + dec_off<T>(r, h * 64 + tid, a.d), v / lsum);
+    }
+}
+
+// Self-attention, second work split (bf16 caches): wave w reads the 16
+// query values of its dims straight from memory (no LDS round trip), sums
+// dims 16w..16w+15 of every position's score as above, and the P V product
+// is spread over all four waves: wave w takes the contiguous positions
+// [w c, w c + c) with c = len / 4 rounded up to a multiple of 8, 8 lanes
+// per 128-byte V row. The first batch of 8 V rows per lane group is issued
+// before the softmax, so its latency overlaps the score reduction. The
+// scores are computed as in self_attn_kernel; the P V sums are grouped by
+// this split, and the waves' partial outputs are added in LDS in wave order.
+__global__ __launch_bounds__(256) void self_attn_bf16_kernel(DecAttnArgs a) {
+    __shared__ float sp[4][512];
+    __shared__ float op[4][64];
+    const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int slot = a.list[r];
+    const int len = a.rowlen[r];
+    const bf16* q = reinterpret_cast<const bf16*>(a.q) + (long long)r * a.d + h * 64 + 16 * w;
+    const u32x4 q0 = *reinterpret_cast<const u32x4*>(q), q1 = *reinterpret_cast<const u32x4*>(q + 8);
+    const long long head = (long long)slot * a.H + h;
+    const bf16* kt = reinterpret_cast<const bf16*>(a.kt) + head * 64 * a.TP;
+    const bf16* vv = reinterpret_cast<const bf16*>(a.v) + head * a.TP * 64;
+    const int p0 = lane * 8;
+    float s[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s[i] = 0.f;
+    if (p0 < len) {
+        float kv[16][8];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) load_vec<bf16>(kt + (long long)(16 * w + j) * a.TP + p0, kv[j], 8);
+        float qv[16];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            qv[2 * e] = __uint_as_float(q0[e] << 16);
+            qv[2 * e + 1] = __uint_as_float(q0[e] & 0xffff0000u);
+            qv[8 + 2 * e] = __uint_as_float(q1[e] << 16);
+            qv[8 + 2 * e + 1] = __uint_as_float(q1[e] & 0xffff0000u);
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) s[i] = fmaf(qv[j], kv[j][i], s[i]);
+    }
+    // this wave's positions for P V, and the first batch of their V rows
+    const int c = ((len + 3) / 4 + 7) & ~7;
+    const int lo = min(len, w * c), hi = min(len, lo + c);
+    const int dg = lane & 7, pg = lane >> 3;
+    u32x4 v0[8];
+    if (lo < hi) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int pc = min(lo + pg + 8 * u, hi - 1);
+            v0[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vv + (long long)pc * 64 + dg * 8));
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sp[w][p0 + i] = s[i];
+    __syncthreads();
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float t = ((sp[0][p0 + i] + sp[1][p0 + i]) + sp[2][p0 + i]) + sp[3][p0 + i];
+        s[i] = (p0 + i < len) ? t * LOG2E : -INFINITY;
+        mx = fmaxf(mx, s[i]);
+    }
+    mx = wave_max(mx);
+    float lsum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        s[i] = (p0 + i < len) ? exp2_softmax(s[i] - mx) : 0.f;
+        lsum += s[i];
+    }
+    lsum = wave_sum(lsum);
+    __syncthreads();  // every wave has read the partial scores
+    if (w == 0) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sp[0][p0 + i] = s[i];
+    }
+    __syncthreads();
+    float o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = 0.f;
+    if (lo < hi) {
+#pragma unroll 1
+        for (int b0 = lo; b0 < hi; b0 += 64) {
+            u32x4 vr[8];
+            float pw[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int pp = b0 + pg + 8 * u;
+                const int pc = min(pp, hi - 1);
+                vr[u] = b0 == lo ? v0[u]
+                                 : __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vv + (long long)pc * 64 + dg * 8));
+                pw[u] = pp < hi ? sp[0][pc] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    o[2 * e] = fmaf(pw[u], __uint_as_float(vr[u][e] << 16), o[2 * e]);
+                    o[2 * e + 1] = fmaf(pw[u], __uint_as_float(vr[u][e] & 0xffff0000u), o[2 * e + 1]);
+                }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        o[i] += __shfl_xor(o[i], 8, 64);
+        o[i] += __shfl_xor(o[i], 16, 64);
+        o[i] += __shfl_xor(o[i], 32, 64);
+    }
+    if (lane < 8) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) op[w][dg * 8 + i] = o[i];
+    }
+    __syncthreads();
+    if (tid < 64) {
+        const float v = ((op[0][tid] + op[1][tid]) + op[2][tid]) + op[3][tid];
+        stf(reinterpret_cast<bf16*>(a.out) + dec_off<bf16>(r, h * 64 + tid, a.d), v / lsum);
     }
 }
 
