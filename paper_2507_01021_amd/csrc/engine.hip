@@ -629,14 +629,15 @@ class EngineT final : public Engine {
         }
     }
 
-    // Raises the device-side decode error flag (a row without an admissible
-    // token) as an error of the call that synchronised; clears it.
+    // Raises the device-side decode error flag (a row or frame without an
+    // admissible token) as an error of the call that synchronised; clears it.
     void check_decode_error() {
         int e = 0;
         WMI_HIP(hipMemcpy(&e, dec_err_, sizeof(int), hipMemcpyDeviceToHost));
         if (e) {
             WMI_HIP(hipMemset(dec_err_, 0, sizeof(int)));
-            throw DeviceError("decode step: a row had no admissible token (non-finite logits); token 0 was recorded");
+            throw DeviceError(ctc_ ? "CTC head: a frame had no finite logit; the blank was recorded for it"
+                                   : "decode step: a row had no admissible token (non-finite logits); token 0 was recorded");
         }
     }
 
@@ -882,6 +883,7 @@ class EngineT final : public Engine {
         WMI_HIP(hipEventSynchronize(ctc_done_[q]));
         WMI_HIP(hipMemcpy(counts, ctc_cnt_[q], n * sizeof(int), hipMemcpyDeviceToHost));
         WMI_HIP(hipMemcpy(tokens, ctc_tok_[q], (size_t)n * N_CTX * sizeof(int), hipMemcpyDeviceToHost));
+        check_decode_error();
     }
 
     double time_cross_attn(int n, int reps) override {
@@ -1213,7 +1215,8 @@ class EngineT final : public Engine {
         if (ctc_) {  // CTC head, per-frame argmax, then decoding into the ticket's buffers
             const int q = ctc_ticket_ & 1;
             gemm(Wctc_, d, 0, zb_, d, 0, V_, M, d, 1, EpiCTC{bctc_, ctc_logits_, V_});
-            hipLaunchKernelGGL(ctc_argmax_kernel, dim3((M + 3) / 4), dim3(256), 0, st_, ctc_logits_, V_, M, ctc_ids_);
+            hipLaunchKernelGGL(ctc_argmax_kernel, dim3((M + 3) / 4), dim3(256), 0, st_, ctc_logits_, V_, M, ctc_ids_,
+                               dec_err_);
             // the batch before last used these buffers: its search must be done
             WMI_HIP(hipStreamWaitEvent(st_, ctc_done_[q], 0));
             if (P_.ctc_beam >= 2) {

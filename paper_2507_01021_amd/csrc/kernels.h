@@ -419,6 +419,12 @@ __global__ __launch_bounds__(resid_ln_threads<E>()) void resid_ln_kernel(const f
 // The P operand uses the lane's own S values directly: the MFMA's reduction
 // index k is mapped to keys so that lane l's eight k's are the keys it holds
 // (keys 4*(l/16)+{0..3} of two 16-key blocks); V^T is read with the same map.
+// LDS tiles are [64 rows][128 bytes] with 16-byte chunks XOR-swizzled by the
+// row. The V^T fragment reads are 8 bytes per lane, and the 16 lanes of one
+// LDS pass read rows r..r+15 at the same key offset: with the 16-byte swizzle
+// alone, rows r and r+8 would hit the same chunk half (a 2-way bank conflict
+// on every pass). In the V^T tile the two 8-byte halves of each chunk are
+// therefore swapped in rows whose bit 3 is set.
 namespace ea {
 constexpr int QW = 64;             // queries per wave
 constexpr int QB = 4 * QW;         // queries per workgroup
@@ -473,13 +479,15 @@ __global__ __launch_bounds__(256, 2) void enc_attn_bf16_kernel(const bf16* __res
             rv[s] = *reinterpret_cast<const u32x4*>(Vb + (long long)(lr + 32 * s) * TQ + k0 + lc * 8);
         }
     };
+    const bool vswap = (lr >> 3) & 1;  // bit 3 of this thread's rows lr and lr + 32
     auto lstore = [&](int buf) {
         unsigned char* tk = lds + buf * 2 * ea::TILE;
         unsigned char* tv = tk + ea::TILE;
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
             *reinterpret_cast<u32x4*>(tk + swz(lr + 32 * s, lc)) = rk[s];
-            *reinterpret_cast<u32x4*>(tv + swz(lr + 32 * s, lc)) = rv[s];
+            *reinterpret_cast<u32x4*>(tv + swz(lr + 32 * s, lc)) =
+                vswap ? u32x4{rv[s].z, rv[s].w, rv[s].x, rv[s].y} : rv[s];
         }
     };
     const int ntiles = (N_CTX + ea::KT - 1) / ea::KT;
@@ -583,10 +591,13 @@ __global__ __launch_bounds__(256, 2) void enc_attn_bf16_kernel(const bf16* __res
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
                 // V^T row (dim) a*16 + fr, keys s*32 + fc*4 .. +3 and s*32 + 16 + fc*4 .. +3
-                const int row = a * 16 + fr;
+                // (bit 3 of the row is bit 3 of fr; it selects the swapped halves)
+                const int row = a * 16 + fr, half = (fr >> 3) & 1;
                 const int kA = s * 32 + fc * 4, kB = kA + 16;
-                const u32x2 lo = *reinterpret_cast<const u32x2*>(tv + swz(row, kA >> 3) + (kA & 7) * 2);
-                const u32x2 hi = *reinterpret_cast<const u32x2*>(tv + swz(row, kB >> 3) + (kB & 7) * 2);
+                const u32x2 lo =
+                    *reinterpret_cast<const u32x2*>(tv + swz(row, kA >> 3) + ((((kA & 7) >> 2) ^ half) << 3));
+                const u32x2 hi =
+                    *reinterpret_cast<const u32x2*>(tv + swz(row, kB >> 3) + ((((kB & 7) >> 2) ^ half) << 3));
                 union { u32x4 u; mfma_bf16x8 v; } cvt;
                 cvt.u = u32x4{lo.x, lo.y, hi.x, hi.y};
 #pragma unroll
@@ -1435,9 +1446,10 @@ inline void skinny_bf16(const bf16* W, int MA, const bf16* X, int n, int K, int 
 // (runs of one id merged, blanks dropped).
 
 // One wave per frame: argmax over the V logits of the frame, the lowest id
-// among equal maxima.
+// among equal maxima. A frame with no finite maximum (every logit -inf or
+// NaN) records the blank and raises *err, which the next read reports.
 __global__ __launch_bounds__(256) void ctc_argmax_kernel(const float* __restrict__ logits, int V, int frames,
-                                                         int* __restrict__ ids) {
+                                                         int* __restrict__ ids, int* __restrict__ err) {
     const int f = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
     if (f >= frames) return;
     const float* row = logits + (long long)f * V;
@@ -1453,7 +1465,10 @@ __global__ __launch_bounds__(256) void ctc_argmax_kernel(const float* __restrict
         const int oi = __shfl_xor(bi, o, 64);
         if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
     }
-    if (lane == 0) ids[f] = bi;
+    if (lane == 0) {
+        ids[f] = bi < V ? bi : 0;   // no finite logit: the blank, and the flag the read reports
+        if (bi >= V) atomicOr(err, 1);
+    }
 }
 
 // One workgroup (1024 threads) per batch entry b over its 1500 frame ids:

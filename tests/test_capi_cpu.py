@@ -140,7 +140,8 @@ def test_greedy_keys_on_host(lib):
     """The decode step's greedy-choice keys, run on the host: the largest
     logit wins, the lowest id among equal logits, negative values and -inf
     order correctly, excluded ids are skipped, and a row with every id
-    excluded yields token 0 with its flag raised (the step's error)."""
+    excluded yields token 0 with its flag raised (the step's error); a row of
+    -inf logits yields id 0 without an error."""
     V = 70
     rng = np.random.default_rng(3)
     lg = rng.normal(size=(6, V)).astype(np.float32)
@@ -157,3 +158,6 @@ def test_greedy_keys_on_host(lib):
     assert tok[4] != 33 and tok[1] == 40 and not bad.any()
     tok, bad = binding.test_greedy_keys(lg[:1], excluded_ids=range(V))
     assert tok.tolist() == [0] and bad.tolist() == [1]
+    # every logit -inf: still a defined choice, the first maximum (id 0), as argmax gives
+    tok, bad = binding.test_greedy_keys(np.full((2, V), -np.inf, np.float32))
+    assert tok.tolist() == [0, 0] and not bad.any()
