@@ -39,7 +39,8 @@ enum {
     WHISPER_OK = 0,
     WHISPER_E_INVAL = -1,    /* bad argument (NULL, out of range, inconsistent) */
     WHISPER_E_NOMEM = -2,    /* device or host allocation failed */
-    WHISPER_E_DEVICE = -3,   /* HIP runtime or kernel launch error */
+    WHISPER_E_DEVICE = -3,   /* HIP runtime or kernel launch error, or non-finite
+                                model output (no admissible token, no finite CTC logit) */
     WHISPER_E_CAPACITY = -4, /* slot index or batch beyond the context's capacity */
     WHISPER_E_STATE = -5,    /* slot busy (encode) or idle (decode step) */
     WHISPER_E_BUFFER = -6,   /* caller's output buffer too small */
@@ -170,6 +171,8 @@ typedef struct whisper_ctx whisper_ctx;
  * (lowest id on ties), runs of one id merged, blanks dropped. Its segments
  * need no prompt (prompt and n_prompt are ignored) and max_new_tokens
  * (1..1500) is the output capacity: n_tokens <= max_new_tokens labels.
+ * A frame with no finite logit (all NaN or -inf) counts as the blank, and
+ * the call that reads its batch fails with WHISPER_E_DEVICE.
  * whisper_batch_transcribe / _serve run the same queue in encoder passes
  * of up to max_encode_batch segments; whisper_batch_encode (n <=
  * max_encode_batch, slots ignored) feeds the debug tensors; the decoder

@@ -104,6 +104,22 @@ def test_ctc_base_bf16_and_queue():
             assert np.array_equal(a["tokens"], b["tokens"])
 
 
+def test_ctc_frames_without_a_finite_logit_raise():
+    """A head whose logits are all NaN (or all -inf) has no best-path id
+    for any frame: the device records the blank for such frames and the
+    call that reads the batch fails with a device error naming the cause,
+    instead of returning an id outside the vocabulary."""
+    shape, segs, slots = synth.workload("ctc-tiny-b2")
+    for bad in (np.nan, -np.inf):
+        W = synth.make_weights(shape, 0)
+        W.values["ctc.b"] = np.full_like(W.values["ctc.b"], bad)
+        with binding.Context(synth.pack_blob(W), max_slots=2) as ctx:
+            with pytest.raises(binding.WhisperError) as e:
+                ctx.transcribe(segs)
+        log(f"head bias {bad}: {e.value}")
+        assert e.value.status == binding.E_DEVICE and "finite logit" in str(e.value)
+
+
 def test_ctc_decoder_calls_refused(tiny):
     shape, W, segs, ref, ctx = tiny
     with pytest.raises(binding.WhisperError):
