@@ -1847,11 +1847,22 @@ __global__ __launch_bounds__(64) void argmax_step_kernel(const unsigned long lon
                                                          int* __restrict__ stop_at, int* __restrict__ err) {
     const int r = blockIdx.x, lane = threadIdx.x;
     const unsigned long long* kr = keys + (long long)r * nk;
-    unsigned long long k = 0;
-    for (int j = lane; j < nk; j += 64) {
-        const unsigned long long c = kr[j];
-        k = c > k ? c : k;
+    // 16 loads in flight per lane (the keys come from other XCDs' writes);
+    // the maximum of integers does not depend on the order it is taken in
+    unsigned long long kk[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) kk[u] = 0;
+    for (int j0 = lane; j0 < nk; j0 += 64 * 16) {
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int j = j0 + 64 * u;
+            const unsigned long long c = j < nk ? kr[j] : 0ull;
+            kk[u] = c > kk[u] ? c : kk[u];
+        }
     }
+    unsigned long long k = kk[0];
+#pragma unroll
+    for (int u = 1; u < 16; ++u) k = kk[u] > k ? kk[u] : k;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
         const unsigned long long c = __shfl_xor(k, o, 64);
