@@ -56,7 +56,8 @@ enum { WHISPER_DTYPE_F32 = 0, WHISPER_DTYPE_BF16 = 1 };
  *   n_audio_ctx       encoder positions, must be 1500 (30 s window)
  *   n_audio_state/head/layer, n_text_state/head/layer: widths, head counts
  *                     (head size must be 64) and layer counts; the two
- *                     widths and head counts must be equal
+ *                     widths and head counts must be equal; width at most
+ *                     2048, at most 256 decoder layers
  *   n_vocab           vocabulary (output head rows)
  *   n_text_ctx        decoder positions, must be 448
  *   dtype             WHISPER_DTYPE_F32: fp32 storage and arithmetic;

@@ -95,8 +95,9 @@ std::string check_params(const whisper_params& p, const whisper_params& blob) {
     if (p.n_audio_head < 1 || p.n_audio_state != 64 * p.n_audio_head) return "head size must be 64";
     if (p.n_audio_state > 2048) return "width above 2048 is not supported";
     if (p.n_mels < 4 || p.n_mels > 128 || p.n_mels % 4) return "n_mels must be a multiple of 4 in 4..128";
-    if (p.n_audio_layer < 1 || p.n_text_layer < 0 || p.n_vocab < (p.n_text_layer == 0 ? 2 : 1))
-        return "encoder layers >= 1, decoder layers >= 0 (0: CTC model), vocabulary >= 1 (CTC: >= 2)";
+    if (p.n_audio_layer < 1 || p.n_text_layer < 0 || p.n_text_layer > 256 ||
+        p.n_vocab < (p.n_text_layer == 0 ? 2 : 1))
+        return "encoder layers >= 1, decoder layers in 0..256 (0: CTC model), vocabulary >= 1 (CTC: >= 2)";
     if (p.max_slots < 1 || p.max_slots > 128) return "max_slots must be in 1..128";
     if (p.max_encode_batch < 0 || p.max_encode_batch > p.max_slots) return "max_encode_batch must be in 0..max_slots";
     if (p.pad_mode != 0 && p.pad_mode != 1) return "pad_mode must be 0 or 1";

@@ -1239,8 +1239,8 @@ class EngineT final : public Engine {
             prof_end(WHISPER_K_ENC_PASS, st_);
             return;
         }
-        gemm(zb_, d, 0, WcK_, d, 0, M, Ld_ * d, d, 1, EpiCrossK<T>{ktc_, slot_of_, d, H_, S_});
-        gemm(WcV_, d, 0, zb_, d, 0, Ld_ * d, M, d, 1, EpiCrossV<T>{bcV_, vc_, slot_of_, d, H_, S_});
+        gemm(zb_, d, 0, WcK_, d, 0, M, Ld_ * d, d, 1, EpiCrossK<T>{ktc_, slot_of_, d, H_, S_, 1.0f / d});
+        gemm(WcV_, d, 0, zb_, d, 0, Ld_ * d, M, d, 1, EpiCrossV<T>{bcV_, vc_, slot_of_, d, H_, S_, 1.0f / d});
         hipLaunchKernelGGL(seat_kernel, dim3(nb), dim3(256), 0, st_, slot_of_, seat_np_, seat_prompts_, seq_, pos_, npr_,
                            stop_at_, prefill_ ? 1 : 0);
         prof_end(WHISPER_K_ENC_PASS, st_);

@@ -129,15 +129,24 @@ struct EpiGelu {
     }
 };
 
+// Layer index n / d of a column n of the stacked per-layer weights, with
+// rd = 1 / d rounded to fp32. For n < 2^20 and d <= 2^11, (n + 1/2) / d lies
+// at least 1 / (2 d) >= 2^-12 from an integer, while the product's error is
+// below (n / d) 2^-23 < 2^-14 (n + 1/2 is exact; rd and the product are
+// each rounded once), so truncation gives the exact quotient. This replaces
+// an integer division (a long instruction sequence) per output.
+__device__ inline int layer_of(int n, float rd) { return (int)(__fmul_rn((float)n + 0.5f, rd)); }
+
 template <class T>
 struct EpiCrossK {  // A = encoder output (4 consecutive positions), B = [Wk of every layer]
     T* kt;               // cross K cache
     const int* slot_of;  // batch entry -> slot
     int d, H, S;
+    float rd;            // 1 / d
     __device__ EpiPre pre(int m, int, int) const { EpiPre p{}; p.s = slot_of[m / N_CTX]; return p; }
     __device__ void operator()(int m, int n, int, float a, float b, float c, float e, const EpiPre& p) const {
         const int bseg = m / N_CTX, t = m - bseg * N_CTX;
-        const int l = n / d, f = n - l * d, h = f >> 6, jj = f & 63;
+        const int l = layer_of(n, rd), f = n - l * d, h = f >> 6, jj = f & 63;
         const long long base = (((long long)l * S + p.s) * H + h) * 64 + jj;
         st4(kt + base * TC + t, a, b, c, e);
     }
@@ -149,6 +158,7 @@ struct EpiCrossV {  // A = [Wv of every layer], B = encoder output
     T* v;             // cross V cache
     const int* slot_of;
     int d, H, S;
+    float rd;  // 1 / d
     __device__ EpiPre pre(int n, int m, int) const {
         EpiPre p{};
         p.a = ld4(bv + n);
@@ -157,7 +167,7 @@ struct EpiCrossV {  // A = [Wv of every layer], B = encoder output
     }
     __device__ void operator()(int n, int m, int, float a, float b, float c, float e, const EpiPre& p) const {
         const int bseg = m / N_CTX, t = m - bseg * N_CTX;
-        const int l = n / d, f = n - l * d, h = f >> 6, jj = f & 63;
+        const int l = layer_of(n, rd), f = n - l * d, h = f >> 6, jj = f & 63;
         const long long row = (((long long)l * S + p.s) * H + h) * TC + t;
         st4(v + row * 64 + jj, a + p.a.x, b + p.a.y, c + p.a.z, e + p.a.w);
     }

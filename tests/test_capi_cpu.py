@@ -161,3 +161,16 @@ def test_greedy_keys_on_host(lib):
     # every logit -inf: still a defined choice, the first maximum (id 0), as argmax gives
     tok, bad = binding.test_greedy_keys(np.full((2, V), -np.inf, np.float32))
     assert tok.tolist() == [0, 0] and not bad.any()
+
+
+def test_cross_cache_layer_index_is_exact():
+    """The cross-attention K/V epilogues find the layer of a stacked weight
+    column n as trunc((n + 1/2) * fp32(1/d)) in fp32 arithmetic instead of an
+    integer division. The bound behind it (n < 2^20, d <= 2^11) covers every
+    width the library accepts (64 x 6 .. 64 x 32) with up to 256 decoder
+    layers; checked here exhaustively in the same fp32 arithmetic."""
+    for d in (384, 512, 768, 1024, 1280, 1536, 2048):
+        n = np.arange(256 * d, dtype=np.int64)
+        rd = np.float32(1.0) / np.float32(d)
+        l = ((n.astype(np.float32) + np.float32(0.5)) * rd).astype(np.int64)
+        assert np.array_equal(l, n // d), d
