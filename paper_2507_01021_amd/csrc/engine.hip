@@ -269,6 +269,9 @@ class EngineT final : public Engine {
             WMI_HIP(hipEventCreateWithFlags(&join_ev_[c], hipEventDisableTiming));
         }
         WMI_HIP(hipEventCreateWithFlags(&fork_ev_, hipEventDisableTiming));
+        WMI_HIP(hipStreamCreateWithFlags(&es_, hipStreamNonBlocking));
+        WMI_HIP(hipEventCreateWithFlags(&enc_fork_, hipEventDisableTiming));
+        WMI_HIP(hipEventCreateWithFlags(&enc_join_, hipEventDisableTiming));
         st_ = own_stream_;
         if (const char* g = getenv("WHISPER_STEP_GRAPHS")) graphs_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_STEP_SPLIT")) split_ = g[0] != '0';
@@ -276,6 +279,7 @@ class EngineT final : public Engine {
         if (const char* g = getenv("WHISPER_FUSED_LN")) fused_ln_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_FREE_CHAINS")) free_run_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_FC2_SPLIT")) fc2_split_ = atoi(g);
+        if (const char* g = getenv("WHISPER_ENC_SPLIT")) enc_split_ = g[0] != '0';
         load_weights(blob, bytes);
         alloc_state();
         scratch_ = static_cast<unsigned char*>(scratch_address(dev_));
@@ -285,6 +289,7 @@ class EngineT final : public Engine {
     ~EngineT() override {
         (void)hipSetDevice(dev_);
         if (st_) (void)hipStreamSynchronize(st_);
+        if (es_) (void)hipStreamSynchronize(es_);
         if (ctc_st_) (void)hipStreamSynchronize(ctc_st_);
         for (auto& pr : prof_)
             for (auto& e : pr.used) { (void)hipEventDestroy(e.first); (void)hipEventDestroy(e.second); }
@@ -317,6 +322,9 @@ class EngineT final : public Engine {
             if (ctc_done_[q]) (void)hipEventDestroy(ctc_done_[q]);
         }
         if (ctc_st_) (void)hipStreamDestroy(ctc_st_);
+        if (enc_fork_) (void)hipEventDestroy(enc_fork_);
+        if (enc_join_) (void)hipEventDestroy(enc_join_);
+        if (es_) (void)hipStreamDestroy(es_);
         if (own_stream_) (void)hipStreamDestroy(own_stream_);
     }
 
@@ -1008,6 +1016,9 @@ class EngineT final : public Engine {
     unsigned long long* stamps_ = nullptr;  // [chain][layer][2] stamp slots
     double wall_khz_ = 100000.0;            // real-time counter ticks per millisecond
     hipStream_t cst_[MAXC] = {};                                   // streams of chains 1.. (chain 0: st_)
+    hipStream_t es_ = nullptr;                                     // the encoder pass's second half
+    hipEvent_t enc_fork_ = nullptr, enc_join_ = nullptr;
+    bool enc_split_ = true;
     hipEvent_t fork_ev_ = nullptr, join_ev_[MAXC] = {};
     // host staging
     Stage stage_[4];
@@ -1092,9 +1103,9 @@ class EngineT final : public Engine {
     }
 
     // -------------------------------------------------------------- kernels
-    void ln(const float* x, T* y, const float* g, const float* b, int rows) {
-        WMI_SWITCH_E(d_, hipLaunchKernelGGL((layer_norm_kernel<T, E>), dim3((rows + 3) / 4), dim3(256), 0, st_, x,
-                                            y, g, b, rows));
+    void ln(const float* x, T* y, const float* g, const float* b, int rows, hipStream_t s = nullptr) {
+        WMI_SWITCH_E(d_, hipLaunchKernelGGL((layer_norm_kernel<T, E>), dim3((rows + 3) / 4), dim3(256), 0,
+                                            s ? s : st_, x, y, g, b, rows));
     }
     // decoder: x += split-K partials + bias, then z = LN(x)
     void resid_ln(int KS, int n, const float* bias, const float* g, const float* b, float* part, float* dx, T* dz,
@@ -1128,9 +1139,43 @@ class EngineT final : public Engine {
 
     template <class Epi>
     void gemm(const T* A, int lda, long long sA, const T* B, int ldb, long long sB, int MA, int MB, int K, int batch,
-              const Epi& epi) {
-        if constexpr (std::is_same<T, bf16>::value) gemm_bf16(A, lda, sA, B, ldb, sB, MA, MB, K, batch, epi, st_);
-        else gemm_simt(A, lda, sA, B, ldb, sB, MA, MB, K, batch, epi, st_);
+              const Epi& epi, hipStream_t s = nullptr) {
+        if (!s) s = st_;
+        if constexpr (std::is_same<T, bf16>::value) gemm_bf16(A, lda, sA, B, ldb, sB, MA, MB, K, batch, epi, s);
+        else gemm_simt(A, lda, sA, B, ldb, sB, MA, MB, K, batch, epi, s);
+    }
+
+    // Encoder layer l over segments b0 .. b0 + nb - 1 of the pass, on stream
+    // s: every buffer is addressed from that segment range, so two ranges
+    // can run on two streams at once.
+    void encoder_layer(int l, int b0, int nb, hipStream_t s) {
+        const EncLayerW<T>& L = enc_[l];
+        const int d = d_, M = nb * N_CTX;
+        const long long tok = (long long)b0 * N_CTX, head = (long long)b0 * H_ * TQ * 64;
+        float* x = x_ + tok * d;
+        T* zb = zb_ + tok * d;
+        T* qh = qh_ + head;
+        T* kh = kh_ + head;
+        T* vt = vt_ + head;
+        T* ob = ob_ + tok * d;
+        T* hb = hb_ + tok * 4 * d;
+        ln(x, zb, L.ln1g, L.ln1b, M, s);
+        gemm(L.Wqk, d, 0, zb, d, 0, 2 * d, M, d, 1, EpiQK<T>{L.bq, qh, kh, d, H_}, s);
+        gemm(zb, d, 0, L.Wv, d, 0, M, d, d, 1, EpiVt<T>{L.bv, vt, H_}, s);
+        prof_begin(WHISPER_K_ENC_ATTN, s);
+        if constexpr (std::is_same<T, bf16>::value)
+            hipLaunchKernelGGL(enc_attn_bf16_kernel, dim3((N_CTX + ea::QB - 1) / ea::QB, nb * H_), dim3(256), 0, s,
+                               qh, kh, vt, ob, H_, d);
+        else
+            hipLaunchKernelGGL(enc_attn_f32_kernel, dim3((N_CTX + 63) / 64, nb * H_), dim3(64), 0, s, qh, kh, vt, ob,
+                               H_, d);
+        prof_end(WHISPER_K_ENC_ATTN, s);
+        gemm(L.Wo, d, 0, ob, d, 0, d, M, d, 1, EpiResid{L.bo, x, d}, s);
+        ln(x, zb, L.ln2g, L.ln2b, M, s);
+        prof_begin(WHISPER_K_ENC_GEMM, s);
+        gemm(L.W1, d, 0, zb, d, 0, 4 * d, M, d, 1, EpiGelu<T>{L.b1, hb, 4 * d}, s);
+        prof_end(WHISPER_K_ENC_GEMM, s);
+        gemm(L.W2, 4 * d, 0, hb, 4 * d, 0, d, M, 4 * d, 1, EpiResid{L.b2, x, d}, s);
     }
 
     // decode projection: rows = weight rows (MA), n activation rows of width K
@@ -1191,25 +1236,25 @@ class EngineT final : public Engine {
         prof_end(WHISPER_K_FRONT_END, st_);
         gemm(W1r_, 3 * CP, 0, ypad_, CP, 3002LL * CP, d, 3000, 3 * CP, nb, EpiConv1<T>{cb1_, h1_, d});
         gemm(W2r_, 3 * d, 0, h1_, 2 * d, 3002LL * d, d, N_CTX, 3 * d, nb, EpiConv2{cb2_, pe_, x_, d});
-        for (int l = 0; l < Le_; ++l) {
-            const EncLayerW<T>& L = enc_[l];
-            ln(x_, zb_, L.ln1g, L.ln1b, M);
-            gemm(L.Wqk, d, 0, zb_, d, 0, 2 * d, M, d, 1, EpiQK<T>{L.bq, qh_, kh_, d, H_});
-            gemm(zb_, d, 0, L.Wv, d, 0, M, d, d, 1, EpiVt<T>{L.bv, vt_, H_});
-            prof_begin(WHISPER_K_ENC_ATTN, st_);
-            if constexpr (std::is_same<T, bf16>::value)
-                hipLaunchKernelGGL(enc_attn_bf16_kernel, dim3((N_CTX + ea::QB - 1) / ea::QB, nb * H_), dim3(256), 0,
-                                   st_, qh_, kh_, vt_, ob_, H_, d);
-            else
-                hipLaunchKernelGGL(enc_attn_f32_kernel, dim3((N_CTX + 63) / 64, nb * H_), dim3(64), 0, st_, qh_, kh_,
-                                   vt_, ob_, H_, d);
-            prof_end(WHISPER_K_ENC_ATTN, st_);
-            gemm(L.Wo, d, 0, ob_, d, 0, d, M, d, 1, EpiResid{L.bo, x_, d});
-            ln(x_, zb_, L.ln2g, L.ln2b, M);
-            prof_begin(WHISPER_K_ENC_GEMM, st_);
-            gemm(L.W1, d, 0, zb_, d, 0, 4 * d, M, d, 1, EpiGelu<T>{L.b1, hb_, 4 * d});
-            prof_end(WHISPER_K_ENC_GEMM, st_);
-            gemm(L.W2, 4 * d, 0, hb_, 4 * d, 0, d, M, 4 * d, 1, EpiResid{L.b2, x_, d});
+        // Two halves of the pass on two streams (bf16 models): the segments
+        // are independent, and the halves' kernels fill each other's
+        // partial last rounds and spread the epilogues' memory phases. With
+        // the per-kernel encoder timers on, one stream, so each timed
+        // launch covers the whole pass.
+        const bool split = std::is_same<T, bf16>::value && enc_split_ && nb >= 2 &&
+                           !prof_[WHISPER_K_ENC_GEMM].on && !prof_[WHISPER_K_ENC_ATTN].on;
+        if (split) {
+            const int nb0 = nb / 2;
+            WMI_HIP(hipEventRecord(enc_fork_, st_));
+            WMI_HIP(hipStreamWaitEvent(es_, enc_fork_, 0));
+            for (int l = 0; l < Le_; ++l) {
+                encoder_layer(l, 0, nb0, st_);
+                encoder_layer(l, nb0, nb - nb0, es_);
+            }
+            WMI_HIP(hipEventRecord(enc_join_, es_));
+            WMI_HIP(hipStreamWaitEvent(st_, enc_join_, 0));
+        } else {
+            for (int l = 0; l < Le_; ++l) encoder_layer(l, 0, nb, st_);
         }
         ln(x_, zb_, lnpg_, lnpb_, M);
         if (ctc_) {  // CTC head, per-frame argmax, then decoding into the ticket's buffers
