@@ -269,9 +269,11 @@ class EngineT final : public Engine {
             WMI_HIP(hipEventCreateWithFlags(&join_ev_[c], hipEventDisableTiming));
         }
         WMI_HIP(hipEventCreateWithFlags(&fork_ev_, hipEventDisableTiming));
-        WMI_HIP(hipStreamCreateWithFlags(&es_, hipStreamNonBlocking));
+        for (int k = 0; k < ENC_PARTS_MAX - 1; ++k) {
+            WMI_HIP(hipStreamCreateWithFlags(&es_[k], hipStreamNonBlocking));
+            WMI_HIP(hipEventCreateWithFlags(&enc_join_[k], hipEventDisableTiming));
+        }
         WMI_HIP(hipEventCreateWithFlags(&enc_fork_, hipEventDisableTiming));
-        WMI_HIP(hipEventCreateWithFlags(&enc_join_, hipEventDisableTiming));
         st_ = own_stream_;
         if (const char* g = getenv("WHISPER_STEP_GRAPHS")) graphs_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_STEP_SPLIT")) split_ = g[0] != '0';
@@ -279,7 +281,7 @@ class EngineT final : public Engine {
         if (const char* g = getenv("WHISPER_FUSED_LN")) fused_ln_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_FREE_CHAINS")) free_run_ = g[0] != '0';
         if (const char* g = getenv("WHISPER_FC2_SPLIT")) fc2_split_ = atoi(g);
-        if (const char* g = getenv("WHISPER_ENC_SPLIT")) enc_split_ = g[0] != '0';
+        if (const char* g = getenv("WHISPER_ENC_SPLIT")) enc_parts_ = std::max(1, std::min(ENC_PARTS_MAX, atoi(g)));
         load_weights(blob, bytes);
         alloc_state();
         scratch_ = static_cast<unsigned char*>(scratch_address(dev_));
@@ -289,7 +291,8 @@ class EngineT final : public Engine {
     ~EngineT() override {
         (void)hipSetDevice(dev_);
         if (st_) (void)hipStreamSynchronize(st_);
-        if (es_) (void)hipStreamSynchronize(es_);
+        for (auto q : es_)
+            if (q) (void)hipStreamSynchronize(q);
         if (ctc_st_) (void)hipStreamSynchronize(ctc_st_);
         for (auto& pr : prof_)
             for (auto& e : pr.used) { (void)hipEventDestroy(e.first); (void)hipEventDestroy(e.second); }
@@ -323,8 +326,10 @@ class EngineT final : public Engine {
         }
         if (ctc_st_) (void)hipStreamDestroy(ctc_st_);
         if (enc_fork_) (void)hipEventDestroy(enc_fork_);
-        if (enc_join_) (void)hipEventDestroy(enc_join_);
-        if (es_) (void)hipStreamDestroy(es_);
+        for (int k = 0; k < ENC_PARTS_MAX - 1; ++k) {
+            if (enc_join_[k]) (void)hipEventDestroy(enc_join_[k]);
+            if (es_[k]) (void)hipStreamDestroy(es_[k]);
+        }
         if (own_stream_) (void)hipStreamDestroy(own_stream_);
     }
 
@@ -1016,9 +1021,10 @@ class EngineT final : public Engine {
     unsigned long long* stamps_ = nullptr;  // [chain][layer][2] stamp slots
     double wall_khz_ = 100000.0;            // real-time counter ticks per millisecond
     hipStream_t cst_[MAXC] = {};                                   // streams of chains 1.. (chain 0: st_)
-    hipStream_t es_ = nullptr;                                     // the encoder pass's second half
-    hipEvent_t enc_fork_ = nullptr, enc_join_ = nullptr;
-    bool enc_split_ = true;
+    static constexpr int ENC_PARTS_MAX = 4;
+    hipStream_t es_[ENC_PARTS_MAX - 1] = {};                       // the encoder pass's parts 1..
+    hipEvent_t enc_fork_ = nullptr, enc_join_[ENC_PARTS_MAX - 1] = {};
+    int enc_parts_ = 2;
     hipEvent_t fork_ev_ = nullptr, join_ev_[MAXC] = {};
     // host staging
     Stage stage_[4];
@@ -1236,23 +1242,27 @@ class EngineT final : public Engine {
         prof_end(WHISPER_K_FRONT_END, st_);
         gemm(W1r_, 3 * CP, 0, ypad_, CP, 3002LL * CP, d, 3000, 3 * CP, nb, EpiConv1<T>{cb1_, h1_, d});
         gemm(W2r_, 3 * d, 0, h1_, 2 * d, 3002LL * d, d, N_CTX, 3 * d, nb, EpiConv2{cb2_, pe_, x_, d});
-        // Two halves of the pass on two streams (bf16 models): the segments
-        // are independent, and the halves' kernels fill each other's
-        // partial last rounds and spread the epilogues' memory phases. With
-        // the per-kernel encoder timers on, one stream, so each timed
-        // launch covers the whole pass.
-        const bool split = std::is_same<T, bf16>::value && enc_split_ && nb >= 2 &&
-                           !prof_[WHISPER_K_ENC_GEMM].on && !prof_[WHISPER_K_ENC_ATTN].on;
-        if (split) {
-            const int nb0 = nb / 2;
+        // The pass in parts of its segments on parallel streams (bf16
+        // models): the segments are independent, and the parts' kernels fill
+        // each other's partial last rounds and spread the epilogues' memory
+        // phases. With the per-kernel encoder timers on, one stream, so each
+        // timed launch covers the whole pass.
+        const int parts = std::is_same<T, bf16>::value && !prof_[WHISPER_K_ENC_GEMM].on &&
+                                  !prof_[WHISPER_K_ENC_ATTN].on
+                              ? std::min(enc_parts_, nb)
+                              : 1;
+        if (parts > 1) {
             WMI_HIP(hipEventRecord(enc_fork_, st_));
-            WMI_HIP(hipStreamWaitEvent(es_, enc_fork_, 0));
-            for (int l = 0; l < Le_; ++l) {
-                encoder_layer(l, 0, nb0, st_);
-                encoder_layer(l, nb0, nb - nb0, es_);
+            for (int k = 1; k < parts; ++k) WMI_HIP(hipStreamWaitEvent(es_[k - 1], enc_fork_, 0));
+            for (int l = 0; l < Le_; ++l)
+                for (int k = 0; k < parts; ++k) {
+                    const int b0 = nb * k / parts, b1 = nb * (k + 1) / parts;
+                    encoder_layer(l, b0, b1 - b0, k == 0 ? st_ : es_[k - 1]);
+                }
+            for (int k = 1; k < parts; ++k) {
+                WMI_HIP(hipEventRecord(enc_join_[k - 1], es_[k - 1]));
+                WMI_HIP(hipStreamWaitEvent(st_, enc_join_[k - 1], 0));
             }
-            WMI_HIP(hipEventRecord(enc_join_, es_));
-            WMI_HIP(hipStreamWaitEvent(st_, enc_join_, 0));
         } else {
             for (int l = 0; l < Le_; ++l) encoder_layer(l, 0, nb, st_);
         }
