@@ -71,6 +71,45 @@ __device__ inline void xcd_tile(int bid, int tilesA, int tilesB, int& ta, int& t
     ta = g * GA + (w - tb * ga);
 }
 
+// Epilogue of a wave's NI x 4 blocks of 16 x 16 results: lane (fr, fc) of
+// block (i, j) holds rows ia + 16 i + 4 fc .. + 3 of column jb + 16 j + fr.
+// For each column block, all of its loads (pre) are issued before its
+// stores. A tile wholly inside the output (full, the common case) skips the
+// per-element bounds tests, each a branch and an exec-mask update.
+template <int NI, class Epi>
+__device__ __forceinline__ void tile_epilogue(const Epi& epi, const mfma_f32x4 (&acc)[NI][4], int ia, int jb, int fr,
+                                              int fc, int z, int MA, int MB, bool full) {
+    if (full) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int jj = jb + j * 16 + fr;
+            EpiPre pre[NI];
+#pragma unroll
+            for (int i = 0; i < NI; ++i) pre[i] = epi.pre(ia + i * 16 + fc * 4, jj, z);
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+                epi(ia + i * 16 + fc * 4, jj, z, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], pre[i]);
+        }
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int jj = jb + j * 16 + fr;
+        const bool jok = jj < MB;
+        EpiPre pre[NI];
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int ii = ia + i * 16 + fc * 4;
+            if (jok && ii < MA) pre[i] = epi.pre(ii, jj, z);
+        }
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int ii = ia + i * 16 + fc * 4;
+            if (jok && ii < MA) epi(ii, jj, z, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], pre[i]);
+        }
+    }
+}
+
 // C = A B^T for A [MA][K], B [MB][K] (bf16, row-major, batched over z):
 // a 256 x 256 workgroup tile, 8 waves (2 per SIMD) of 128 x 64 each on
 // 16x16x32 MFMAs, so one wave's MFMAs run while the other waits on its LDS
@@ -150,22 +189,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_kernel(
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
 #undef WMI_ISSUE8
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int jj = b0 + wb + j * 16 + fr;
-        const bool jok = jj < MB;
-        EpiPre pre[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int ii = a0 + wa + i * 16 + fc * 4;
-            if (jok && ii < MA) pre[i] = epi.pre(ii, jj, z);
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int ii = a0 + wa + i * 16 + fc * 4;
-            if (jok && ii < MA) epi(ii, jj, z, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], pre[i]);
-        }
-    }
+    tile_epilogue(epi, acc, a0 + wa, b0 + wb, fr, fc, z, MA, MB, a0 + gb::BM <= MA && b0 + gb::BN <= MB);
 }
 
 // Two-workgroups-per-CU variant: a 256 x 128 tile, 8 waves of 64 x 64
@@ -242,22 +266,7 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_h_kernel(
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
 #undef WMI_ISSUE3
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int jj = b0 + wb + j * 16 + fr;
-        const bool jok = jj < MB;
-        EpiPre pre[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int ii = a0 + wa + i * 16 + fc * 4;
-            if (jok && ii < MA) pre[i] = epi.pre(ii, jj, z);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int ii = a0 + wa + i * 16 + fc * 4;
-            if (jok && ii < MA) epi(ii, jj, z, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3], pre[i]);
-        }
-    }
+    tile_epilogue(epi, acc, a0 + wa, b0 + wb, fr, fc, z, MA, MB, a0 + gh::BM <= MA && b0 + gh::BN <= MB);
 }
 
 // Raises kernel f's dynamic LDS limit to `bytes` on the current device, once
