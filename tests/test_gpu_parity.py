@@ -285,3 +285,31 @@ def test_tiny_end_of_text_and_logit_filters_match_oracle(tiny):
         assert not np.isin(r["tokens"], list(suppress)).any()
         if r["tokens"].size:
             assert int(r["tokens"][0]) not in first
+
+
+def test_base_encoder_parts_bit_identical(monkeypatch):
+    """An encode pass may run its layers in parts of its segments on
+    parallel streams (WHISPER_ENC_SPLIT, read at context creation). A
+    segment's encoder output does not depend on that, nor on the other
+    segments of its pass (bit-exact): every GEMM output row, attention head
+    and layer norm belongs to one segment."""
+    shape = synth.BASE
+    W = synth.make_weights(shape, 0)
+    blob = synth.pack_blob(W)
+    segs = synth.fixed_batch(shape, [16000 * s for s in (3, 11, 30, 7, 19)], 4, seed=9)
+    outs = {}
+    for parts in ("1", "2", "3"):
+        monkeypatch.setenv("WHISPER_ENC_SPLIT", parts)
+        with binding.Context(blob, max_slots=10) as ctx:
+            ctx.encode(segs, [0, 1, 2, 3, 4])
+            outs[parts] = [ctx.debug_copy(binding.T_ENC_OUT, i, (1500, shape.d)) for i in range(5)]
+            if parts == "2":
+                solo = []
+                for i, s in enumerate(segs):
+                    ctx.encode([s], [5 + i])
+                    solo.append(ctx.debug_copy(binding.T_ENC_OUT, 0, (1500, shape.d)))
+        log(f"parts={parts}: encoded")
+    for i in range(5):
+        assert np.array_equal(outs["1"][i], outs["2"][i])
+        assert np.array_equal(outs["1"][i], outs["3"][i])
+        assert np.array_equal(outs["1"][i], solo[i])
