@@ -11,6 +11,9 @@ Prints one JSON line: RTFx (audio seconds transcribed per second), the
 roofline of the dominant kernel (decode-step cross-attention, HBM-bound)
 measured with HIP events on the library's stream, encoder MFMA and decode
 HBM fractions, and the CPU oracle timed on a bounded sample on the host.
+After the headline workload, each `--secondary` workload (by default the
+128-slot refill queue and the 64-slot ragged batch) gets one timed call with
+the same encoder and decode accounting, under "secondary".
 
     python bench.py [--steps K] [--warmup W] [--workload large-v3-b32]
 """
@@ -286,8 +289,9 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="large-v3-b32")
-    ap.add_argument("--secondary", default="turbo-u64-q512",
-                    help="refill workload measured after the headline one in the same run ('' to skip)")
+    ap.add_argument("--secondary", default="turbo-u64-q512,small-u8-b64",
+                    help="comma-separated decoder workloads (continuous batching with refill, ragged "
+                         "retirement) measured after the headline one in the same run ('' to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
@@ -357,15 +361,19 @@ def main():
         # every segment is encoded as a full 30 s window: RTFx over padded seconds
         "padded_rtfx": r["padded_rtfx"],
     }
-    if a.secondary and a.secondary != a.workload and not a.max_new:
-        # the refill workload (continuous batching with slot refill), one
-        # timed call after one warm-up call, same accounting
-        r2, ctx2, shape2, _, segs2, slots2, _, audio2 = run_decoder_workload(
-            binding, torch, a.secondary, 1, 1, a.pad_mode, 0, a.prefill, 0, per_kernel=False)
-        ctx2.close()
-        out["secondary"] = {"workload": a.secondary, "segments": len(segs2), "slots": slots2,
-                            "audio_s": round(audio2, 2), "value": r2["value"], "unit": "audio-s/s",
-                            "ms_per_call": r2["ms_per_call"], "encoder": r2["encoder"], "decode": r2["decode"]}
+    more = [w for w in a.secondary.split(",") if w and w != a.workload] if not a.max_new else []
+    if more:
+        # the refill / ragged workloads, each one timed call after one
+        # warm-up call, same accounting
+        out["secondary"] = []
+        for w in more:
+            r2, ctx2, shape2, _, segs2, slots2, _, audio2 = run_decoder_workload(
+                binding, torch, w, 1, 1, a.pad_mode, 0, a.prefill, 0, per_kernel=False)
+            ctx2.close()
+            out["secondary"].append({"workload": w, "segments": len(segs2), "slots": slots2,
+                                     "audio_s": round(audio2, 2), "value": r2["value"], "unit": "audio-s/s",
+                                     "ms_per_call": r2["ms_per_call"], "encoder": r2["encoder"],
+                                     "decode": r2["decode"]})
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, W, segs)
     print(json.dumps(out), flush=True)
