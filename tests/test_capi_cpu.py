@@ -174,3 +174,22 @@ def test_cross_cache_layer_index_is_exact():
         rd = np.float32(1.0) / np.float32(d)
         l = ((n.astype(np.float32) + np.float32(0.5)) * rd).astype(np.int64)
         assert np.array_equal(l, n // d), d
+
+
+def test_c_client_builds_against_the_header(lib, tmp_path):
+    """tests/c_client.c (the plain C caller the GPU tests run) compiles
+    warning-free against the header, links the library and rejects a
+    missing argument before any library call."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    lib_dir = os.path.dirname(binding.LIB_PATH)
+    exe = str(tmp_path / "whisper_c_client")
+    subprocess.run([cc, "-O2", "-std=c11", "-Wall", "-Wextra", "-Werror", "-I", os.path.join(root, "include"),
+                    os.path.join(root, "tests", "c_client.c"), "-L", lib_dir, "-lwhisper_mi355x",
+                    f"-Wl,-rpath,{lib_dir}", "-o", exe], check=True)
+    p = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert p.returncode == 1 and "usage" in p.stderr
