@@ -54,13 +54,21 @@ def check_tokens(gpu_tok, ref_logits, tol=None, gpu_logits=None, min_strict=1):
     return strict, near
 
 
-def check_free_run(gpu_tok, ref_tok, ref_logits, band, min_agree=1):
+def check_free_run(gpu_tok, ref_tok, ref_logits, band, min_agree=1, along=None):
     """A free run (each side feeding its own choices back) against the
     oracle's: the tokens agree up to the first position where they differ;
     there the oracle's choice must have been a near tie (top-1 - top-2 within
     the band of that position) and the GPU's token must lie within the band
     of the top-1. Returns the number of leading tokens that agree (asserted
-    to be at least min_agree, or the whole run)."""
+    to be at least min_agree, or the whole run).
+
+    With `along` (a function that returns the oracle's logits at every
+    position when the oracle is fed the GPU's own tokens), a run that
+    leaves the oracle's at a near tie is followed to its end on the GPU's
+    path: every later GPU token must be the oracle's choice on that path
+    where the choice is clear, and lie within the band of its top-1 where it
+    is a near tie (past the split, the band is the largest of `band`). The
+    whole run is then checked, and the return value is its length."""
     gpu_tok = np.asarray(gpu_tok)
     ref_tok = np.asarray(ref_tok)
     n = min(gpu_tok.size, ref_tok.size)
@@ -72,6 +80,17 @@ def check_free_run(gpu_tok, ref_tok, ref_logits, band, min_agree=1):
         top = np.sort(o)[-2:]
         assert top[1] - top[0] <= band[i], ("free run diverged at a clear position", i, top[1] - top[0], band[i])
         assert o[int(gpu_tok[i])] >= top[1] - band[i]
+        if along is not None:
+            lg = np.asarray(along(gpu_tok[:n]), np.float64)
+            b = float(np.max(band))
+            for j in range(i + 1, n):
+                order = np.argsort(-lg[j], kind="stable")
+                t1, t2, g = lg[j, order[0]], lg[j, order[1]], int(gpu_tok[j])
+                if t1 - t2 > b:
+                    assert g == int(order[0]), ("GPU path: not the oracle's clear choice", j, g, int(order[0]))
+                else:
+                    assert lg[j, g] >= t1 - b, ("GPU path: outside the near-tie band", j, g, t1 - lg[j, g], b)
+            i = n
     assert i >= min(min_agree, n), (i, min_agree)
     return i
 

@@ -8,8 +8,10 @@ the oracle computes one by one, over each workload's whole decode length:
   (64 for the base workload, 224 for large-v3 in the 32-slot two-chain
   step, the full ragged lengths of the small and turbo queues);
 * free-running tokens (a whole transcribe call) against the oracle's own
-  free run, up to the first position where they differ, which must be a
-  near tie;
+  free run up to the first position where they differ, which must be a
+  near tie, and from there on against the oracle fed the GPU's own tokens
+  (clear choices equal, near ties within the band), so every token of the
+  run is checked;
 * for whole transcribe calls, the exact id mapping, token placement and
   work counters of every segment, and batch = solo.
 
@@ -35,15 +37,21 @@ def log(*a):
 
 
 def oracle_segment(W, shape, seg, n_steps):
-    """The oracle's free greedy run of one segment: encoder output, tokens
-    and the logits of every choice (progress printed as it goes)."""
+    """The oracle's free greedy run of one segment: encoder output, tokens,
+    the logits of every choice (progress printed as it goes) and a function
+    that returns the oracle's logits along a given token path."""
     mel = oracle.log_mel_segment(seg.audio, shape.n_mels)
     E = M.encoder(W, shape, mel[None])
     log(f"  oracle encoder done")
     ckv = M._seg_ckv(M.cross_kv(W, shape, E), 0)
     toks, lg = M.greedy(W, shape, ckv, seg.prompt, n_steps,
                         progress=lambda i: i % 32 == 0 and log(f"  oracle step {i} of {n_steps}"))
-    return E[0], toks, lg
+
+    def along(path):
+        log(f"  oracle along the GPU's path, {len(path)} tokens")
+        return M.greedy(W, shape, ckv, seg.prompt, len(path), forced=[int(t) for t in path])[1]
+
+    return E[0], toks, lg, along
 
 
 def run_teacher_forced(ctx, slots, forced_by_index, n_prompt, n_gen, other_tok=220):
@@ -124,8 +132,8 @@ def test_fixed_batch_bench_config(name, sample):
             assert (r["user_id"], r["segment_id"], r["status"]) == (s.user_id, s.segment_id, 0)
             assert r["tokens"].size == s.max_new_tokens
         for k in sample:
-            agree = check_free_run(res[k]["tokens"], refs[k][1], refs[k][2], band[k])
-            log(f"{name}: segment {k} free run agrees with the oracle's on {agree} of {n_gen} tokens")
+            agree = check_free_run(res[k]["tokens"], refs[k][1], refs[k][2], band[k], along=refs[k][3])
+            log(f"{name}: segment {k} free run checked on {agree} of {n_gen} tokens")
 
 
 @pytest.mark.parametrize("name,sample", [("small-u8-b64", [5, 40]), ("turbo-u64-q512", [300])])
@@ -160,14 +168,14 @@ def test_continuous_batching_workload(name, sample):
         for k in sample:
             n_gen = segs[k].max_new_tokens
             log(f"{name}: oracle free run of segment {k}, {n_gen} tokens")
-            E_ref, toks_ref, lg_ref = oracle_segment(W, shape, segs[k], n_gen)
+            E_ref, toks_ref, lg_ref, along = oracle_segment(W, shape, segs[k], n_gen)
             ctx.encode([segs[k]], [0])
             E = ctx.debug_copy(binding.T_ENC_OUT, 0, (1500, shape.d))
             assert rel_row_err(E, E_ref).max() < TOL["bf16"]
             got = run_teacher_forced(ctx, [0], {0: toks_ref}, len(segs[k].prompt), n_gen)
             band = check_segment(f"{name} segment {k}", *got[0], toks_ref, lg_ref, TOL["bf16"])
-            agree = check_free_run(res[k]["tokens"], toks_ref, lg_ref, band)
-            log(f"{name}: segment {k} free run agrees with the oracle's on {agree} of {n_gen} tokens")
+            agree = check_free_run(res[k]["tokens"], toks_ref, lg_ref, band, along=along)
+            log(f"{name}: segment {k} free run checked on {agree} of {n_gen} tokens")
         # the same segment alone gives the same tokens (batch invariance)
         k = sample[0]
         solo = ctx.transcribe([segs[k]])[0]
