@@ -1,8 +1,8 @@
 """GPU edge cases against the oracle, through the C ABI: the empty call, the
 shortest and longest segments (1 and 480000 samples), and a decode that
 fills the text context to its last position (4 prompt tokens + 444 new =
-448), for the encoder-decoder and the CTC variant (1 and 1500 frames).
-Tolerances as in test_gpu_parity (fp32 model)."""
+448, in the fp32 and the bf16 model), for the encoder-decoder and the CTC
+variant (1 and 1500 frames). Tolerances as in test_gpu_parity."""
 import sys
 
 import numpy as np
@@ -12,7 +12,8 @@ import oracle
 from oracle import ctc as OC
 from paper_2507_01021_amd import binding, synth
 
-from parity import TOL, check_ctc_entry, check_tokens, drive_teacher_forced, oracle_run, rel_row_err
+from parity import (TOL, check_ctc_entry, check_tokens, drive_teacher_forced, float64_weights, oracle_run,
+                    rel_row_err)
 
 pytestmark = pytest.mark.gpu
 
@@ -72,6 +73,29 @@ def test_decode_to_the_last_text_position(tiny):
     res = ctx.transcribe(segs)
     for r, s in zip(res, segs):
         assert r["tokens"].size == n_new
+
+
+def test_bf16_decode_to_the_last_text_position():
+    """The bf16 decode path (base shape) filled to position 447: the
+    self-attention kernel's P·V over more than 256 cached positions (a
+    second batch of V rows per wave), the cache appends and the head at every
+    position, against the oracle under teacher forcing."""
+    shape = synth.BASE
+    W = synth.make_weights(shape, 0)
+    n_new = shape.n_text_ctx - 4
+    segs = synth.fixed_batch(shape, [64000, 288000], n_new, seed=13)
+    log(f"base: oracle decode of {n_new} tokens for 2 segments")
+    ref = oracle_run(float64_weights(W), shape, segs, n_new=n_new)
+    with binding.Context(synth.pack_blob(W), max_slots=2) as ctx:
+        log(f"base: teacher-forced decode of {n_new} tokens in 2 slots")
+        ctx.encode(segs, [0, 1])
+        toks, lgs = drive_teacher_forced(ctx, [0, 1], segs, ref, n_new)
+        for k in range(2):
+            e = rel_row_err(lgs[k], ref[k]["logits"])
+            strict, near = check_tokens(toks[k], ref[k]["logits"], gpu_logits=lgs[k], min_strict=n_new // 2)
+            log(f"slot {k}: logits rel err max {e.max():.2e} (last position {e[-1]:.2e}), "
+                f"tokens strict {strict} near-tie {near}")
+            assert e.max() < TOL["bf16"]
 
 
 def test_ctc_shortest_and_longest_segments():
