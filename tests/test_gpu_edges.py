@@ -1,8 +1,9 @@
 """GPU edge cases against the oracle, through the C ABI: the empty call, the
-shortest and longest segments (1 and 480000 samples), and a decode that
-fills the text context to its last position (4 prompt tokens + 444 new =
-448, in the fp32 and the bf16 model), for the encoder-decoder and the CTC
-variant (1 and 1500 frames). Tolerances as in test_gpu_parity."""
+shortest and longest segments (1 and 480000 samples), a decode that fills
+the text context to its last position (4 prompt tokens + 444 new = 448, in
+the fp32 and the bf16 model), the model widths no workload uses, for the
+encoder-decoder and the CTC variant (1 and 1500 frames). Tolerances as in
+test_gpu_parity."""
 import sys
 
 import numpy as np
@@ -96,6 +97,31 @@ def test_bf16_decode_to_the_last_text_position():
             log(f"slot {k}: logits rel err max {e.max():.2e} (last position {e[-1]:.2e}), "
                 f"tokens strict {strict} near-tie {near}")
             assert e.max() < TOL["bf16"]
+
+
+@pytest.mark.parametrize("d", [1024, 1536, 2048])
+def test_widths_without_a_workload(d):
+    """Model widths the library accepts that no workload uses (1024 is
+    Whisper medium's, 2048 the largest allowed; with the workloads' 384,
+    512, 768 and 1280 every supported width runs), bf16, one encoder and two
+    decoder layers with the full vocabulary: encoder output, teacher-forced
+    logits and tokens of one segment against the oracle."""
+    shape = synth.BASE.with_(name=f"w{d}", d=d, n_head=d // 64, n_enc=1, n_dec=2)
+    W = synth.make_weights(shape, 0)
+    segs = synth.fixed_batch(shape, [400000], 8, seed=14)
+    log(f"width {d}: oracle")
+    ref = oracle_run(float64_weights(W), shape, segs, n_new=8)
+    with binding.Context(synth.pack_blob(W), max_slots=1) as ctx:
+        log(f"width {d}: encode and teacher-forced decode")
+        ctx.encode(segs, [0])
+        E = ctx.debug_copy(binding.T_ENC_OUT, 0, (1500, d))
+        ee = rel_row_err(E, ref[0]["E"]).max()
+        toks, lgs = drive_teacher_forced(ctx, [0], segs, ref, 8)
+        e = rel_row_err(lgs[0], ref[0]["logits"])
+        strict, near = check_tokens(toks[0], ref[0]["logits"], gpu_logits=lgs[0], min_strict=4)
+        log(f"width {d}: encoder rel err {ee:.2e}, logits rel err max {e.max():.2e}, "
+            f"tokens strict {strict} near-tie {near}")
+        assert ee < TOL["bf16"] and e.max() < TOL["bf16"]
 
 
 def test_ctc_shortest_and_longest_segments():
