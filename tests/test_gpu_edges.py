@@ -1,7 +1,8 @@
 """GPU edge cases against the oracle, through the C ABI: the empty call, the
 shortest and longest segments (1 and 480000 samples), a decode that fills
 the text context to its last position (4 prompt tokens + 444 new = 448, in
-the fp32 and the bf16 model), the model widths no workload uses, for the
+the fp32 and the bf16 model), the model widths and mel channel counts no
+workload uses, for the
 encoder-decoder and the CTC variant (1 and 1500 frames). Tolerances as in
 test_gpu_parity."""
 import sys
@@ -122,6 +123,30 @@ def test_widths_without_a_workload(d):
         log(f"width {d}: encoder rel err {ee:.2e}, logits rel err max {e.max():.2e}, "
             f"tokens strict {strict} near-tie {near}")
         assert ee < TOL["bf16"] and e.max() < TOL["bf16"]
+
+
+@pytest.mark.parametrize("n_mels", [4, 68, 100])
+def test_mel_counts_without_a_workload(n_mels):
+    """Mel channel counts the library accepts besides Whisper's 80 and 128
+    (multiples of 4 up to 128): log-mel features, encoder output and
+    teacher-forced logits of one segment against the oracle (bf16, base
+    width, one encoder and one decoder layer)."""
+    shape = synth.BASE.with_(name=f"m{n_mels}", n_mels=n_mels, n_enc=1, n_dec=1)
+    W = synth.make_weights(shape, 0)
+    segs = synth.fixed_batch(shape, [200000], 6, seed=15)
+    ref = oracle_run(float64_weights(W), shape, segs, n_new=6)
+    with binding.Context(synth.pack_blob(W), max_slots=1) as ctx:
+        log(f"{n_mels} mel channels: encode and teacher-forced decode")
+        ctx.encode(segs, [0])
+        mel = ctx.debug_copy(binding.T_MEL, 0, (n_mels, 3000))
+        me = np.abs(mel - ref[0]["mel"]).max()
+        E = ctx.debug_copy(binding.T_ENC_OUT, 0, (1500, shape.d))
+        ee = rel_row_err(E, ref[0]["E"]).max()
+        toks, lgs = drive_teacher_forced(ctx, [0], segs, ref, 6)
+        e = rel_row_err(lgs[0], ref[0]["logits"]).max()
+        check_tokens(toks[0], ref[0]["logits"], gpu_logits=lgs[0], min_strict=3)
+        log(f"{n_mels} mel channels: mel abs err {me:.1e}, encoder rel err {ee:.2e}, logits rel err {e:.2e}")
+        assert me < 2e-5 and ee < TOL["bf16"] and e < TOL["bf16"]
 
 
 def test_ctc_shortest_and_longest_segments():
