@@ -1,8 +1,8 @@
 """GPU edge cases against the oracle, through the C ABI: the empty call, the
 shortest and longest segments (1 and 480000 samples), a decode that fills
 the text context to its last position (4 prompt tokens + 444 new = 448, in
-the fp32 and the bf16 model), the model widths and mel channel counts no
-workload uses, for the
+the fp32 and the bf16 model), the model widths, mel channel counts and
+small vocabularies no workload uses, for the
 encoder-decoder and the CTC variant (1 and 1500 frames). Tolerances as in
 test_gpu_parity."""
 import sys
@@ -147,6 +147,35 @@ def test_mel_counts_without_a_workload(n_mels):
         check_tokens(toks[0], ref[0]["logits"], gpu_logits=lgs[0], min_strict=3)
         log(f"{n_mels} mel channels: mel abs err {me:.1e}, encoder rel err {ee:.2e}, logits rel err {e:.2e}")
         assert me < 2e-5 and ee < TOL["bf16"] and e < TOL["bf16"]
+
+
+@pytest.mark.parametrize("n_vocab", [1, 33, 1000])
+def test_small_vocabularies(n_vocab):
+    """Decoder vocabularies far below Whisper's, down to a single id (the
+    last 32-id tile of the head ragged or alone): teacher-forced logits and
+    greedy tokens of two segments against the oracle (bf16, base width, one
+    encoder and two decoder layers, prompts of in-range ids)."""
+    shape = synth.BASE.with_(name=f"v{n_vocab}", n_vocab=n_vocab, n_enc=1, n_dec=2)
+    W = synth.make_weights(shape, 0)
+    segs = synth.fixed_batch(shape, [48000, 160000], 8, seed=16)
+    for k, sg in enumerate(segs):
+        sg.prompt = [(3 * k + j) % n_vocab for j in range(3)]
+    ref = oracle_run(float64_weights(W), shape, segs, n_new=8)
+    with binding.Context(synth.pack_blob(W), max_slots=2) as ctx:
+        log(f"vocabulary {n_vocab}: encode and teacher-forced decode")
+        ctx.encode(segs, [0, 1])
+        toks, lgs = drive_teacher_forced(ctx, [0, 1], segs, ref, 8)
+        for k in range(2):
+            e = rel_row_err(lgs[k], ref[k]["logits"]).max()
+            log(f"vocabulary {n_vocab} slot {k}: logits rel err {e:.2e}")
+            assert e < TOL["bf16"]
+            assert np.all((np.asarray(toks[k]) >= 0) & (np.asarray(toks[k]) < n_vocab))
+            if n_vocab > 1:
+                check_tokens(toks[k], ref[k]["logits"], gpu_logits=lgs[k], min_strict=4)
+        res = ctx.transcribe(segs)
+        for r, sg in zip(res, segs):
+            assert r["tokens"].size == sg.max_new_tokens
+            assert np.all((r["tokens"] >= 0) & (r["tokens"] < n_vocab))
 
 
 def test_ctc_shortest_and_longest_segments():
