@@ -1,8 +1,8 @@
 """GPU edge cases against the oracle, through the C ABI: the empty call, the
 shortest and longest segments (1 and 480000 samples), a decode that fills
 the text context to its last position (4 prompt tokens + 444 new = 448, in
-the fp32 and the bf16 model), the model widths, mel channel counts and
-small vocabularies no workload uses, for the
+the fp32 and the bf16 model), the model widths (bf16 and fp32), mel channel
+counts and small vocabularies no workload uses, for the
 encoder-decoder and the CTC variant (1 and 1500 frames). Tolerances as in
 test_gpu_parity."""
 import sys
@@ -123,6 +123,28 @@ def test_widths_without_a_workload(d):
         log(f"width {d}: encoder rel err {ee:.2e}, logits rel err max {e.max():.2e}, "
             f"tokens strict {strict} near-tie {near}")
         assert ee < TOL["bf16"] and e.max() < TOL["bf16"]
+
+
+@pytest.mark.parametrize("d", [512, 1280, 2048])
+def test_fp32_model_widths(d):
+    """The fp32 model (SIMT GEMMs, fp32 caches) beyond the tiny width:
+    encoder output and teacher-forced logits and tokens of one segment
+    against the oracle at the fp32 tolerance (one encoder and two decoder
+    layers, full vocabulary)."""
+    shape = synth.TINY.with_(name=f"f{d}", d=d, n_head=d // 64, n_enc=1, n_dec=2)
+    W = synth.make_weights(shape, 0)
+    segs = synth.fixed_batch(shape, [240000], 8, seed=17)
+    ref = oracle_run(float64_weights(W), shape, segs, n_new=8)
+    with binding.Context(synth.pack_blob(W), max_slots=1) as ctx:
+        log(f"fp32 width {d}: encode and teacher-forced decode")
+        ctx.encode(segs, [0])
+        E = ctx.debug_copy(binding.T_ENC_OUT, 0, (1500, d))
+        ee = rel_row_err(E, ref[0]["E"]).max()
+        toks, lgs = drive_teacher_forced(ctx, [0], segs, ref, 8)
+        e = rel_row_err(lgs[0], ref[0]["logits"]).max()
+        check_tokens(toks[0], ref[0]["logits"], gpu_logits=lgs[0], min_strict=6)
+        log(f"fp32 width {d}: encoder rel err {ee:.2e}, logits rel err {e:.2e}")
+        assert ee < TOL["f32"] and e < TOL["f32"]
 
 
 @pytest.mark.parametrize("n_mels", [4, 68, 100])
