@@ -146,6 +146,37 @@ def test_base_batch_equals_solo_on_gpu(base):
     drain(ctx, [0, 3, 4])
 
 
+def test_base_tokens_independent_of_the_schedule():
+    """Segments are independent units (Section 2.3): the queue's schedule
+    (slots, encoder batch size, refill threshold, queue policy) changes
+    which segments share an encode pass or a decode step, never a token.
+    Eleven bf16 segments of mixed lengths and token counts, transcribed
+    under five schedules, give bit-identical tokens."""
+    shape = synth.BASE.with_(n_enc=2, n_dec=2)
+    W = synth.make_weights(shape, 0)
+    blob = synth.pack_blob(W)
+    segs = synth.uniform_batch(shape, 11, 8, seed=21)
+    for k, sg in enumerate(segs):
+        sg.segment_id = 1000 + k
+        sg.max_new_tokens = 3 + (7 * k) % 13
+        sg.arrival_us = 1000 * ((5 * k) % 11)
+    schedules = [dict(max_slots=11), dict(max_slots=4, max_encode_batch=1),
+                 dict(max_slots=5, max_encode_batch=3, refill_min=2), dict(max_slots=3, max_encode_batch=2),
+                 dict(max_slots=6, refill_min=3, batch_policy=1, step_cost_us=300, max_wait_ms=5)]
+    want = None
+    for sch in schedules:
+        with binding.Context(blob, **sch) as ctx:
+            log(f"base, 11 segments: {sch}")
+            res = ctx.transcribe(segs)
+        for sg, r in zip(segs, res):
+            assert (r["segment_id"], r["status"], r["tokens"].size) == (sg.segment_id, 0, sg.max_new_tokens)
+        if want is None:
+            want = [r["tokens"] for r in res]
+        else:
+            for a, r in zip(want, res):
+                assert np.array_equal(a, r["tokens"])
+
+
 def test_pad_mode_feature_domain_mel():
     shape = synth.TINY.with_(n_enc=1, n_dec=1, n_vocab=500)
     W = synth.make_weights(shape, 0)
